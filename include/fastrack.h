@@ -1,0 +1,129 @@
+/*
+ * fastrack.h -- C ABI of the gfx950 multi-chain AES-256-GCM library.
+ *
+ * The library implements the GPU side of the paper's secure CPU-to-GPU path
+ * (Fastrack, arXiv 2410.15240): authenticated decryption of a transfer with
+ * AES-256-GCM restructured as multi-chaining authentication (section 5.2), the
+ * reverse direction (encrypt + tag), and a chunked host-to-device pipeline that
+ * overlaps PCIe copies with decryption and verification (section 5.3).
+ *
+ * Chains. A buffer of `len` bytes is split into n = ceil(len / chain_bytes)
+ * chains; chain i covers bytes [i*chain_bytes, min(len, (i+1)*chain_bytes)).
+ * Each chain is an independent AES-256-GCM message (SP 800-38D, 96-bit IV,
+ * 128-bit tag) with
+ *     IV_i = base_iv XOR (0^32 || [i]_64)   (chain index big-endian in IV bytes 4..11)
+ *     A_i  = aad[i*aad_bytes .. (i+1)*aad_bytes)
+ * so chain 0 with no AAD is exactly standard GCM under base_iv. Binding the
+ * chain index into the IV (and, if the caller wishes, into the AAD as the
+ * paper's serial number, section 5.4) makes reordered chains fail.
+ *
+ * Pointers. `key` and `base_iv` are HOST pointers (32 and 12 bytes). Names
+ * starting with d_ are DEVICE pointers (e.g. a torch tensor's data_ptr()),
+ * h_ are HOST pointers. d_ct / d_pt must be 16-byte aligned; tags, AAD and ok
+ * arrays have no alignment requirement. The caller allocates and owns every
+ * buffer. The library keeps a small per-(device, key) cache of key-derived
+ * tables (about 0.9 MiB each) and a per-(device, stream) scratch area for
+ * partial GHASH values; fastrack_shutdown() releases both.
+ *
+ * Asynchrony. Calls enqueue work on the given HIP stream (NULL = the null
+ * stream of the current device) and return; results are valid once the stream
+ * has completed that work. `stream` is a hipStream_t passed as void*.
+ *
+ * Errors. The return value is FASTRACK_OK (0) or a negative code; the message
+ * of the last failure on the calling thread is fastrack_last_error(). Argument
+ * checks happen before any work is enqueued. A failed tag is NOT an error: it
+ * sets ok[i] = 0 while the plaintext of that chain is still written (the
+ * paper's eager evaluation uses plaintext before authentication completes and
+ * abandons it on failure, section 5.3).
+ */
+#ifndef FASTRACK_H
+#define FASTRACK_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum fastrack_status {
+    FASTRACK_OK = 0,
+    FASTRACK_EINVAL = -1,      /* invalid argument (see each function) */
+    FASTRACK_EHIP = -2,        /* a HIP runtime call failed */
+    FASTRACK_ENOTPINNED = -3,  /* a host buffer that must be pinned is pageable */
+    FASTRACK_ENOMEM = -4       /* device allocation for the key cache or scratch failed */
+};
+
+/* flags */
+#define FASTRACK_F_SEQ_GHASH 1u  /* the paper's baseline authentication: one sequential
+                                    GHASH chain per tag (section 5.2); same output */
+
+/* Number of chains, ceil(len / chain_bytes); 0 when chain_bytes is 0. */
+uint64_t fastrack_num_chains(uint64_t len, uint64_t chain_bytes);
+
+/*
+ * Decrypt and verify (paper section 5.2: the receiver decrypts with AES-CTR and
+ * regenerates each chain's GMAC tag to compare against the received one).
+ *   d_ct    [len] ciphertext on the device
+ *   d_tags  [n][16] received tags
+ *   d_aad   [n][aad_bytes] per-chain AAD; ignored (may be NULL) when aad_bytes == 0
+ *   d_pt    [len] plaintext out; may equal d_ct exactly (in place), must not
+ *           overlap it otherwise
+ *   d_ok    [n] out: 1 = tag verified, 0 = rejected
+ *   flags   0 or FASTRACK_F_SEQ_GHASH
+ * EINVAL: NULL key/base_iv/d_ct/d_pt/d_tags/d_ok, or NULL d_aad with
+ * aad_bytes > 0; chain_bytes == 0, not a multiple of 16, or above
+ * (2^32 - 2) * 16; d_ct/d_pt not 16-byte aligned or partially overlapping;
+ * more than 2^32 - 1 chains; unknown flags. len == 0 is a successful no-op.
+ */
+int fastrack_gcm_decrypt_verify(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                                const uint8_t *d_ct, uint64_t len, const uint8_t *d_tags,
+                                const uint8_t *d_aad, uint32_t aad_bytes, uint8_t *d_pt, uint8_t *d_ok,
+                                uint32_t flags, void *stream);
+
+/*
+ * Encrypt and tag: the GPU-to-CPU direction (paper section 1.1: the sender
+ * encrypts and generates the MAC tag). Same chain layout and checks as above.
+ *   d_pt    [len] plaintext on the device
+ *   d_ct    [len] ciphertext out; may equal d_pt exactly
+ *   d_tags  [n][16] tags out
+ */
+int fastrack_gcm_encrypt_tag(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                             const uint8_t *d_pt, uint64_t len, const uint8_t *d_aad, uint32_t aad_bytes,
+                             uint8_t *d_ct, uint8_t *d_tags, uint32_t flags, void *stream);
+
+/* Bytes of device staging that fastrack_pipeline_h2d needs for these sizes. */
+uint64_t fastrack_pipeline_stage_bytes(uint64_t len, uint64_t chain_bytes, uint32_t aad_bytes,
+                                       uint64_t chunk_bytes, int depth);
+
+/*
+ * Pipelined host-to-device decrypt + verify (paper section 5.3, decryption
+ * pipeline): ciphertext in a pinned host "bounce buffer" (section 3.1) is
+ * copied in chunks of chunk_bytes on copy_stream into a ring of `depth`
+ * device staging slots, and each chunk's chains are decrypted and verified on
+ * compute_stream while the next chunks are in flight.
+ *   h_ct         [len] ciphertext, PINNED host memory (ENOTPINNED otherwise)
+ *   h_tags       [n][16] host tags; h_aad [n][aad_bytes] host AAD (or NULL)
+ *   chunk_bytes  a nonzero multiple of chain_bytes
+ *   depth        2 or 3
+ *   d_stage      device workspace of stage_bytes >= fastrack_pipeline_stage_bytes(...)
+ *   d_pt, d_ok   device outputs as in fastrack_gcm_decrypt_verify
+ * Results are valid once compute_stream has completed (it waits on the copies).
+ * EINVAL additionally covers chunk_bytes, depth and an undersized d_stage.
+ */
+int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                          const uint8_t *h_ct, uint64_t len, const uint8_t *h_tags, const uint8_t *h_aad,
+                          uint32_t aad_bytes, uint64_t chunk_bytes, int depth, uint8_t *d_stage,
+                          uint64_t stage_bytes, uint8_t *d_pt, uint8_t *d_ok, void *copy_stream,
+                          void *compute_stream);
+
+/* Message of the last failure on this thread ("" if none). */
+const char *fastrack_last_error(void);
+
+/* Release the key-table cache and scratch areas (waits for the device first). */
+void fastrack_shutdown(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FASTRACK_H */

@@ -1,0 +1,170 @@
+"""Python binding of the gfx950 multi-chain AES-256-GCM library (libfastrack.so).
+
+Argument marshalling only: every step of the path runs in the library's HIP
+kernels. PyTorch supplies device memory, pinned host memory and streams. The
+binding raises if the native library is missing; there is no fallback.
+
+Chain layout, IV derivation and error behaviour are documented in
+include/fastrack.h.
+"""
+import ctypes as _ct
+import os as _os
+
+import torch as _torch  # loads the HIP runtime that the library then shares
+
+from . import build as _build
+
+__all__ = ["FastrackError", "decrypt_verify", "encrypt_tag", "pipeline_h2d", "num_chains", "stage_bytes",
+           "shutdown", "library_path", "F_SEQ_GHASH"]
+
+F_SEQ_GHASH = 1
+
+OK, EINVAL, EHIP, ENOTPINNED, ENOMEM = 0, -1, -2, -3, -4
+_NAMES = {EINVAL: "EINVAL", EHIP: "EHIP", ENOTPINNED: "ENOTPINNED", ENOMEM: "ENOMEM"}
+
+
+class FastrackError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__("%s (%d): %s" % (_NAMES.get(code, "error"), code, msg))
+        self.code = code
+
+
+_lib = None
+
+
+def library_path() -> str:
+    return _build.LIB
+
+
+def lib():
+    """The loaded native library. Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not _os.path.exists(_build.LIB):
+            raise RuntimeError("libfastrack.so is not built; run `python -m paper_2410_15240_amd.build` "
+                               "(or __graft_entry__.build())")
+        L = _ct.CDLL(_build.LIB)
+        vp, u8p, u64, u32 = _ct.c_void_p, _ct.c_void_p, _ct.c_uint64, _ct.c_uint32
+        L.fastrack_num_chains.argtypes = [u64, u64]
+        L.fastrack_num_chains.restype = u64
+        L.fastrack_gcm_decrypt_verify.argtypes = [u8p, u8p, u64, u8p, u64, u8p, u8p, u32, u8p, u8p, u32, vp]
+        L.fastrack_gcm_decrypt_verify.restype = _ct.c_int
+        L.fastrack_gcm_encrypt_tag.argtypes = [u8p, u8p, u64, u8p, u64, u8p, u32, u8p, u8p, u32, vp]
+        L.fastrack_gcm_encrypt_tag.restype = _ct.c_int
+        L.fastrack_pipeline_stage_bytes.argtypes = [u64, u64, u32, u64, _ct.c_int]
+        L.fastrack_pipeline_stage_bytes.restype = u64
+        L.fastrack_pipeline_h2d.argtypes = [u8p, u8p, u64, u8p, u64, u8p, u8p, u32, u64, _ct.c_int, u8p, u64, u8p,
+                                            u8p, vp, vp]
+        L.fastrack_pipeline_h2d.restype = _ct.c_int
+        L.fastrack_last_error.restype = _ct.c_char_p
+        L.fastrack_shutdown.restype = None
+        _lib = L
+    return _lib
+
+
+def _check(rc):
+    if rc != OK:
+        raise FastrackError(rc, lib().fastrack_last_error().decode(errors="replace"))
+
+
+def _host_bytes(x, n, what):
+    if isinstance(x, _torch.Tensor):
+        x = x.detach().to("cpu", _torch.uint8).contiguous().numpy().tobytes()
+    elif not isinstance(x, (bytes, bytearray)):
+        x = bytes(memoryview(x).cast("B"))
+    x = bytes(x)
+    if len(x) != n:
+        raise ValueError("%s must be %d bytes, got %d" % (what, n, len(x)))
+    return _ct.create_string_buffer(x, n)
+
+
+def _dptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(s):
+    if s is None:
+        return _torch.cuda.current_stream().cuda_stream
+    return s.cuda_stream if hasattr(s, "cuda_stream") else int(s)
+
+
+def _u8_dev(t, what):
+    if not (isinstance(t, _torch.Tensor) and t.is_cuda and t.dtype == _torch.uint8 and t.is_contiguous()):
+        raise ValueError("%s must be a contiguous uint8 CUDA tensor" % what)
+    return t
+
+
+def num_chains(length, chain_bytes):
+    return int(lib().fastrack_num_chains(length, chain_bytes))
+
+
+def stage_bytes(length, chain_bytes, aad_bytes, chunk_bytes, depth):
+    return int(lib().fastrack_pipeline_stage_bytes(length, chain_bytes, aad_bytes, chunk_bytes, depth))
+
+
+def decrypt_verify(key, base_iv, chain_bytes, ct, tags, aad=None, out=None, ok=None, flags=0, stream=None):
+    """Decrypt + verify every chain of ct (uint8 CUDA tensor). Returns (pt, ok)."""
+    _u8_dev(ct, "ct")
+    n = num_chains(ct.numel(), chain_bytes)
+    _u8_dev(tags, "tags")
+    aad_bytes = 0 if aad is None else aad.numel() // max(n, 1)
+    if aad is not None:
+        _u8_dev(aad, "aad")
+    if out is None:
+        out = _torch.empty_like(ct)
+    if ok is None:
+        ok = _torch.empty(n, dtype=_torch.uint8, device=ct.device)
+    _check(lib().fastrack_gcm_decrypt_verify(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
+                                             chain_bytes, _dptr(ct), ct.numel(), _dptr(tags), _dptr(aad), aad_bytes,
+                                             _dptr(out), _dptr(ok), flags, _stream(stream)))
+    return out, ok
+
+
+def encrypt_tag(key, base_iv, chain_bytes, pt, aad=None, out=None, tags=None, flags=0, stream=None):
+    """Encrypt every chain of pt (uint8 CUDA tensor) and produce its tag. Returns (ct, tags)."""
+    _u8_dev(pt, "pt")
+    n = num_chains(pt.numel(), chain_bytes)
+    aad_bytes = 0 if aad is None else aad.numel() // max(n, 1)
+    if aad is not None:
+        _u8_dev(aad, "aad")
+    if out is None:
+        out = _torch.empty_like(pt)
+    if tags is None:
+        tags = _torch.empty((n, 16), dtype=_torch.uint8, device=pt.device)
+    _check(lib().fastrack_gcm_encrypt_tag(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
+                                          chain_bytes, _dptr(pt), pt.numel(), _dptr(aad), aad_bytes, _dptr(out),
+                                          _dptr(tags), flags, _stream(stream)))
+    return out, tags
+
+
+def pipeline_h2d(key, base_iv, chain_bytes, h_ct, h_tags, h_aad=None, chunk_bytes=8 << 20, depth=2, stage=None,
+                 out=None, ok=None, copy_stream=None, compute_stream=None, device=None):
+    """Chunked H2D copy of pinned ciphertext overlapped with decrypt + verify. Returns (pt, ok) on the device."""
+    if not (isinstance(h_ct, _torch.Tensor) and h_ct.device.type == "cpu" and h_ct.dtype == _torch.uint8):
+        raise ValueError("h_ct must be a uint8 CPU tensor in pinned memory")
+    device = _torch.device("cuda", _torch.cuda.current_device()) if device is None else _torch.device(device)
+    length = h_ct.numel()
+    n = num_chains(length, chain_bytes)
+    aad_bytes = 0 if h_aad is None else h_aad.numel() // max(n, 1)
+    need = stage_bytes(length, chain_bytes, aad_bytes, chunk_bytes, depth)
+    if stage is None:
+        stage = _torch.empty(need, dtype=_torch.uint8, device=device)
+    if out is None:
+        out = _torch.empty(length, dtype=_torch.uint8, device=device)
+    if ok is None:
+        ok = _torch.empty(n, dtype=_torch.uint8, device=device)
+    h_tags = h_tags.contiguous()
+    if h_aad is not None:
+        h_aad = h_aad.contiguous()
+    cs = _stream(copy_stream)
+    ks = _stream(compute_stream)
+    _check(lib().fastrack_pipeline_h2d(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"), chain_bytes,
+                                       h_ct.data_ptr(), length, h_tags.data_ptr(), _dptr(h_aad), aad_bytes,
+                                       chunk_bytes, depth, _dptr(stage), stage.numel(), _dptr(out), _dptr(ok), cs,
+                                       ks))
+    return out, ok
+
+
+def shutdown():
+    if _lib is not None:
+        _lib.fastrack_shutdown()

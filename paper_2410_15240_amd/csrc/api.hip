@@ -1,0 +1,500 @@
+// C ABI of the multi-chain AES-256-GCM library: argument checks, the per-key
+// table cache, per-stream scratch, work planning and the H2D pipeline.
+#include <hip/hip_runtime.h>
+
+#include <array>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "fastrack.h"
+#include "keyctx.h"
+#include "launch.h"
+
+using namespace fastrack;
+
+#define FT_EXPORT extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char *what)
+{
+    return fail(FASTRACK_EHIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr uint64_t kMaxChainBlocks = 0xFFFFFFFEull;   // GCM: at most 2^32 - 2 blocks per message
+constexpr size_t kMaxKeys = 8;
+constexpr int kMinSegLog2 = 8;                          // segments of >= 256 blocks (4 per lane)
+
+struct KeyEntry {
+    int dev;
+    std::array<uint8_t, 32> key;
+    KeyCtx *ctx;
+    hipEvent_t ready;
+    uint64_t last_use;
+};
+
+struct ScratchEntry {
+    int dev;
+    hipStream_t stream;
+    void *ptr;
+    size_t bytes;
+};
+
+struct DevInfo {
+    int dev;
+    int num_cu;
+};
+
+std::mutex g_mu;
+std::vector<KeyEntry> g_keys;
+std::vector<ScratchEntry> g_scratch;
+std::vector<DevInfo> g_dev;
+uint64_t g_tick = 0;
+
+int num_cu_of(int dev, int *out)
+{
+    for (auto &d : g_dev)
+        if (d.dev == dev) {
+            *out = d.num_cu;
+            return FASTRACK_OK;
+        }
+    int n = 0;
+    hipError_t e = hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess)
+        return hip_fail(e, "hipDeviceGetAttribute");
+    g_dev.push_back({dev, n});
+    *out = n;
+    return FASTRACK_OK;
+}
+
+void free_key_entry(KeyEntry &k)
+{
+    (void)hipMemset(k.ctx, 0, sizeof(KeyCtx));   // key-derived material does not outlive the entry
+    (void)hipFree(k.ctx);
+    (void)hipEventDestroy(k.ready);
+}
+
+// Device tables for (current device, key); setup is enqueued on `s` the first time.
+int key_ctx(const uint8_t *key, hipStream_t s, int dev, const KeyCtx **out)
+{
+    std::array<uint8_t, 32> k;
+    std::memcpy(k.data(), key, 32);
+    for (auto &e : g_keys)
+        if (e.dev == dev && e.key == k) {
+            e.last_use = ++g_tick;
+            hipError_t he = hipStreamWaitEvent(s, e.ready, 0);
+            if (he != hipSuccess)
+                return hip_fail(he, "hipStreamWaitEvent");
+            *out = e.ctx;
+            return FASTRACK_OK;
+        }
+    size_t same_dev = 0, victim = g_keys.size();
+    for (size_t i = 0; i < g_keys.size(); ++i)
+        if (g_keys[i].dev == dev) {
+            ++same_dev;
+            if (victim == g_keys.size() || g_keys[i].last_use < g_keys[victim].last_use)
+                victim = i;
+        }
+    if (same_dev >= kMaxKeys) {
+        // Work queued on any stream may still read the victim's tables.
+        hipError_t he = hipDeviceSynchronize();
+        if (he != hipSuccess)
+            return hip_fail(he, "hipDeviceSynchronize");
+        free_key_entry(g_keys[victim]);
+        g_keys.erase(g_keys.begin() + (long)victim);
+    }
+    KeyEntry e;
+    e.dev = dev;
+    e.key = k;
+    e.last_use = ++g_tick;
+    hipError_t he = hipMalloc(reinterpret_cast<void **>(&e.ctx), sizeof(KeyCtx));
+    if (he != hipSuccess)
+        return fail(FASTRACK_ENOMEM, "hipMalloc(%zu) for the key tables: %s", sizeof(KeyCtx), hipGetErrorString(he));
+    uint32_t words[8];
+    for (int i = 0; i < 8; ++i)
+        words[i] = (uint32_t)key[4 * i] | ((uint32_t)key[4 * i + 1] << 8) | ((uint32_t)key[4 * i + 2] << 16) |
+                   ((uint32_t)key[4 * i + 3] << 24);
+    he = launch_key_setup(words, e.ctx, s);
+    std::memset(words, 0, sizeof words);
+    if (he != hipSuccess) {
+        (void)hipFree(e.ctx);
+        return hip_fail(he, "key setup launch");
+    }
+    he = hipEventCreateWithFlags(&e.ready, hipEventDisableTiming);
+    if (he == hipSuccess)
+        he = hipEventRecord(e.ready, s);
+    if (he != hipSuccess) {
+        (void)hipStreamSynchronize(s);
+        (void)hipFree(e.ctx);
+        return hip_fail(he, "hipEventRecord");
+    }
+    g_keys.push_back(e);
+    *out = e.ctx;
+    return FASTRACK_OK;
+}
+
+// Scratch of at least `bytes` private to (device, stream): work on one stream is ordered.
+int scratch_for(int dev, hipStream_t s, size_t bytes, void **out)
+{
+    for (auto &e : g_scratch)
+        if (e.dev == dev && e.stream == s) {
+            if (e.bytes >= bytes) {
+                *out = e.ptr;
+                return FASTRACK_OK;
+            }
+            hipError_t he = hipStreamSynchronize(s);   // earlier launches may still use the old area
+            if (he != hipSuccess)
+                return hip_fail(he, "hipStreamSynchronize");
+            (void)hipFree(e.ptr);
+            e.ptr = nullptr;
+            e.bytes = 0;
+            he = hipMalloc(&e.ptr, bytes);
+            if (he != hipSuccess)
+                return fail(FASTRACK_ENOMEM, "hipMalloc(%zu) for scratch: %s", bytes, hipGetErrorString(he));
+            e.bytes = bytes;
+            *out = e.ptr;
+            return FASTRACK_OK;
+        }
+    ScratchEntry e{dev, s, nullptr, bytes};
+    hipError_t he = hipMalloc(&e.ptr, bytes);
+    if (he != hipSuccess)
+        return fail(FASTRACK_ENOMEM, "hipMalloc(%zu) for scratch: %s", bytes, hipGetErrorString(he));
+    g_scratch.push_back(e);
+    *out = e.ptr;
+    return FASTRACK_OK;
+}
+
+uint32_t ceil_log2(uint64_t x)
+{
+    uint32_t r = 0;
+    while ((1ull << r) < x)
+        ++r;
+    return r;
+}
+
+// Split `len` bytes (chains chain_base ..) into (chain, segment) work items.
+void make_plan(uint64_t len, uint64_t chain_bytes, uint64_t chain_base, int num_cu, GcmLaunch &p)
+{
+    const uint64_t n = (len + chain_bytes - 1) / chain_bytes;
+    const uint64_t qc = chain_bytes / 16;
+    p.chain_bytes = chain_bytes;
+    p.chain_base = chain_base;
+    p.n_chains = (uint32_t)n;
+    p.qc = (uint32_t)qc;
+    p.last_len = len - (n - 1) * chain_bytes;
+    p.q_last = (uint32_t)((p.last_len + 15) / 16);
+    uint32_t lg = ceil_log2(qc);
+    if (lg > 31)
+        lg = 31;
+    const uint64_t target = (uint64_t)num_cu * 16 * 2;   // two items per resident wave
+    while (lg > (uint32_t)kMinSegLog2 && n * ((qc + (1ull << lg) - 1) >> lg) < target)
+        --lg;
+    p.seg_log2 = lg;
+    p.segs_full = (uint32_t)((qc + (1ull << lg) - 1) >> lg);
+    p.segs_last = (uint32_t)((p.q_last + (1ull << lg) - 1) >> lg);
+    p.n_items = (n - 1) * p.segs_full + p.segs_last;
+}
+
+bool overlap_bad(const void *a, const void *b, uint64_t len)
+{
+    uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+    if (x == y)
+        return false;
+    return x < y + len && y < x + len;
+}
+
+int check_common(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes, uint64_t len, const void *in,
+                 const void *out, const void *aad, uint32_t aad_bytes, uint32_t flags)
+{
+    if (!key || !base_iv)
+        return fail(FASTRACK_EINVAL, "key and base_iv must be non-NULL host pointers");
+    if (chain_bytes == 0 || chain_bytes % 16 != 0)
+        return fail(FASTRACK_EINVAL, "chain_bytes must be a nonzero multiple of 16 (got %llu)",
+                    (unsigned long long)chain_bytes);
+    if (chain_bytes / 16 > kMaxChainBlocks)
+        return fail(FASTRACK_EINVAL, "chain_bytes above (2^32-2)*16, the GCM message limit");
+    if (flags & ~FASTRACK_F_SEQ_GHASH)
+        return fail(FASTRACK_EINVAL, "unknown flags 0x%x", flags);
+    if (aad_bytes && !aad)
+        return fail(FASTRACK_EINVAL, "aad is NULL but aad_bytes = %u", aad_bytes);
+    if (len == 0)
+        return FASTRACK_OK;
+    if (!in || !out)
+        return fail(FASTRACK_EINVAL, "input and output buffers must be non-NULL");
+    if (((uintptr_t)in & 15) || ((uintptr_t)out & 15))
+        return fail(FASTRACK_EINVAL, "input and output buffers must be 16-byte aligned");
+    if (overlap_bad(in, out, len))
+        return fail(FASTRACK_EINVAL, "input and output overlap without being the same buffer");
+    if ((len + chain_bytes - 1) / chain_bytes > 0xFFFFFFFFull)
+        return fail(FASTRACK_EINVAL, "more than 2^32-1 chains");
+    return FASTRACK_OK;
+}
+
+void iv_words(const uint8_t *iv, uint32_t w[3])
+{
+    for (int j = 0; j < 3; ++j)
+        w[j] = (uint32_t)iv[4 * j] | ((uint32_t)iv[4 * j + 1] << 8) | ((uint32_t)iv[4 * j + 2] << 16) |
+               ((uint32_t)iv[4 * j + 3] << 24);
+}
+
+// Enqueue one decrypt/encrypt over [in, in+len) covering chains chain_base.. .
+int run_gcm(bool encrypt, const KeyCtx *ctx, const uint8_t *base_iv, uint64_t chain_bytes, uint64_t chain_base,
+            const uint8_t *in, uint64_t len, uint8_t *out, const uint8_t *aad, uint32_t aad_bytes,
+            const uint8_t *tags_in, uint8_t *tags_out, uint8_t *ok, uint32_t flags, int dev, int num_cu,
+            hipStream_t s)
+{
+    GcmLaunch p;
+    std::memset(&p, 0, sizeof p);
+    make_plan(len, chain_bytes, chain_base, num_cu, p);
+    p.ctx = ctx;
+    p.in = in;
+    p.out = out;
+    iv_words(base_iv, p.iv);
+    p.aad = aad;
+    p.aad_bytes = aad_bytes;
+    p.tags_in = tags_in;
+    p.tags_out = tags_out;
+    p.ok = ok;
+    hipError_t he;
+    if (flags & FASTRACK_F_SEQ_GHASH) {
+        p.do_ghash = 0;
+        if (!encrypt) {   // tag over the ciphertext before an in-place decrypt overwrites it
+            he = launch_seq_ghash(p, false, s);
+            if (he != hipSuccess)
+                return hip_fail(he, "sequential GHASH launch");
+        }
+        he = launch_gcm(p, encrypt, num_cu, s);
+        if (he != hipSuccess)
+            return hip_fail(he, "CTR launch");
+        if (encrypt) {
+            he = launch_seq_ghash(p, true, s);
+            if (he != hipSuccess)
+                return hip_fail(he, "sequential GHASH launch");
+        }
+        return FASTRACK_OK;
+    }
+    p.do_ghash = 1;
+    {
+        void *sc = nullptr;
+        int rc = scratch_for(dev, s, (size_t)p.n_items * 16, &sc);
+        if (rc)
+            return rc;
+        p.partials = reinterpret_cast<uint4 *>(sc);
+    }
+    he = launch_gcm(p, encrypt, num_cu, s);
+    if (he != hipSuccess)
+        return hip_fail(he, "GCM launch");
+    return FASTRACK_OK;
+}
+
+int current_device(int *dev, int *ncu)
+{
+    hipError_t he = hipGetDevice(dev);
+    if (he != hipSuccess)
+        return hip_fail(he, "hipGetDevice");
+    return num_cu_of(*dev, ncu);
+}
+
+uint64_t round256(uint64_t x) { return (x + 255) & ~255ull; }
+
+}  // namespace
+
+FT_EXPORT uint64_t fastrack_num_chains(uint64_t len, uint64_t chain_bytes)
+{
+    return chain_bytes ? (len + chain_bytes - 1) / chain_bytes : 0;
+}
+
+FT_EXPORT const char *fastrack_last_error(void) { return g_err.c_str(); }
+
+FT_EXPORT int fastrack_gcm_decrypt_verify(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                                          const uint8_t *d_ct, uint64_t len, const uint8_t *d_tags,
+                                          const uint8_t *d_aad, uint32_t aad_bytes, uint8_t *d_pt, uint8_t *d_ok,
+                                          uint32_t flags, void *stream)
+{
+    g_err.clear();
+    int rc = check_common(key, base_iv, chain_bytes, len, d_ct, d_pt, d_aad, aad_bytes, flags);
+    if (rc || len == 0)
+        return rc;
+    if (!d_tags || !d_ok)
+        return fail(FASTRACK_EINVAL, "d_tags and d_ok must be non-NULL");
+    std::lock_guard<std::mutex> lk(g_mu);
+    int dev, ncu;
+    if ((rc = current_device(&dev, &ncu)))
+        return rc;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const KeyCtx *ctx;
+    if ((rc = key_ctx(key, s, dev, &ctx)))
+        return rc;
+    return run_gcm(false, ctx, base_iv, chain_bytes, 0, d_ct, len, d_pt, aad_bytes ? d_aad : nullptr, aad_bytes,
+                   d_tags, nullptr, d_ok, flags, dev, ncu, s);
+}
+
+FT_EXPORT int fastrack_gcm_encrypt_tag(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                                       const uint8_t *d_pt, uint64_t len, const uint8_t *d_aad, uint32_t aad_bytes,
+                                       uint8_t *d_ct, uint8_t *d_tags, uint32_t flags, void *stream)
+{
+    g_err.clear();
+    int rc = check_common(key, base_iv, chain_bytes, len, d_pt, d_ct, d_aad, aad_bytes, flags);
+    if (rc || len == 0)
+        return rc;
+    if (!d_tags)
+        return fail(FASTRACK_EINVAL, "d_tags must be non-NULL");
+    std::lock_guard<std::mutex> lk(g_mu);
+    int dev, ncu;
+    if ((rc = current_device(&dev, &ncu)))
+        return rc;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const KeyCtx *ctx;
+    if ((rc = key_ctx(key, s, dev, &ctx)))
+        return rc;
+    return run_gcm(true, ctx, base_iv, chain_bytes, 0, d_pt, len, d_ct, aad_bytes ? d_aad : nullptr, aad_bytes,
+                   nullptr, d_tags, nullptr, flags, dev, ncu, s);
+}
+
+FT_EXPORT uint64_t fastrack_pipeline_stage_bytes(uint64_t len, uint64_t chain_bytes, uint32_t aad_bytes,
+                                                 uint64_t chunk_bytes, int depth)
+{
+    if (chain_bytes == 0 || depth < 1)
+        return 0;
+    const uint64_t n = (len + chain_bytes - 1) / chain_bytes;
+    return (uint64_t)depth * round256(chunk_bytes) + round256(16 * n) + round256((uint64_t)aad_bytes * n);
+}
+
+FT_EXPORT int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                                    const uint8_t *h_ct, uint64_t len, const uint8_t *h_tags, const uint8_t *h_aad,
+                                    uint32_t aad_bytes, uint64_t chunk_bytes, int depth, uint8_t *d_stage,
+                                    uint64_t stage_bytes, uint8_t *d_pt, uint8_t *d_ok, void *copy_stream,
+                                    void *compute_stream)
+{
+    g_err.clear();
+    int rc = check_common(key, base_iv, chain_bytes, len, h_ct, d_pt, h_aad, aad_bytes, 0);
+    if (rc || len == 0)
+        return rc;
+    if (!h_tags || !d_ok || !d_stage)
+        return fail(FASTRACK_EINVAL, "h_tags, d_ok and d_stage must be non-NULL");
+    if (chunk_bytes == 0 || chunk_bytes % chain_bytes != 0)
+        return fail(FASTRACK_EINVAL, "chunk_bytes must be a nonzero multiple of chain_bytes");
+    if (depth != 2 && depth != 3)
+        return fail(FASTRACK_EINVAL, "depth must be 2 or 3");
+    if ((uintptr_t)d_stage & 255)
+        return fail(FASTRACK_EINVAL, "d_stage must be 256-byte aligned");
+    const uint64_t need = fastrack_pipeline_stage_bytes(len, chain_bytes, aad_bytes, chunk_bytes, depth);
+    if (stage_bytes < need)
+        return fail(FASTRACK_EINVAL, "d_stage holds %llu bytes, the pipeline needs %llu",
+                    (unsigned long long)stage_bytes, (unsigned long long)need);
+
+    hipPointerAttribute_t attr;
+    hipError_t he = hipPointerGetAttributes(&attr, h_ct);
+    if (he != hipSuccess || attr.type != hipMemoryTypeHost) {
+        (void)hipGetLastError();
+        return fail(FASTRACK_ENOTPINNED, "h_ct is not pinned host memory");
+    }
+
+    std::lock_guard<std::mutex> lk(g_mu);
+    int dev, ncu;
+    if ((rc = current_device(&dev, &ncu)))
+        return rc;
+    hipStream_t cs = reinterpret_cast<hipStream_t>(copy_stream);
+    hipStream_t ks = reinterpret_cast<hipStream_t>(compute_stream);
+    const KeyCtx *ctx;
+    if ((rc = key_ctx(key, ks, dev, &ctx)))
+        return rc;
+
+    const uint64_t n = (len + chain_bytes - 1) / chain_bytes;
+    const uint64_t slot_bytes = round256(chunk_bytes);
+    uint8_t *d_tags = d_stage + (uint64_t)depth * slot_bytes;
+    uint8_t *d_aad = d_tags + round256(16 * n);
+
+    std::vector<hipEvent_t> ev;
+    auto cleanup = [&]() {
+        for (auto e : ev)
+            (void)hipEventDestroy(e);
+    };
+    for (int i = 0; i < 2 * depth + 1; ++i) {
+        hipEvent_t e;
+        he = hipEventCreateWithFlags(&e, hipEventDisableTiming);
+        if (he != hipSuccess) {
+            cleanup();
+            return hip_fail(he, "hipEventCreate");
+        }
+        ev.push_back(e);
+    }
+    hipEvent_t meta = ev[0];
+    hipEvent_t *copied = &ev[1], *freed = &ev[1 + depth];
+
+    he = hipMemcpyAsync(d_tags, h_tags, 16 * n, hipMemcpyHostToDevice, cs);
+    if (he == hipSuccess && aad_bytes)
+        he = hipMemcpyAsync(d_aad, h_aad, (size_t)aad_bytes * n, hipMemcpyHostToDevice, cs);
+    if (he == hipSuccess)
+        he = hipEventRecord(meta, cs);
+    if (he == hipSuccess)
+        he = hipStreamWaitEvent(ks, meta, 0);
+    if (he != hipSuccess) {
+        cleanup();
+        return hip_fail(he, "pipeline tag/AAD upload");
+    }
+    const uint64_t nchunks = (len + chunk_bytes - 1) / chunk_bytes;
+    const uint64_t cpc = chunk_bytes / chain_bytes;
+    for (uint64_t k = 0; k < nchunks; ++k) {
+        const int slot = (int)(k % (uint64_t)depth);
+        const uint64_t off = k * chunk_bytes;
+        const uint64_t bytes = len - off < chunk_bytes ? len - off : chunk_bytes;
+        uint8_t *stage = d_stage + (uint64_t)slot * slot_bytes;
+        if (k >= (uint64_t)depth)
+            he = hipStreamWaitEvent(cs, freed[slot], 0);   // the slot's previous chunk has been decrypted
+        if (he == hipSuccess)
+            he = hipMemcpyAsync(stage, h_ct + off, bytes, hipMemcpyHostToDevice, cs);
+        if (he == hipSuccess)
+            he = hipEventRecord(copied[slot], cs);
+        if (he == hipSuccess)
+            he = hipStreamWaitEvent(ks, copied[slot], 0);
+        if (he != hipSuccess) {
+            cleanup();
+            return hip_fail(he, "pipeline copy");
+        }
+        rc = run_gcm(false, ctx, base_iv, chain_bytes, k * cpc, stage, bytes, d_pt + off, aad_bytes ? d_aad : nullptr,
+                     aad_bytes, d_tags, nullptr, d_ok, 0, dev, ncu, ks);
+        if (rc) {
+            cleanup();
+            return rc;
+        }
+        he = hipEventRecord(freed[slot], ks);
+        if (he != hipSuccess) {
+            cleanup();
+            return hip_fail(he, "hipEventRecord");
+        }
+    }
+    cleanup();
+    return FASTRACK_OK;
+}
+
+FT_EXPORT void fastrack_shutdown(void)
+{
+    std::lock_guard<std::mutex> lk(g_mu);
+    if (g_keys.empty() && g_scratch.empty())
+        return;
+    (void)hipDeviceSynchronize();
+    for (auto &k : g_keys)
+        free_key_entry(k);
+    g_keys.clear();
+    for (auto &s : g_scratch)
+        (void)hipFree(s.ptr);
+    g_scratch.clear();
+}

@@ -1,0 +1,144 @@
+// GF(2^128) arithmetic of GCM on the device.
+//
+// GHASH multiplies by the hash subkey H in GF(2^128) with the reduction
+// polynomial x^128 + x^7 + x^2 + x + 1; the bit of degree 0 is the most
+// significant bit of the first byte (SP 800-38D 6.3; the paper's Galois-field
+// authentication, section 3.2). A multiplication by a FIXED element Y is a
+// GF(2)-linear map, so it is evaluated with precomputed positional tables:
+// X . Y = XOR over positions p of table[p][digit_p(X)], which needs no carries
+// and no carry-less multiply instruction (CDNA has none).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "keyctx.h"
+
+namespace fastrack {
+
+struct u4 {
+    uint32_t w[4];
+};
+
+__device__ __forceinline__ uint32_t xor3(uint32_t a, uint32_t b, uint32_t c)
+{
+    return __builtin_amdgcn_bitop3_b32(a, b, c, 0x96);
+}
+
+__device__ __forceinline__ uint32_t bswap32(uint32_t x)
+{
+    return __builtin_amdgcn_perm(0u, x, 0x00010203u);
+}
+
+// ---- big-endian-word helpers (setup only) -------------------------------
+// In big-endian-word form w[0] bit 31 is degree 0 and w[3] bit 0 is degree 127.
+
+__device__ __forceinline__ u4 to_be(const u4 &a)
+{
+    u4 r;
+    for (int j = 0; j < 4; ++j)
+        r.w[j] = bswap32(a.w[j]);
+    return r;
+}
+
+__device__ __forceinline__ u4 from_be(const u4 &a) { return to_be(a); }
+
+// Y . x^k for 0 <= k <= 64, in big-endian-word form. Multiplying by x^k moves
+// every coefficient k degrees up (k bits toward the end of the string). The k
+// bits that pass degree 127 form F(x) . x^128, and x^128 = 1 + x + x^2 + x^7,
+// so they come back as F xor F.x xor F.x^2 xor F.x^7. For k <= 64, F has
+// degree < 64 and the fold cannot overflow again.
+__device__ inline u4 be_mul_xk(const u4 &y, int k)
+{
+    if (k == 0)
+        return y;
+    // 128-bit value v = w0:w1:w2:w3 (w0 most significant as an integer).
+    uint64_t hi = ((uint64_t)y.w[0] << 32) | y.w[1];
+    uint64_t lo = ((uint64_t)y.w[2] << 32) | y.w[3];
+    uint64_t nhi, nlo, f;
+    if (k < 64) {
+        f = lo << (64 - k);               // the k bits that fall off, left-aligned
+        nlo = (lo >> k) | (hi << (64 - k));
+        nhi = hi >> k;
+    } else {                              // k == 64
+        f = lo;
+        nlo = hi;
+        nhi = 0;
+    }
+    // f holds F left-aligned in a 64-bit word: degree d of F sits at bit 63-d,
+    // which is exactly where degree d lives in the high word. Fold F.(1+x+x^2+x^7).
+    uint64_t r_hi = f ^ (f >> 1) ^ (f >> 2) ^ (f >> 7);
+    uint64_t r_lo = (f << 63) ^ (f << 62) ^ (f << 57);
+    nhi ^= r_hi;
+    nlo ^= r_lo;
+    u4 r;
+    r.w[0] = (uint32_t)(nhi >> 32);
+    r.w[1] = (uint32_t)nhi;
+    r.w[2] = (uint32_t)(nlo >> 32);
+    r.w[3] = (uint32_t)nlo;
+    return r;
+}
+
+// Y . x^k for 0 <= k <= 127 (two steps of at most 64).
+__device__ inline u4 be_mul_xk_any(const u4 &y, int k)
+{
+    if (k <= 64)
+        return be_mul_xk(y, k);
+    return be_mul_xk(be_mul_xk(y, 64), k - 64);
+}
+
+// ---- little-endian-word table multiplies -------------------------------
+
+// X . Y with Y's 4-bit positional table. Word j holds bytes 4j..4j+3, and
+// byte 4j+b holds nibble positions 8j+2b (high nibble) and 8j+2b+1 (low).
+// Register indices stay compile-time constants so nothing is spilled to memory.
+__device__ inline u4 mul_tab4(const u4 &x, const Tab4 *__restrict__ t)
+{
+    u4 z = {{0u, 0u, 0u, 0u}};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const uint32_t w = x.w[j];
+#pragma unroll 2
+        for (int b = 0; b < 4; ++b) {
+            const uint32_t byte = (w >> (8 * b)) & 0xFFu;
+            const int p = 8 * j + 2 * b;
+            const uint4 ea = *reinterpret_cast<const uint4 *>(t->e[p][byte >> 4]);
+            const uint4 eb = *reinterpret_cast<const uint4 *>(t->e[p + 1][byte & 0xFu]);
+            z.w[0] = xor3(z.w[0], ea.x, eb.x);
+            z.w[1] = xor3(z.w[1], ea.y, eb.y);
+            z.w[2] = xor3(z.w[2], ea.z, eb.z);
+            z.w[3] = xor3(z.w[3], ea.w, eb.w);
+        }
+    }
+    return z;
+}
+
+// X . H^e for 0 <= e < 2^32 using the squares tables H^(2^t).
+__device__ inline u4 mul_hpow(u4 x, uint32_t e, const KeyCtx *__restrict__ c)
+{
+    while (e) {
+        int t = __builtin_ctz(e);
+        x = mul_tab4(x, &c->sq_tab[t]);
+        e &= e - 1;
+    }
+    return x;
+}
+
+__device__ __forceinline__ u4 xor4(const u4 &a, const u4 &b)
+{
+    u4 r;
+    for (int j = 0; j < 4; ++j)
+        r.w[j] = a.w[j] ^ b.w[j];
+    return r;
+}
+
+// XOR of a value over the 64 lanes of a wave; every lane receives the result.
+__device__ inline u4 wave_xor(u4 v)
+{
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1)
+        for (int j = 0; j < 4; ++j)
+            v.w[j] ^= __shfl_xor(v.w[j], off, 64);
+    return v;
+}
+
+}  // namespace fastrack

@@ -1,0 +1,544 @@
+// gfx950 kernels for multi-chain AES-256-GCM (the paper's section 5.2,
+// "Multi-chaining authentication", and its GPU decryption / authentication
+// kernels of section 5.2-5.3).
+//
+//   key_setup_kernel   once per key: S-box, T0, round keys, H = AES_K(0),
+//                      powers of H and the GF(2^128) multiplication tables.
+//   gcm_kernel<ENC>    the streaming hot path: AES-256-CTR keystream XOR the
+//                      data (section 3.2, AES-CTR) fused with GHASH over the
+//                      ciphertext, parallel INSIDE each chain.
+//   finalize_kernel    combines the per-segment GHASH partials of chains that
+//                      were split over several waves, then tags / verifies.
+//   seq_ghash_kernel   the paper's baseline authentication: one sequential
+//                      Horner chain per tag (kept for comparison).
+//
+// GHASH inside a chain (GHASH definition: SP 800-38D 6.4; the paper's GMAC
+// chain, section 3.2). For blocks X_1..X_m, GHASH = sum_j X_j . H^(m-j+1).
+// A wave of 64 lanes takes 64 consecutive blocks per iteration (lane l gets
+// block 64k + l, so loads are one coalesced 1 KiB access per wave). Each lane
+// runs its own Horner chain with the fixed multiplier H^64:
+//     acc_l <- acc_l . H^64  xor  X_(64k+l)
+// and at the end of its segment the lanes are combined as
+//     G = sum_l acc_l . H^(64-l)
+// (lane l's last block has 63-l blocks after it). A segment shorter than a
+// multiple of 64 is padded with zero blocks at its START, which leaves GHASH
+// unchanged. Segments are aligned to the end of the chain, so segment s of S
+// carries the weight H^((S-1-s) . 2^seg_log2) when the chain is assembled.
+// With G_C = GHASH over the ciphertext blocks of a chain and q their number,
+//     S = (GHASH(A) . H^q  xor  G_C  xor  [len A]_64 || [len C]_64) . H,
+//     T = S xor AES_K(J0),   J0 = IV_i || 0^31 || 1.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "aes_dev.h"
+#include "gf128_dev.h"
+#include "keyctx.h"
+#include "launch.h"
+
+namespace fastrack {
+
+// ===========================================================================
+// Key setup
+// ===========================================================================
+
+struct SetupArgs {
+    uint32_t key[8];
+};
+
+// Entry p of the 4-bit positional table of y (little-endian form): the 16
+// multiples (nibble v at degrees 4p..4p+3) . y, v's bit 3 being degree 4p.
+__device__ inline void build_tab4_row(const u4 &y, int p, Tab4 *out)
+{
+    u4 b0 = be_mul_xk_any(to_be(y), 4 * p);
+    u4 b1 = be_mul_xk(b0, 1), b2 = be_mul_xk(b1, 1), b3 = be_mul_xk(b2, 1);
+    for (int v = 0; v < 16; ++v) {
+        u4 e = {{0u, 0u, 0u, 0u}};
+        if (v & 8) e = xor4(e, b0);
+        if (v & 4) e = xor4(e, b1);
+        if (v & 2) e = xor4(e, b2);
+        if (v & 1) e = xor4(e, b3);
+        u4 le = from_be(e);
+        for (int j = 0; j < 4; ++j)
+            out->e[p][v][j] = le.w[j];
+    }
+}
+
+__global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__restrict__ ctx)
+{
+    __shared__ uint32_t s_sbox[256];
+    __shared__ uint32_t s_t0[256];
+    __shared__ uint32_t s_rk[60];
+    __shared__ u4 s_hp[kMaxPow + 1];
+    __shared__ u4 s_hsq[kSquares];
+    __shared__ u4 s_basis[128];
+    __shared__ Tab4 s_tab;
+    const int tid = threadIdx.x;
+
+    if (tid < 256) {
+        uint32_t s = sbox_entry(tid);
+        s_sbox[tid] = s;
+        ctx->sbox[tid] = (uint8_t)s;
+        uint32_t t = t0_entry(s);
+        s_t0[tid] = t;
+        ctx->t0[tid] = t;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        uint32_t rk[60];
+        expand_key_256(a.key, rk, [&](uint32_t x) { return s_sbox[x]; });
+        for (int i = 0; i < 60; ++i) {
+            s_rk[i] = rk[i];
+            ctx->rk[i] = rk[i];
+        }
+    }
+    __syncthreads();
+    if (tid == 0) {
+        u4 zero = {{0u, 0u, 0u, 0u}};
+        u4 h = aes256_encrypt_tt(zero, s_rk, [&](uint32_t x) { return s_t0[x]; });
+        u4 one = {{0x80u, 0u, 0u, 0u}};   // the block 0x80 || 0^120 is 1
+        s_hp[0] = one;
+        s_hp[1] = h;
+        for (int j = 0; j < 4; ++j)
+            ctx->h[j] = h.w[j];
+    }
+    __syncthreads();
+
+    // Powers H^1..H^64 by doubling: with a table for H^(2^r), H^(2^r + j) = H^j . H^(2^r).
+    for (int r = 0; r < 6; ++r) {
+        const int half = 1 << r;
+        if (tid < kTab4Pos)
+            build_tab4_row(s_hp[half], tid, &s_tab);
+        __syncthreads();
+        if (tid < half)
+            s_hp[half + tid + 1] = mul_tab4(s_hp[tid + 1], &s_tab);
+        __syncthreads();
+    }
+    // Squares H^(2^t): t <= 6 are already powers; the rest by repeated squaring.
+    if (tid <= 6)
+        s_hsq[tid] = s_hp[1 << tid];
+    __syncthreads();
+    for (int t = 7; t < kSquares; ++t) {
+        if (tid < kTab4Pos)
+            build_tab4_row(s_hsq[t - 1], tid, &s_tab);
+        __syncthreads();
+        if (tid == 0)
+            s_hsq[t] = mul_tab4(s_hsq[t - 1], &s_tab);
+        __syncthreads();
+    }
+    for (int i = tid; i <= kMaxPow; i += blockDim.x)
+        for (int j = 0; j < 4; ++j)
+            ctx->hp[i][j] = s_hp[i].w[j];
+    for (int i = tid; i < kSquares; i += blockDim.x)
+        for (int j = 0; j < 4; ++j)
+            ctx->hsq[i][j] = s_hsq[i].w[j];
+
+    // 4-bit tables of every H^e (e = 1..64) and every H^(2^t).
+    for (int task = tid; task < (kMaxPow + kSquares) * kTab4Pos; task += blockDim.x) {
+        int tbl = task / kTab4Pos, p = task % kTab4Pos;
+        if (tbl < kMaxPow)
+            build_tab4_row(s_hp[tbl + 1], p, &ctx->pow_tab[tbl]);
+        else
+            build_tab4_row(s_hsq[tbl - kMaxPow], p, &ctx->sq_tab[tbl - kMaxPow]);
+    }
+
+    // 8-bit positional table of H^64: g8[k][v] = (byte v at byte k) . H^64, v's bit 7 = degree 8k.
+    if (tid < 128)
+        s_basis[tid] = be_mul_xk_any(to_be(s_hp[kMaxPow]), tid);
+    __syncthreads();
+    for (int ent = tid; ent < 16 * 256; ent += blockDim.x) {
+        int k = ent >> 8, v = ent & 255;
+        u4 e = {{0u, 0u, 0u, 0u}};
+        for (int b = 0; b < 8; ++b)
+            if (v & (0x80 >> b))
+                e = xor4(e, s_basis[8 * k + b]);
+        u4 le = from_be(e);
+        for (int j = 0; j < 4; ++j)
+            ctx->g8[k][v][j] = le.w[j];
+    }
+}
+
+hipError_t launch_key_setup(const uint32_t key_words[8], KeyCtx *ctx, hipStream_t s)
+{
+    SetupArgs a;
+    for (int i = 0; i < 8; ++i)
+        a.key[i] = key_words[i];
+    hipLaunchKernelGGL(key_setup_kernel, dim3(1), dim3(1024), 0, s, a, ctx);
+    return hipGetLastError();
+}
+
+// ===========================================================================
+// Shared per-chain pieces
+// ===========================================================================
+
+__device__ __forceinline__ u4 zero4()
+{
+    u4 z = {{0u, 0u, 0u, 0u}};
+    return z;
+}
+
+// Little-endian word form of the 96-bit IV of global chain i:
+// base_IV xor (0^32 || [i]_64), the index big-endian in IV bytes 4..11.
+__device__ __forceinline__ void chain_iv(const GcmLaunch &p, uint64_t gchain, uint32_t iv[3])
+{
+    iv[0] = p.iv[0];
+    iv[1] = p.iv[1] ^ bswap32((uint32_t)(gchain >> 32));
+    iv[2] = p.iv[2] ^ bswap32((uint32_t)gchain);
+}
+
+// Load n (<= 16) bytes as a zero-padded block (constant register indices only).
+__device__ inline u4 load_bytes(const uint8_t *src, uint32_t n)
+{
+    u4 r = zero4();
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+            if ((uint32_t)(4 * j + b) < n)
+                r.w[j] |= (uint32_t)src[4 * j + b] << (8 * b);
+    return r;
+}
+
+__device__ inline void store_bytes(uint8_t *dst, const u4 &v, uint32_t n)
+{
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+            if ((uint32_t)(4 * j + b) < n)
+                dst[4 * j + b] = (uint8_t)(v.w[j] >> (8 * b));
+}
+
+// Tag of one chain from G_C (computed redundantly by the lanes of one wave;
+// lane 0 writes). T(x) returns T0[x] for the J0 encryption.
+template <bool ENC, class LK>
+__device__ inline void chain_finalize(const GcmLaunch &p, uint32_t chain_local, u4 gc, LK T)
+{
+    const KeyCtx *c = p.ctx;
+    const uint64_t gchain = p.chain_base + chain_local;
+    const bool last = chain_local == p.n_chains - 1;
+    const uint64_t len_i = last ? p.last_len : p.chain_bytes;
+    const uint32_t q = last ? p.q_last : p.qc;
+
+    u4 y = zero4();
+    if (p.aad_bytes) {
+        const uint8_t *a = p.aad + gchain * p.aad_bytes;
+        for (uint32_t off = 0; off < p.aad_bytes; off += 16) {
+            uint32_t n = p.aad_bytes - off < 16 ? p.aad_bytes - off : 16;
+            y = mul_tab4(xor4(y, load_bytes(a + off, n)), &c->pow_tab[0]);
+        }
+        y = mul_hpow(y, q, c);
+    }
+    y = xor4(y, gc);
+    const uint64_t abits = (uint64_t)p.aad_bytes * 8, cbits = len_i * 8;
+    u4 lens = {{bswap32((uint32_t)(abits >> 32)), bswap32((uint32_t)abits), bswap32((uint32_t)(cbits >> 32)),
+                bswap32((uint32_t)cbits)}};
+    y = mul_tab4(xor4(y, lens), &c->pow_tab[0]);
+
+    uint32_t iv[3];
+    chain_iv(p, gchain, iv);
+    u4 j0 = {{iv[0], iv[1], iv[2], bswap32(1u)}};
+    u4 e = aes256_encrypt_tt(j0, c->rk, T);
+    u4 tag = xor4(y, e);
+    if ((threadIdx.x & 63) == 0) {
+        if (ENC) {
+            store_bytes(p.tags_out + 16 * gchain, tag, 16);
+        } else {
+            u4 got = load_bytes(p.tags_in + 16 * gchain, 16);
+            uint32_t d = (got.w[0] ^ tag.w[0]) | (got.w[1] ^ tag.w[1]) | (got.w[2] ^ tag.w[2]) | (got.w[3] ^ tag.w[3]);
+            p.ok[gchain] = d == 0 ? 1 : 0;
+        }
+    }
+}
+
+// Position of an item: chain, and the block range [b, e) of its segment.
+struct ItemPos {
+    uint32_t chain, s, S, q, b, e;
+};
+
+__device__ __forceinline__ ItemPos item_pos(const GcmLaunch &p, uint64_t item)
+{
+    ItemPos r;
+    r.chain = (uint32_t)(item / p.segs_full);
+    r.s = (uint32_t)(item - (uint64_t)r.chain * p.segs_full);
+    const bool last = r.chain == p.n_chains - 1;
+    r.q = last ? p.q_last : p.qc;
+    r.S = last ? p.segs_last : p.segs_full;
+    r.e = r.q - ((r.S - 1 - r.s) << p.seg_log2);
+    r.b = r.s == 0 ? 0u : r.e - (1u << p.seg_log2);
+    return r;
+}
+
+// ===========================================================================
+// The streaming kernel
+// ===========================================================================
+//
+// LDS layout (128 KiB, one workgroup per CU):
+//   [0, 64 KiB)        g8: the 8-bit table of H^64, entry (k, v) at (k*256 + v)*16
+//   [64 KiB, 128 KiB)  T0 replicated 64 times: T0[x] for lane l at 64 KiB + x*256 + l*4,
+//                      so every lane reads its own bank and lookups never conflict.
+// A T0 address is built with one v_perm_b32: byte 0 = lane*4, byte 1 = the state
+// byte, byte 2 = 1 (the 64 KiB base), byte 3 = 0.
+
+constexpr int kThreads = 1024;
+constexpr int kWavesPerWg = kThreads / 64;
+constexpr uint32_t kLdsBytes = 128 * 1024;
+
+#define FT_SEL(k) (0x0C020400u + ((uint32_t)(k) << 8))
+
+__device__ __forceinline__ uint32_t tlk(const char *lds, uint32_t word, uint32_t lanec, uint32_t sel)
+{
+    return *reinterpret_cast<const uint32_t *>(lds + __builtin_amdgcn_perm(word, lanec, sel));
+}
+
+// A uniform value held in a VGPR: the 60 round-key words stay resident in
+// vector registers (the kernel has room for them) instead of overflowing the
+// scalar register file.
+__device__ __forceinline__ uint32_t in_vgpr(uint32_t x)
+{
+    uint32_t r;
+    asm("v_mov_b32 %0, %1" : "=v"(r) : "s"(x));
+    return r;
+}
+
+template <bool ENC>
+__global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
+{
+    // Static, so its LDS address is a compile-time constant and a v_perm result
+    // can be used as the ds_read address with no further add.
+    __shared__ uint4 lds4[kLdsBytes / 16];
+    const char *lds = reinterpret_cast<const char *>(lds4);
+    const int tid = threadIdx.x;
+    const uint32_t lane = tid & 63;
+    const KeyCtx *__restrict__ c = p.ctx;
+
+    {
+        uint32_t *t = reinterpret_cast<uint32_t *>(lds4) + 16384;
+        for (int i = tid; i < 16384; i += kThreads)
+            t[i] = c->t0[i >> 6];
+        if (p.do_ghash) {
+            const uint4 *g = reinterpret_cast<const uint4 *>(c->g8);
+            for (int i = tid; i < 4096; i += kThreads)
+                lds4[i] = g[i];
+        }
+    }
+    __syncthreads();
+
+    const uint32_t lanec = 0x10000u | (lane << 2);
+    uint32_t rk[60];
+#pragma unroll
+    for (int i = 0; i < 60; ++i)
+        rk[i] = in_vgpr(__builtin_amdgcn_readfirstlane(c->rk[i]));
+
+    const uint64_t nwaves = (uint64_t)gridDim.x * kWavesPerWg;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerWg + (tid >> 6));
+    for (uint64_t item = wave; item < p.n_items; item += nwaves) {
+        const ItemPos ip = item_pos(p, item);
+        const uint64_t gchain = p.chain_base + ip.chain;
+        uint32_t iv[3];
+        chain_iv(p, gchain, iv);
+        const uint32_t c0 = iv[0] ^ rk[0], c1 = iv[1] ^ rk[1], c2 = iv[2] ^ rk[2];
+        const uint8_t *src = p.in + (uint64_t)ip.chain * p.chain_bytes;
+        uint8_t *dst = p.out + (uint64_t)ip.chain * p.chain_bytes;
+        const bool last_chain = ip.chain == p.n_chains - 1;
+        const uint32_t tail = last_chain ? (uint32_t)(p.last_len & 15) : 0u;   // bytes of a final partial block
+        const uint32_t nblk = ip.e - ip.b;
+        const uint32_t K = (nblk + 63) >> 6;
+        const int pad = (int)((K << 6) - nblk);
+
+        u4 acc = zero4();
+        for (uint32_t k = 0; k < K; ++k) {
+            const int v = (int)(k << 6) + (int)lane - pad;
+            const bool active = v >= 0;
+            const uint32_t t = ip.b + (uint32_t)v;                 // block index inside the chain
+            const bool partial = active && tail != 0 && t == ip.q - 1;
+            u4 d = zero4();
+            if (active) {
+                if (!partial) {
+                    const uint4 x = reinterpret_cast<const uint4 *>(src)[t];
+                    d.w[0] = x.x; d.w[1] = x.y; d.w[2] = x.z; d.w[3] = x.w;
+                } else {
+                    d = load_bytes(src + 16ull * t, tail);
+                }
+            }
+            // Counter block IV_i || [t + 2]_32 (data blocks start at inc32(J0)).
+            uint32_t s0 = c0, s1 = c1, s2 = c2, s3 = bswap32(t + 2u) ^ rk[3];
+#pragma unroll
+            for (int r = 1; r < 14; ++r) {
+                const uint32_t n0 = xor3(tlk(lds, s0, lanec, FT_SEL(0)), rotl32(tlk(lds, s1, lanec, FT_SEL(1)), 8),
+                                         xor3(rotl32(tlk(lds, s2, lanec, FT_SEL(2)), 16),
+                                              rotl32(tlk(lds, s3, lanec, FT_SEL(3)), 24), rk[4 * r + 0]));
+                const uint32_t n1 = xor3(tlk(lds, s1, lanec, FT_SEL(0)), rotl32(tlk(lds, s2, lanec, FT_SEL(1)), 8),
+                                         xor3(rotl32(tlk(lds, s3, lanec, FT_SEL(2)), 16),
+                                              rotl32(tlk(lds, s0, lanec, FT_SEL(3)), 24), rk[4 * r + 1]));
+                const uint32_t n2 = xor3(tlk(lds, s2, lanec, FT_SEL(0)), rotl32(tlk(lds, s3, lanec, FT_SEL(1)), 8),
+                                         xor3(rotl32(tlk(lds, s0, lanec, FT_SEL(2)), 16),
+                                              rotl32(tlk(lds, s1, lanec, FT_SEL(3)), 24), rk[4 * r + 2]));
+                const uint32_t n3 = xor3(tlk(lds, s3, lanec, FT_SEL(0)), rotl32(tlk(lds, s0, lanec, FT_SEL(1)), 8),
+                                         xor3(rotl32(tlk(lds, s1, lanec, FT_SEL(2)), 16),
+                                              rotl32(tlk(lds, s2, lanec, FT_SEL(3)), 24), rk[4 * r + 3]));
+                s0 = n0; s1 = n1; s2 = n2; s3 = n3;
+            }
+            // Final round: S(x) is byte 1 of T0[x]; assemble four of them with v_perm.
+            u4 o;
+            {
+                const uint32_t st[4] = {s0, s1, s2, s3};
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const uint32_t a0 = tlk(lds, st[j], lanec, FT_SEL(0));
+                    const uint32_t a1 = tlk(lds, st[(j + 1) & 3], lanec, FT_SEL(1));
+                    const uint32_t a2 = tlk(lds, st[(j + 2) & 3], lanec, FT_SEL(2));
+                    const uint32_t a3 = tlk(lds, st[(j + 3) & 3], lanec, FT_SEL(3));
+                    const uint32_t lo = __builtin_amdgcn_perm(a1, a0, 0x0C0C0501u);
+                    const uint32_t hi = __builtin_amdgcn_perm(a3, a2, 0x05010C0Cu);
+                    o.w[j] = xor3(lo, hi, rk[56 + j] ^ d.w[j]);
+                }
+            }
+            if (active) {
+                if (!partial) {
+                    reinterpret_cast<uint4 *>(dst)[t] = make_uint4(o.w[0], o.w[1], o.w[2], o.w[3]);
+                } else {
+                    store_bytes(dst + 16ull * t, o, tail);
+                }
+            }
+            if (p.do_ghash) {
+                u4 g = ENC ? o : d;
+                if (ENC) {
+                    if (!active) {
+                        g = zero4();
+                    } else if (partial) {                     // GHASH sees the ciphertext zero-padded
+                        for (int j = 0; j < 4; ++j) {
+                            const int nb = (int)tail - 4 * j;
+                            const uint32_t m = nb >= 4 ? 0xFFFFFFFFu : (nb <= 0 ? 0u : ((1u << (8 * nb)) - 1u));
+                            g.w[j] &= m;
+                        }
+                    }
+                }
+                if (k == 0) {
+                    acc = g;
+                } else {
+                    // acc <- acc . H^64 xor g, 16 lookups into the 8-bit table.
+                    u4 z = g;
+#pragma unroll
+                    for (int kb = 0; kb < 16; kb += 2) {
+                        const uint32_t ba = (acc.w[kb >> 2] >> (8 * (kb & 3))) & 0xFFu;
+                        const uint32_t bb = (acc.w[(kb + 1) >> 2] >> (8 * ((kb + 1) & 3))) & 0xFFu;
+                        const uint4 ea = lds4[(kb << 8) | ba];
+                        const uint4 eb = lds4[((kb + 1) << 8) | bb];
+                        z.w[0] = xor3(z.w[0], ea.x, eb.x);
+                        z.w[1] = xor3(z.w[1], ea.y, eb.y);
+                        z.w[2] = xor3(z.w[2], ea.z, eb.z);
+                        z.w[3] = xor3(z.w[3], ea.w, eb.w);
+                    }
+                    acc = z;
+                }
+            }
+        }
+        if (p.do_ghash) {
+            // Lane l's Horner chain carries weight H^(64-l) within the segment.
+            acc = mul_tab4(acc, &c->pow_tab[63 - lane]);
+            const u4 g = wave_xor(acc);
+            if (lane == 0)
+                p.partials[item] = make_uint4(g.w[0], g.w[1], g.w[2], g.w[3]);
+        }
+    }
+}
+
+// One wave per chain: fold the segment partials of chains split over several waves.
+template <bool ENC>
+__global__ __launch_bounds__(256) void finalize_kernel(GcmLaunch p)
+{
+    const uint32_t chain = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const uint32_t lane = threadIdx.x & 63;
+    if (chain >= p.n_chains)
+        return;
+    const KeyCtx *__restrict__ c = p.ctx;
+    const bool last = chain == p.n_chains - 1;
+    const uint32_t S = last ? p.segs_last : p.segs_full;
+    u4 acc = zero4();
+    for (uint32_t s = lane; s < S; s += 64) {
+        const uint4 g = p.partials[(uint64_t)chain * p.segs_full + s];
+        u4 gv = {{g.x, g.y, g.z, g.w}};
+        acc = xor4(acc, mul_hpow(gv, (S - 1 - s) << p.seg_log2, c));
+    }
+    const u4 gc = wave_xor(acc);
+    chain_finalize<ENC>(p, chain, gc, [&](uint32_t x) { return c->t0[x]; });
+}
+
+// The paper's baseline authentication: one thread per chain, Horner with H over
+// A, then every ciphertext block in order, then the length block.
+template <bool ENC>
+__global__ __launch_bounds__(256) void seq_ghash_kernel(GcmLaunch p)
+{
+    const uint32_t chain = blockIdx.x * blockDim.x + threadIdx.x;
+    if (chain >= p.n_chains)
+        return;
+    const KeyCtx *__restrict__ c = p.ctx;
+    const uint64_t gchain = p.chain_base + chain;
+    const bool last = chain == p.n_chains - 1;
+    const uint64_t len_i = last ? p.last_len : p.chain_bytes;
+    const Tab4 *hT = &c->pow_tab[0];
+    u4 y = zero4();
+    const uint8_t *a = p.aad + gchain * p.aad_bytes;
+    for (uint32_t off = 0; off < p.aad_bytes; off += 16) {
+        uint32_t n = p.aad_bytes - off < 16 ? p.aad_bytes - off : 16;
+        y = mul_tab4(xor4(y, load_bytes(a + off, n)), hT);
+    }
+    const uint8_t *ct = (ENC ? p.out : p.in) + (uint64_t)chain * p.chain_bytes;
+    const uint64_t whole = len_i / 16;
+    for (uint64_t t = 0; t < whole; ++t) {
+        const uint4 x = reinterpret_cast<const uint4 *>(ct)[t];
+        u4 xv = {{x.x, x.y, x.z, x.w}};
+        y = mul_tab4(xor4(y, xv), hT);
+    }
+    if (len_i & 15)
+        y = mul_tab4(xor4(y, load_bytes(ct + 16 * whole, (uint32_t)(len_i & 15))), hT);
+    const uint64_t abits = (uint64_t)p.aad_bytes * 8, cbits = len_i * 8;
+    u4 lens = {{bswap32((uint32_t)(abits >> 32)), bswap32((uint32_t)abits), bswap32((uint32_t)(cbits >> 32)),
+                bswap32((uint32_t)cbits)}};
+    y = mul_tab4(xor4(y, lens), hT);
+    uint32_t iv[3];
+    chain_iv(p, gchain, iv);
+    u4 j0 = {{iv[0], iv[1], iv[2], bswap32(1u)}};
+    u4 tag = xor4(y, aes256_encrypt_tt(j0, c->rk, [&](uint32_t x) { return c->t0[x]; }));
+    if (ENC) {
+        store_bytes(p.tags_out + 16 * gchain, tag, 16);
+    } else {
+        u4 got = load_bytes(p.tags_in + 16 * gchain, 16);
+        uint32_t d = (got.w[0] ^ tag.w[0]) | (got.w[1] ^ tag.w[1]) | (got.w[2] ^ tag.w[2]) | (got.w[3] ^ tag.w[3]);
+        p.ok[gchain] = d == 0 ? 1 : 0;
+    }
+}
+
+hipError_t launch_gcm(const GcmLaunch &p, bool encrypt, int num_cu, hipStream_t s)
+{
+    if (p.n_items == 0)
+        return hipSuccess;
+    uint64_t wgs = (p.n_items + kWavesPerWg - 1) / kWavesPerWg;
+    if (wgs > (uint64_t)num_cu)
+        wgs = (uint64_t)num_cu;
+    if (encrypt)
+        hipLaunchKernelGGL(gcm_kernel<true>, dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+    else
+        hipLaunchKernelGGL(gcm_kernel<false>, dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || !p.do_ghash)
+        return e;
+    const uint32_t fwgs = (p.n_chains + 3) / 4;
+    if (encrypt)
+        hipLaunchKernelGGL(finalize_kernel<true>, dim3(fwgs), dim3(256), 0, s, p);
+    else
+        hipLaunchKernelGGL(finalize_kernel<false>, dim3(fwgs), dim3(256), 0, s, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_seq_ghash(const GcmLaunch &p, bool encrypt, hipStream_t s)
+{
+    const uint32_t wgs = (p.n_chains + 255) / 256;
+    if (encrypt)
+        hipLaunchKernelGGL(seq_ghash_kernel<true>, dim3(wgs), dim3(256), 0, s, p);
+    else
+        hipLaunchKernelGGL(seq_ghash_kernel<false>, dim3(wgs), dim3(256), 0, s, p);
+    return hipGetLastError();
+}
+
+}  // namespace fastrack

@@ -1,0 +1,41 @@
+// Per-key device context for multi-chain AES-256-GCM on gfx950.
+//
+// One KeyCtx lives in device memory per (device, key). It is produced by the
+// setup kernel and read by every decrypt/encrypt launch for that key.
+//
+// Data layout conventions (shared by every kernel in this library):
+//   * A 16-byte block is held as 4 little-endian u32 words exactly as a
+//     16-byte-aligned vector load returns them: word j = bytes 4j..4j+3 with
+//     byte 4j in bits 0..7. AES state column j is word j (row r in bits 8r..).
+//   * GF(2^128) elements use the same little-endian-word form for storage,
+//     table lookups and XOR. Only the shift-based routines used during setup
+//     switch to a big-endian-word form (GCM's bit 0, the coefficient of x^0,
+//     is the most significant bit of byte 0).
+//   * Round key rk[4r + j] is column j of round key r in the same word form.
+#pragma once
+#include <stdint.h>
+
+namespace fastrack {
+
+constexpr int kTab4Pos = 32;    // nibble positions of a 128-bit operand
+constexpr int kTab4Ent = 16;    // values of a nibble
+constexpr int kMaxPow = 64;     // lane-combine powers H^1 .. H^64 (one wave of 64 lanes)
+constexpr int kSquares = 32;    // H^(2^t), t = 0..31 (chains are < 2^32 blocks)
+
+struct Tab4 {                   // 4-bit positional multiplication table of a fixed Y:
+    uint32_t e[kTab4Pos][kTab4Ent][4];   // e[p][v] = (nibble v at degrees 4p..4p+3) . Y
+};
+
+struct KeyCtx {
+    uint32_t rk[60];            // AES-256 round keys (FIPS-197 key expansion)
+    uint32_t t0[256];           // T0[x] = {02}S(x) | S(x)<<8 | S(x)<<16 | {03}S(x)<<24
+    uint8_t sbox[256];
+    uint32_t h[4];              // H = AES_K(0^128)
+    uint32_t hp[kMaxPow + 1][4];      // hp[e] = H^e, e = 0..64 (hp[0] = 1)
+    uint32_t hsq[kSquares][4];        // hsq[t] = H^(2^t)
+    Tab4 pow_tab[kMaxPow];      // pow_tab[e-1]: table of H^e, e = 1..64
+    Tab4 sq_tab[kSquares];      // sq_tab[t]: table of H^(2^t)
+    uint32_t g8[16][256][4];    // 8-bit positional table of H^64: g8[k][v] = (byte v at byte k) . H^64
+};
+
+}  // namespace fastrack

@@ -1,0 +1,42 @@
+// Host-side launch interface between the C ABI (api.hip) and the kernels
+// (kernels.hip). Internal to the library.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "keyctx.h"
+
+namespace fastrack {
+
+// One launch of the streaming kernel over `n_chains` consecutive chains.
+// The work is split into items (chain, segment); a segment is a run of
+// 2^seg_log2 blocks aligned to the END of its chain (segment 0 may be short).
+struct GcmLaunch {
+    const KeyCtx *ctx;
+    const uint8_t *in;          // 16-byte aligned; chain 0 of this launch starts here
+    uint8_t *out;               // 16-byte aligned; may equal `in`
+    uint64_t chain_bytes;       // multiple of 16
+    uint64_t last_len;          // bytes in the last chain of this launch (1..chain_bytes)
+    uint64_t chain_base;        // global index of chain 0 (IV, tag, AAD and ok indexing)
+    uint64_t n_items;
+    uint32_t n_chains;
+    uint32_t qc;                // blocks in a full chain
+    uint32_t q_last;            // blocks in the last chain (a partial block counts as one)
+    uint32_t seg_log2;
+    uint32_t segs_full;         // segments of a full chain
+    uint32_t segs_last;         // segments of the last chain
+    uint32_t iv[3];             // base IV as little-endian words
+    uint32_t aad_bytes;
+    const uint8_t *aad;         // global chain i's AAD at aad + i * aad_bytes
+    const uint8_t *tags_in;     // decrypt: received tags, global chain i at tags_in + 16 i
+    uint8_t *tags_out;          // encrypt: produced tags
+    uint8_t *ok;                // decrypt: ok[global chain] = 1 accept / 0 reject
+    uint4 *partials;            // per-item GHASH partials when a chain has several segments
+    uint32_t do_ghash;          // 0: keystream only (the sequential-GHASH variant tags separately)
+};
+
+hipError_t launch_key_setup(const uint32_t key_words[8], KeyCtx *ctx, hipStream_t s);
+hipError_t launch_gcm(const GcmLaunch &p, bool encrypt, int num_cu, hipStream_t s);
+hipError_t launch_seq_ghash(const GcmLaunch &p, bool encrypt, hipStream_t s);
+
+}  // namespace fastrack

@@ -1,0 +1,111 @@
+"""The C ABI without a GPU: the library loads, exports every declared symbol,
+and rejects invalid arguments before any HIP call is made."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fastrack.h")
+
+
+@pytest.fixture(scope="module")
+def L():
+    import paper_2410_15240_amd as F
+    if not os.path.exists(F.library_path()):
+        from paper_2410_15240_amd import build
+        build.build()
+    return F.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^[A-Za-z_][\w \t\*]*?\b(fastrack_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for want in ("fastrack_gcm_decrypt_verify", "fastrack_gcm_encrypt_tag", "fastrack_pipeline_h2d",
+                 "fastrack_num_chains", "fastrack_last_error", "fastrack_shutdown", "fastrack_pipeline_stage_bytes"):
+        assert want in names
+
+
+def test_library_exports_every_declared_symbol(L):
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_num_chains_and_stage_bytes(L):
+    assert L.fastrack_num_chains(0, 16) == 0
+    assert L.fastrack_num_chains(1, 16) == 1
+    assert L.fastrack_num_chains(1 << 20, 65536) == 16
+    assert L.fastrack_num_chains(1 << 20, 1 << 20) == 1
+    assert L.fastrack_num_chains((1 << 20) + 1, 1 << 20) == 2
+    assert L.fastrack_num_chains(100, 0) == 0
+    n = 4096
+    assert L.fastrack_pipeline_stage_bytes(4 << 30, 1 << 20, 0, 8 << 20, 2) == 2 * (8 << 20) + 16 * n
+    assert L.fastrack_pipeline_stage_bytes(4 << 30, 1 << 20, 32, 8 << 20, 3) == 3 * (8 << 20) + 16 * n + 32 * n
+
+
+KEY = ctypes.create_string_buffer(32)
+IV = ctypes.create_string_buffer(12)
+A = 0x10000  # fake, 16-byte aligned "device" addresses: never dereferenced on these paths
+B = 0x90000
+
+
+def dec(L, chain=4096, ct=A, length=65536, tags=B + 0x100000, aad=None, abytes=0, pt=B, ok=B + 0x200000, flags=0,
+        key=KEY, iv=IV):
+    return L.fastrack_gcm_decrypt_verify(key, iv, chain, ct, length, tags, aad, abytes, pt, ok, flags, None)
+
+
+def enc(L, chain=4096, pt=A, length=65536, aad=None, abytes=0, ct=B, tags=B + 0x100000, flags=0):
+    return L.fastrack_gcm_encrypt_tag(KEY, IV, chain, pt, length, aad, abytes, ct, tags, flags, None)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(chain=0), dict(chain=24), dict(chain=(1 << 32) * 16),
+    dict(key=None), dict(iv=None),
+    dict(ct=None), dict(pt=None), dict(tags=None), dict(ok=None),
+    dict(ct=A + 8), dict(pt=B + 4),
+    dict(pt=A + 16),                       # partial overlap of input and output
+    dict(abytes=32, aad=None),
+    dict(flags=2),
+])
+def test_decrypt_rejects_bad_arguments(L, kw):
+    L.fastrack_last_error.restype = ctypes.c_char_p
+    assert dec(L, **kw) == -1
+    assert L.fastrack_last_error()
+
+
+@pytest.mark.parametrize("kw", [dict(chain=0), dict(tags=None), dict(ct=A + 32), dict(pt=A + 1), dict(flags=8)])
+def test_encrypt_rejects_bad_arguments(L, kw):
+    assert enc(L, **kw) == -1
+
+
+def test_zero_length_is_a_no_op(L):
+    assert dec(L, length=0) == 0
+    assert enc(L, length=0) == 0
+
+
+def pipe(L, chain=1 << 20, length=16 << 20, chunk=8 << 20, depth=2, stage=0x100000000, stage_bytes=None,
+         h_ct=0x20000, h_tags=0x40000):
+    if stage_bytes is None:
+        stage_bytes = L.fastrack_pipeline_stage_bytes(length, chain, 0, chunk, depth)
+    return L.fastrack_pipeline_h2d(KEY, IV, chain, h_ct, length, h_tags, None, 0, chunk, depth, stage,
+                                   stage_bytes, 0x300000000, 0x400000000, None, None)
+
+
+@pytest.mark.parametrize("kw", [dict(depth=1), dict(depth=4), dict(chunk=(8 << 20) + 16), dict(chunk=0),
+                                dict(stage_bytes=1024), dict(stage=0x100000010), dict(stage=None),
+                                dict(h_tags=None)])
+def test_pipeline_rejects_bad_arguments(L, kw):
+    assert pipe(L, **kw) == -1
+
+
+def test_binding_fails_loudly_without_the_library(monkeypatch):
+    import paper_2410_15240_amd as F
+    monkeypatch.setattr(F._build, "LIB", "/nonexistent/libfastrack.so")
+    monkeypatch.setattr(F, "_lib", None)
+    with pytest.raises(RuntimeError):
+        F.lib()
