@@ -1,0 +1,294 @@
+"""Benchmark of the multi-chain AES-256-GCM hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--skip-pipeline] [--skip-cpu]
+
+A timed step is one decrypt + verify pass of the 64 MiB image batch
+(256x3x224x224 uint8, zero-padded, 32-byte AAD per chain) at each of the chain
+sizes 4 KiB, 16 KiB, 64 KiB, 256 KiB and 1 MiB, with every input already
+resident in HBM. `value` is the payload decrypted per second over the whole
+timed region (GB/s, 1e9 bytes). Outside the timed region the script also
+measures encrypt + tag (256 MiB fp32 gradients, 256 KiB chains), the
+sequential-GHASH baseline against the multi-chain path (1 MiB buffer), the
+pipelined 4 GiB host-to-device decrypt against a plain pinned copy, and the
+CPU oracle on the host cores. One JSON line is printed.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0            # MI355X HBM3E peak
+# Integer VALU peak: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (one 32-bit op per lane per clock).
+ALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
+# Algorithmic 32-bit integer operations per 16-byte block of decrypt + verify in
+# the T-table formulation (derivation in the design doc): AES-256 rounds 1-13 at 16
+# table lookups + 16 XORs each, the final round at 16 S-box lookups + 16 byte
+# merges/XORs, the initial AddRoundKey (4), the data XOR (4), the counter (1),
+# and one GF(2^128) multiply by a fixed element through 8-bit tables
+# (16 lookups + 64 XORs).
+ALG_OPS_PER_BLOCK = 13 * 32 + 32 + 4 + 4 + 1 + 16 + 64
+
+KiB, MiB, GiB = 1024, 1 << 20, 1 << 30
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--skip-pipeline", action="store_true")
+    ap.add_argument("--skip-cpu", action="store_true")
+    ap.add_argument("--skip-extras", action="store_true", help="only the timed decrypt sweep")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU: the path is per-GPU and shards by whole chains with no exchange "
+              "(see DESIGN.md); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2410_15240_amd as F
+    import workloads as W
+
+    if not os.path.exists(F.library_path()):
+        from paper_2410_15240_amd import build
+        build.build()
+    F.lib()
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+
+    # ---------------- inputs (config: image batch, chain sweep) ----------------
+    w = W.config2()
+    payload = torch.from_numpy(w.payload).to(dev)
+    L = payload.numel()
+    cases = []
+    for chain in w.chain_sizes:
+        aad = torch.from_numpy(w.aad(chain)).to(dev)
+        ct, tags = F.encrypt_tag(w.key, w.base_iv, chain, payload, aad)
+        out = torch.empty_like(ct)
+        ok = torch.empty(tags.shape[0], dtype=torch.uint8, device=dev)
+        cases.append((chain, ct, tags, aad, out, ok))
+    torch.cuda.synchronize()
+
+    def step(evs=None):
+        for i, (chain, ct, tags, aad, out, ok) in enumerate(cases):
+            if evs is not None:
+                evs[i][0].record(stream)
+            F.decrypt_verify(w.key, w.base_iv, chain, ct, tags, aad, out=out, ok=ok)
+            if evs is not None:
+                evs[i][1].record(stream)
+
+    log("warmup", args.warmup)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    per = [[] for _ in cases]
+    ev_all = [[[torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)] for _ in cases]
+              for _ in range(args.steps)]
+    t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    log("timed steps", args.steps)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for s in range(args.steps):
+        step(ev_all[s])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t_start.elapsed_time(t_end)
+    for s in range(args.steps):
+        for i in range(len(cases)):
+            per[i].append(ev_all[s][i][0].elapsed_time(ev_all[s][i][1]))
+    for chain, ct, tags, aad, out, ok in cases:
+        assert bool(ok.all()), "benchmark decrypt rejected a chain"
+        assert torch.equal(out, payload), "benchmark decrypt produced wrong plaintext"
+    ms_per_step = total_ms / args.steps
+    value = len(cases) * L / (ms_per_step * 1e-3) / 1e9
+    sweep = {}
+    alg_bytes = []
+    for i, (chain, ct, tags, aad, out, ok) in enumerate(cases):
+        n = tags.shape[0]
+        ms = float(np.median(per[i]))
+        sweep["%dKiB" % (chain // KiB)] = {"gbps": round(L / (ms * 1e-3) / 1e9, 1), "us": round(ms * 1e3, 1),
+                                           "chains": n}
+        alg_bytes.append(2 * L + n * (16 + 32 + 1))   # payload in + out, tags, AAD, ok flags
+    launch_ms = float(np.mean([np.mean(p) for p in per]))
+    bytes_per_launch = float(np.mean(alg_bytes))
+    blocks = L // 16
+    achieved_tops = blocks * ALG_OPS_PER_BLOCK / (launch_ms * 1e-3) / 1e12
+    hbm_gbs = bytes_per_launch / (launch_ms * 1e-3) / 1e9
+    log("decrypt sweep %.1f GB/s, %.3f ms/step" % (value, ms_per_step))
+
+    result = {
+        "metric": "AES-256-GCM decrypt+verify GB/s vs chain size; % HBM peak; pipelined H2D GB/s",
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "wall_s": round(wall, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u8",
+        "data": "synthetic (seeded uint8 image batch, zero-padded; see workloads/)",
+        "config": {"workload": "image-batch-64MiB: 256x3x224x224 uint8 zero-padded to 64 MiB, decrypt+verify at "
+                               "chain sizes 4K/16K/64K/256K/1M, 32-byte AAD per chain",
+                   "bytes_per_step": len(cases) * L, "parallelism": "single GPU"},
+        "sweep": sweep,
+        "roofline": {"bound": "alu", "achieved": round(achieved_tops, 2), "peak": round(ALU_PEAK_TOPS, 2),
+                     "unit": "Tops/s", "frac": round(achieved_tops / ALU_PEAK_TOPS, 3), "traffic": None,
+                     "kernel": "gcm_kernel<decrypt> (+ per-chain finalize)",
+                     "alg_ops_per_block": ALG_OPS_PER_BLOCK, "launch_us": round(launch_ms * 1e3, 2)},
+        "hbm": {"achieved": round(hbm_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(hbm_gbs / HBM_PEAK_GBS, 3), "alg_bytes_per_launch": int(bytes_per_launch)},
+    }
+
+    if not args.skip_extras:
+        result.update(extras(F, W, torch, np, dev, stream, args))
+    if not args.skip_cpu:
+        result["cpu_baseline"] = cpu_baseline(W, np, cases, w)
+    print(json.dumps(result), flush=True)
+
+
+def time_calls(torch, stream, fn, reps):
+    fn()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(reps):
+        fn()
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / reps
+
+
+def extras(F, W, torch, np, dev, stream, args):
+    res = {}
+    # encrypt + tag: fp32 gradients, 256 KiB chains
+    w4 = W.config4()
+    pt4 = torch.from_numpy(w4.payload).to(dev)
+    c4 = w4.chain_sizes[0]
+    out4 = torch.empty_like(pt4)
+    tags4 = torch.empty((F.num_chains(pt4.numel(), c4), 16), dtype=torch.uint8, device=dev)
+    ms = time_calls(torch, stream, lambda: F.encrypt_tag(w4.key, w4.base_iv, c4, pt4, out=out4, tags=tags4), 20)
+    res["encrypt_tag"] = {"workload": "fp32-gradients-256MiB, 256 KiB chains", "gbps": round(pt4.numel() / ms / 1e6, 1),
+                          "us": round(ms * 1e3, 1)}
+    log("encrypt+tag %.1f GB/s" % res["encrypt_tag"]["gbps"])
+    del pt4, out4, tags4
+
+    # the paper's sequential GHASH vs multi-chain, 1 MiB buffer
+    w1 = W.config1()
+    p1 = torch.from_numpy(w1.payload).to(dev)
+    seq = {}
+    for chain in w1.chain_sizes:
+        ct1, tg1 = F.encrypt_tag(w1.key, w1.base_iv, chain, p1)
+        o1 = torch.empty_like(ct1)
+        k1 = torch.empty(tg1.shape[0], dtype=torch.uint8, device=dev)
+        for name, flags in (("multi_chain", 0), ("sequential_ghash", F.F_SEQ_GHASH)):
+            ms = time_calls(torch, stream, lambda: F.decrypt_verify(w1.key, w1.base_iv, chain, ct1, tg1, out=o1,
+                                                                   ok=k1, flags=flags), 50)
+            assert bool(k1.all())
+            seq["%s_%dKiB" % (name, chain // KiB)] = {"us": round(ms * 1e3, 1),
+                                                      "gbps": round(p1.numel() / ms / 1e6, 2)}
+    res["config1_1MiB"] = seq
+    log("1 MiB:", seq)
+
+    # per-key setup (first call with a new key)
+    key2 = bytes(range(32))
+    t = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ct1, tg1 = F.encrypt_tag(w1.key, w1.base_iv, 65536, p1)
+    torch.cuda.synchronize()
+    t[0].record(stream)
+    F.decrypt_verify(key2, w1.base_iv, 65536, ct1, tg1)
+    t[1].record(stream)
+    torch.cuda.synchronize()
+    res["cold_key_call_us"] = round(t[0].elapsed_time(t[1]) * 1e3, 1)
+
+    if not args.skip_pipeline:
+        res["pipeline_h2d"] = pipeline(F, W, torch, np, dev)
+    return res
+
+
+def pipeline(F, W, torch, np, dev):
+    length, chain, chunk = 4 * GiB, MiB, 8 * MiB
+    rng = W.rng_for(5)
+    key, iv = W.draw_key_iv(rng)
+    # Seeded bytes (a 64 MiB random block tiled), encrypted on the GPU: the bench
+    # times the path; correctness of this path is established by the tests.
+    block = torch.from_numpy(np.frombuffer(rng.bytes(64 * MiB), np.uint8).copy())
+    h_ct = torch.empty(length, dtype=torch.uint8, pin_memory=True)
+    n = F.num_chains(length, chain)
+    h_tags = torch.empty((n, 16), dtype=torch.uint8)
+    d_pt = block.to(dev).repeat(length // block.numel())
+    d_ct, d_tags = F.encrypt_tag(key, iv, chain, d_pt)
+    h_ct.copy_(d_ct)
+    h_tags.copy_(d_tags)
+    del d_ct, d_tags
+    torch.cuda.synchronize()
+    res = {"workload": "uniform-4GiB (seeded 64 MiB block tiled), 1 MiB chains, 8 MiB chunks"}
+    stage = torch.empty(F.stage_bytes(length, chain, 0, chunk, 3), dtype=torch.uint8, device=dev)
+    out = torch.empty(length, dtype=torch.uint8, device=dev)
+    ok = torch.empty(n, dtype=torch.uint8, device=dev)
+    cs, ks = torch.cuda.Stream(), torch.cuda.Stream()
+    for depth in (2, 3):
+        F.pipeline_h2d(key, iv, chain, h_ct, h_tags, None, chunk, depth, stage, out, ok, cs, ks)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        F.pipeline_h2d(key, iv, chain, h_ct, h_tags, None, chunk, depth, stage, out, ok, cs, ks)
+        ks.synchronize()
+        cs.synchronize()
+        dt = time.perf_counter() - t0
+        assert bool(ok.all()) and torch.equal(out, d_pt), "pipeline produced wrong output"
+        res["depth%d_gbps" % depth] = round(length / dt / 1e9, 2)
+        log("pipeline depth %d: %.2f GB/s" % (depth, length / dt / 1e9))
+    # plain pinned copy of the same bytes in the same chunks on one stream
+    with torch.cuda.stream(cs):
+        for rep in range(2):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for off in range(0, length, chunk):
+                out[off:off + chunk].copy_(h_ct[off:off + chunk], non_blocking=True)
+            cs.synchronize()
+            dt = time.perf_counter() - t0
+    res["pinned_copy_gbps"] = round(length / dt / 1e9, 2)
+    best = max(res["depth2_gbps"], res["depth3_gbps"])
+    res["ratio_vs_copy"] = round(best / res["pinned_copy_gbps"], 3)
+    log("pinned copy %.2f GB/s" % res["pinned_copy_gbps"])
+    del stage, out, ok, h_ct, d_pt
+    torch.cuda.empty_cache()
+    return res
+
+
+def cpu_baseline(W, np, cases, w):
+    import oracle
+    # the oracle decrypts the same image batch at every chain size of the sweep
+    total = 0
+    t0 = time.perf_counter()
+    for chain, ct, tags, aad, out, ok in cases:
+        c = ct.cpu().numpy()
+        t = tags.cpu().numpy()
+        a = aad.cpu().numpy()
+        s = time.perf_counter()
+        _, okc = oracle.chains_decrypt(w.key, w.base_iv, chain, c, t, a, 32)
+        total += time.perf_counter() - s
+        assert okc.all()
+    nbytes = sum(ct.numel() for _, ct, *_ in cases)
+    log("cpu oracle %.3f GB/s (%.1f s)" % (nbytes / total / 1e9, time.perf_counter() - t0))
+    return {"value": round(nbytes / total / 1e9, 4), "unit": "GB/s", "cores": oracle.max_threads(), "kind": "oracle",
+            "sample": "the 64 MiB image batch decrypted + verified at all 5 chain sizes (320 MiB), OpenMP over chains"}
+
+
+if __name__ == "__main__":
+    main()

@@ -18,15 +18,18 @@
 // block 64k + l, so loads are one coalesced 1 KiB access per wave). Each lane
 // runs its own Horner chain with the fixed multiplier H^64:
 //     acc_l <- acc_l . H^64  xor  X_(64k+l)
-// and at the end of its segment the lanes are combined as
-//     G = sum_l acc_l . H^(64-l)
+// and at the end of its segment the lanes are combined with one extra factor H:
+//     G'_s = sum_l acc_l . H^(65-l)
 // (lane l's last block has 63-l blocks after it). A segment shorter than a
 // multiple of 64 is padded with zero blocks at its START, which leaves GHASH
 // unchanged. Segments are aligned to the end of the chain, so segment s of S
-// carries the weight H^((S-1-s) . 2^seg_log2) when the chain is assembled.
-// With G_C = GHASH over the ciphertext blocks of a chain and q their number,
-//     S = (GHASH(A) . H^q  xor  G_C  xor  [len A]_64 || [len C]_64) . H,
-//     T = S xor AES_K(J0),   J0 = IV_i || 0^31 || 1.
+// carries the weight H^((S-1-s) . 2^seg_log2) within the chain.
+// With q ciphertext blocks, G_C = GHASH over them, A the AAD and L the length
+// block [len A]_64 || [len C]_64 (lengths in bits):
+//     GHASH(A || C || L) = G_C . H  xor  GHASH(A) . H^(q+1)  xor  L . H
+//     T = GHASH(A || C || L) xor AES_K(J0),   J0 = IV_i || 0^31 || 1.
+// The streaming kernel produces G_C . H; everything else depends only on the
+// AAD, the lengths and the IV, and is added per chain by the finalize kernel.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -68,7 +71,7 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
     __shared__ uint32_t s_sbox[256];
     __shared__ uint32_t s_t0[256];
     __shared__ uint32_t s_rk[60];
-    __shared__ u4 s_hp[kMaxPow + 1];
+    __shared__ u4 s_hp[kMaxPow + 2];
     __shared__ u4 s_hsq[kSquares];
     __shared__ u4 s_basis[128];
     __shared__ Tab4 s_tab;
@@ -113,6 +116,13 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
             s_hp[half + tid + 1] = mul_tab4(s_hp[tid + 1], &s_tab);
         __syncthreads();
     }
+    // H^65 = H^64 . H
+    if (tid < kTab4Pos)
+        build_tab4_row(s_hp[1], tid, &s_tab);
+    __syncthreads();
+    if (tid == 0)
+        s_hp[kMaxPow + 1] = mul_tab4(s_hp[kMaxPow], &s_tab);
+    __syncthreads();
     // Squares H^(2^t): t <= 6 are already powers; the rest by repeated squaring.
     if (tid <= 6)
         s_hsq[tid] = s_hp[1 << tid];
@@ -125,20 +135,22 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
             s_hsq[t] = mul_tab4(s_hsq[t - 1], &s_tab);
         __syncthreads();
     }
-    for (int i = tid; i <= kMaxPow; i += blockDim.x)
+    for (int i = tid; i <= kMaxPow + 1; i += blockDim.x)
         for (int j = 0; j < 4; ++j)
             ctx->hp[i][j] = s_hp[i].w[j];
     for (int i = tid; i < kSquares; i += blockDim.x)
         for (int j = 0; j < 4; ++j)
             ctx->hsq[i][j] = s_hsq[i].w[j];
 
-    // 4-bit tables of every H^e (e = 1..64) and every H^(2^t).
-    for (int task = tid; task < (kMaxPow + kSquares) * kTab4Pos; task += blockDim.x) {
-        int tbl = task / kTab4Pos, p = task % kTab4Pos;
-        if (tbl < kMaxPow)
-            build_tab4_row(s_hp[tbl + 1], p, &ctx->pow_tab[tbl]);
+    // 4-bit tables: H, the lane weights H^(65-l) and every H^(2^t).
+    for (int task = tid; task < (1 + kMaxPow + kSquares) * kTab4Pos; task += blockDim.x) {
+        const int tbl = task / kTab4Pos, p = task % kTab4Pos;
+        if (tbl == 0)
+            build_tab4_row(s_hp[1], p, &ctx->h1_tab);
+        else if (tbl <= kMaxPow)
+            build_tab4_row(s_hp[kMaxPow + 1 - (tbl - 1)], p, &ctx->lane_tab[tbl - 1]);
         else
-            build_tab4_row(s_hsq[tbl - kMaxPow], p, &ctx->sq_tab[tbl - kMaxPow]);
+            build_tab4_row(s_hsq[tbl - 1 - kMaxPow], p, &ctx->sq_tab[tbl - 1 - kMaxPow]);
     }
 
     // 8-bit positional table of H^64: g8[k][v] = (byte v at byte k) . H^64, v's bit 7 = degree 8k.
@@ -208,48 +220,6 @@ __device__ inline void store_bytes(uint8_t *dst, const u4 &v, uint32_t n)
                 dst[4 * j + b] = (uint8_t)(v.w[j] >> (8 * b));
 }
 
-// Tag of one chain from G_C (computed redundantly by the lanes of one wave;
-// lane 0 writes). T(x) returns T0[x] for the J0 encryption.
-template <bool ENC, class LK>
-__device__ inline void chain_finalize(const GcmLaunch &p, uint32_t chain_local, u4 gc, LK T)
-{
-    const KeyCtx *c = p.ctx;
-    const uint64_t gchain = p.chain_base + chain_local;
-    const bool last = chain_local == p.n_chains - 1;
-    const uint64_t len_i = last ? p.last_len : p.chain_bytes;
-    const uint32_t q = last ? p.q_last : p.qc;
-
-    u4 y = zero4();
-    if (p.aad_bytes) {
-        const uint8_t *a = p.aad + gchain * p.aad_bytes;
-        for (uint32_t off = 0; off < p.aad_bytes; off += 16) {
-            uint32_t n = p.aad_bytes - off < 16 ? p.aad_bytes - off : 16;
-            y = mul_tab4(xor4(y, load_bytes(a + off, n)), &c->pow_tab[0]);
-        }
-        y = mul_hpow(y, q, c);
-    }
-    y = xor4(y, gc);
-    const uint64_t abits = (uint64_t)p.aad_bytes * 8, cbits = len_i * 8;
-    u4 lens = {{bswap32((uint32_t)(abits >> 32)), bswap32((uint32_t)abits), bswap32((uint32_t)(cbits >> 32)),
-                bswap32((uint32_t)cbits)}};
-    y = mul_tab4(xor4(y, lens), &c->pow_tab[0]);
-
-    uint32_t iv[3];
-    chain_iv(p, gchain, iv);
-    u4 j0 = {{iv[0], iv[1], iv[2], bswap32(1u)}};
-    u4 e = aes256_encrypt_tt(j0, c->rk, T);
-    u4 tag = xor4(y, e);
-    if ((threadIdx.x & 63) == 0) {
-        if (ENC) {
-            store_bytes(p.tags_out + 16 * gchain, tag, 16);
-        } else {
-            u4 got = load_bytes(p.tags_in + 16 * gchain, 16);
-            uint32_t d = (got.w[0] ^ tag.w[0]) | (got.w[1] ^ tag.w[1]) | (got.w[2] ^ tag.w[2]) | (got.w[3] ^ tag.w[3]);
-            p.ok[gchain] = d == 0 ? 1 : 0;
-        }
-    }
-}
-
 // Position of an item: chain, and the block range [b, e) of its segment.
 struct ItemPos {
     uint32_t chain, s, S, q, b, e;
@@ -267,6 +237,7 @@ __device__ __forceinline__ ItemPos item_pos(const GcmLaunch &p, uint64_t item)
     r.b = r.s == 0 ? 0u : r.e - (1u << p.seg_log2);
     return r;
 }
+
 
 // ===========================================================================
 // The streaming kernel
@@ -336,7 +307,17 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
         const uint64_t gchain = p.chain_base + ip.chain;
         uint32_t iv[3];
         chain_iv(p, gchain, iv);
+        // Counter mode: columns 0..2 of the state after AddRoundKey are the IV and
+        // fixed for the whole chain, so 12 of round 1's 16 lookups are too.
         const uint32_t c0 = iv[0] ^ rk[0], c1 = iv[1] ^ rk[1], c2 = iv[2] ^ rk[2];
+        const uint32_t p0 = xor3(tlk(lds, c0, lanec, FT_SEL(0)), rotl32(tlk(lds, c1, lanec, FT_SEL(1)), 8),
+                                 xor3(rotl32(tlk(lds, c2, lanec, FT_SEL(2)), 16), rk[4], 0u));
+        const uint32_t p1 = xor3(tlk(lds, c1, lanec, FT_SEL(0)), rotl32(tlk(lds, c2, lanec, FT_SEL(1)), 8),
+                                 xor3(rotl32(tlk(lds, c0, lanec, FT_SEL(3)), 24), rk[5], 0u));
+        const uint32_t p2 = xor3(tlk(lds, c2, lanec, FT_SEL(0)), rotl32(tlk(lds, c0, lanec, FT_SEL(2)), 16),
+                                 xor3(rotl32(tlk(lds, c1, lanec, FT_SEL(3)), 24), rk[6], 0u));
+        const uint32_t p3 = xor3(rotl32(tlk(lds, c0, lanec, FT_SEL(1)), 8), rotl32(tlk(lds, c1, lanec, FT_SEL(2)), 16),
+                                 xor3(rotl32(tlk(lds, c2, lanec, FT_SEL(3)), 24), rk[7], 0u));
         const uint8_t *src = p.in + (uint64_t)ip.chain * p.chain_bytes;
         uint8_t *dst = p.out + (uint64_t)ip.chain * p.chain_bytes;
         const bool last_chain = ip.chain == p.n_chains - 1;
@@ -361,9 +342,14 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
                 }
             }
             // Counter block IV_i || [t + 2]_32 (data blocks start at inc32(J0)).
-            uint32_t s0 = c0, s1 = c1, s2 = c2, s3 = bswap32(t + 2u) ^ rk[3];
+            const uint32_t s3i = bswap32(t + 2u) ^ rk[3];
+            // Round 1: only the counter column varies; it feeds row 3-j of output column j.
+            uint32_t s0 = xor3(p0, rotl32(tlk(lds, s3i, lanec, FT_SEL(3)), 24), 0u);
+            uint32_t s1 = xor3(p1, rotl32(tlk(lds, s3i, lanec, FT_SEL(2)), 16), 0u);
+            uint32_t s2 = xor3(p2, rotl32(tlk(lds, s3i, lanec, FT_SEL(1)), 8), 0u);
+            uint32_t s3 = xor3(p3, tlk(lds, s3i, lanec, FT_SEL(0)), 0u);
 #pragma unroll
-            for (int r = 1; r < 14; ++r) {
+            for (int r = 2; r < 14; ++r) {
                 const uint32_t n0 = xor3(tlk(lds, s0, lanec, FT_SEL(0)), rotl32(tlk(lds, s1, lanec, FT_SEL(1)), 8),
                                          xor3(rotl32(tlk(lds, s2, lanec, FT_SEL(2)), 16),
                                               rotl32(tlk(lds, s3, lanec, FT_SEL(3)), 24), rk[4 * r + 0]));
@@ -434,8 +420,8 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
             }
         }
         if (p.do_ghash) {
-            // Lane l's Horner chain carries weight H^(64-l) within the segment.
-            acc = mul_tab4(acc, &c->pow_tab[63 - lane]);
+            // Lane l's Horner chain carries weight H^(64-l) in its segment; one more H for the tag.
+            acc = mul_tab4(acc, &c->lane_tab[lane]);
             const u4 g = wave_xor(acc);
             if (lane == 0)
                 p.partials[item] = make_uint4(g.w[0], g.w[1], g.w[2], g.w[3]);
@@ -443,25 +429,106 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
     }
 }
 
-// One wave per chain: fold the segment partials of chains split over several waves.
-template <bool ENC>
-__global__ __launch_bounds__(256) void finalize_kernel(GcmLaunch p)
+// ===========================================================================
+// Per-chain tag: T = G_C.H xor GHASH(A).H^(q+1) xor L.H xor AES_K(J0)
+// ===========================================================================
+
+// GHASH(A) . H^(q+1) xor L . H for global chain `gchain` of length len_i (q blocks).
+__device__ inline u4 aad_len_term(const GcmLaunch &p, uint64_t gchain, uint64_t len_i, uint32_t q)
 {
+    const KeyCtx *c = p.ctx;
+    u4 y = zero4();
+    if (p.aad_bytes) {
+        const uint8_t *a = p.aad + gchain * p.aad_bytes;
+        for (uint32_t off = 0; off < p.aad_bytes; off += 16) {
+            const uint32_t n = p.aad_bytes - off < 16 ? p.aad_bytes - off : 16;
+            y = mul_tab4(xor4(y, load_bytes(a + off, n)), &c->h1_tab);
+        }
+        y = mul_hpow(y, q + 1u, c);
+    }
+    const uint64_t abits = (uint64_t)p.aad_bytes * 8, cbits = len_i * 8;
+    const u4 lens = {{bswap32((uint32_t)(abits >> 32)), bswap32((uint32_t)abits), bswap32((uint32_t)(cbits >> 32)),
+                      bswap32((uint32_t)cbits)}};
+    return xor4(y, mul_tab4(lens, &c->h1_tab));
+}
+
+template <class LK>
+__device__ inline u4 j0_mask(const GcmLaunch &p, uint64_t gchain, LK T)
+{
+    uint32_t iv[3];
+    chain_iv(p, gchain, iv);
+    const u4 j0 = {{iv[0], iv[1], iv[2], bswap32(1u)}};
+    return aes256_encrypt_tt(j0, p.ctx->rk, T);
+}
+
+template <bool ENC>
+__device__ inline void emit_tag(const GcmLaunch &p, uint64_t gchain, const u4 &tag)
+{
+    if (ENC) {
+        store_bytes(p.tags_out + 16 * gchain, tag, 16);
+    } else {
+        const u4 got = load_bytes(p.tags_in + 16 * gchain, 16);
+        const uint32_t d = (got.w[0] ^ tag.w[0]) | (got.w[1] ^ tag.w[1]) | (got.w[2] ^ tag.w[2]) |
+                           (got.w[3] ^ tag.w[3]);
+        p.ok[gchain] = d == 0 ? 1 : 0;
+    }
+}
+
+// One thread per chain, for chains that were one segment each.
+template <bool ENC>
+__global__ __launch_bounds__(256) void finalize_single_kernel(GcmLaunch p)
+{
+    __shared__ uint32_t s_t0[256];
+    s_t0[threadIdx.x] = p.ctx->t0[threadIdx.x];
+    __syncthreads();
+    const uint32_t chain = blockIdx.x * blockDim.x + threadIdx.x;
+    if (chain >= p.n_chains)
+        return;
+    const uint64_t gchain = p.chain_base + chain;
+    const bool last = chain == p.n_chains - 1;
+    const uint64_t len_i = last ? p.last_len : p.chain_bytes;
+    const uint32_t q = last ? p.q_last : p.qc;
+    const uint4 g = p.partials[chain];
+    u4 tag = {{g.x, g.y, g.z, g.w}};
+    tag = xor4(tag, aad_len_term(p, gchain, len_i, q));
+    tag = xor4(tag, j0_mask(p, gchain, [&](uint32_t x) { return s_t0[x]; }));
+    emit_tag<ENC>(p, gchain, tag);
+}
+
+// One wave per chain, for chains split into several segments: lanes weight the
+// segment partials by H^((S-1-s) . 2^seg_log2); lane 62 adds the AAD/length
+// term and lane 63 the J0 mask; the wave XOR is the tag.
+template <bool ENC>
+__global__ __launch_bounds__(256) void finalize_multi_kernel(GcmLaunch p)
+{
+    __shared__ uint32_t s_t0[256];
+    s_t0[threadIdx.x] = p.ctx->t0[threadIdx.x];
+    __syncthreads();
     const uint32_t chain = blockIdx.x * 4 + (threadIdx.x >> 6);
     const uint32_t lane = threadIdx.x & 63;
     if (chain >= p.n_chains)
         return;
     const KeyCtx *__restrict__ c = p.ctx;
+    const uint64_t gchain = p.chain_base + chain;
     const bool last = chain == p.n_chains - 1;
     const uint32_t S = last ? p.segs_last : p.segs_full;
+    const uint64_t len_i = last ? p.last_len : p.chain_bytes;
+    const uint32_t q = last ? p.q_last : p.qc;
     u4 acc = zero4();
-    for (uint32_t s = lane; s < S; s += 64) {
+    for (uint32_t s = lane; s < S; s += 62) {
+        if (lane >= 62)
+            break;
         const uint4 g = p.partials[(uint64_t)chain * p.segs_full + s];
-        u4 gv = {{g.x, g.y, g.z, g.w}};
+        const u4 gv = {{g.x, g.y, g.z, g.w}};
         acc = xor4(acc, mul_hpow(gv, (S - 1 - s) << p.seg_log2, c));
     }
-    const u4 gc = wave_xor(acc);
-    chain_finalize<ENC>(p, chain, gc, [&](uint32_t x) { return c->t0[x]; });
+    if (lane == 62)
+        acc = aad_len_term(p, gchain, len_i, q);
+    if (lane == 63)
+        acc = j0_mask(p, gchain, [&](uint32_t x) { return s_t0[x]; });
+    const u4 tag = wave_xor(acc);
+    if (lane == 0)
+        emit_tag<ENC>(p, gchain, tag);
 }
 
 // The paper's baseline authentication: one thread per chain, Horner with H over
@@ -469,6 +536,9 @@ __global__ __launch_bounds__(256) void finalize_kernel(GcmLaunch p)
 template <bool ENC>
 __global__ __launch_bounds__(256) void seq_ghash_kernel(GcmLaunch p)
 {
+    __shared__ uint32_t s_t0[256];
+    s_t0[threadIdx.x] = p.ctx->t0[threadIdx.x];
+    __syncthreads();
     const uint32_t chain = blockIdx.x * blockDim.x + threadIdx.x;
     if (chain >= p.n_chains)
         return;
@@ -476,59 +546,52 @@ __global__ __launch_bounds__(256) void seq_ghash_kernel(GcmLaunch p)
     const uint64_t gchain = p.chain_base + chain;
     const bool last = chain == p.n_chains - 1;
     const uint64_t len_i = last ? p.last_len : p.chain_bytes;
-    const Tab4 *hT = &c->pow_tab[0];
+    const Tab4 *hT = &c->h1_tab;
     u4 y = zero4();
     const uint8_t *a = p.aad + gchain * p.aad_bytes;
     for (uint32_t off = 0; off < p.aad_bytes; off += 16) {
-        uint32_t n = p.aad_bytes - off < 16 ? p.aad_bytes - off : 16;
+        const uint32_t n = p.aad_bytes - off < 16 ? p.aad_bytes - off : 16;
         y = mul_tab4(xor4(y, load_bytes(a + off, n)), hT);
     }
     const uint8_t *ct = (ENC ? p.out : p.in) + (uint64_t)chain * p.chain_bytes;
     const uint64_t whole = len_i / 16;
     for (uint64_t t = 0; t < whole; ++t) {
         const uint4 x = reinterpret_cast<const uint4 *>(ct)[t];
-        u4 xv = {{x.x, x.y, x.z, x.w}};
+        const u4 xv = {{x.x, x.y, x.z, x.w}};
         y = mul_tab4(xor4(y, xv), hT);
     }
     if (len_i & 15)
         y = mul_tab4(xor4(y, load_bytes(ct + 16 * whole, (uint32_t)(len_i & 15))), hT);
     const uint64_t abits = (uint64_t)p.aad_bytes * 8, cbits = len_i * 8;
-    u4 lens = {{bswap32((uint32_t)(abits >> 32)), bswap32((uint32_t)abits), bswap32((uint32_t)(cbits >> 32)),
-                bswap32((uint32_t)cbits)}};
+    const u4 lens = {{bswap32((uint32_t)(abits >> 32)), bswap32((uint32_t)abits), bswap32((uint32_t)(cbits >> 32)),
+                      bswap32((uint32_t)cbits)}};
     y = mul_tab4(xor4(y, lens), hT);
-    uint32_t iv[3];
-    chain_iv(p, gchain, iv);
-    u4 j0 = {{iv[0], iv[1], iv[2], bswap32(1u)}};
-    u4 tag = xor4(y, aes256_encrypt_tt(j0, c->rk, [&](uint32_t x) { return c->t0[x]; }));
-    if (ENC) {
-        store_bytes(p.tags_out + 16 * gchain, tag, 16);
-    } else {
-        u4 got = load_bytes(p.tags_in + 16 * gchain, 16);
-        uint32_t d = (got.w[0] ^ tag.w[0]) | (got.w[1] ^ tag.w[1]) | (got.w[2] ^ tag.w[2]) | (got.w[3] ^ tag.w[3]);
-        p.ok[gchain] = d == 0 ? 1 : 0;
-    }
+    const u4 tag = xor4(y, j0_mask(p, gchain, [&](uint32_t x) { return s_t0[x]; }));
+    emit_tag<ENC>(p, gchain, tag);
 }
 
-hipError_t launch_gcm(const GcmLaunch &p, bool encrypt, int num_cu, hipStream_t s)
+template <bool ENC>
+static hipError_t launch_gcm_t(const GcmLaunch &p, int num_cu, hipStream_t s)
 {
     if (p.n_items == 0)
         return hipSuccess;
     uint64_t wgs = (p.n_items + kWavesPerWg - 1) / kWavesPerWg;
     if (wgs > (uint64_t)num_cu)
         wgs = (uint64_t)num_cu;
-    if (encrypt)
-        hipLaunchKernelGGL(gcm_kernel<true>, dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
-    else
-        hipLaunchKernelGGL(gcm_kernel<false>, dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+    hipLaunchKernelGGL(gcm_kernel<ENC>, dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !p.do_ghash)
         return e;
-    const uint32_t fwgs = (p.n_chains + 3) / 4;
-    if (encrypt)
-        hipLaunchKernelGGL(finalize_kernel<true>, dim3(fwgs), dim3(256), 0, s, p);
+    if (p.segs_full == 1)
+        hipLaunchKernelGGL(finalize_single_kernel<ENC>, dim3((p.n_chains + 255) / 256), dim3(256), 0, s, p);
     else
-        hipLaunchKernelGGL(finalize_kernel<false>, dim3(fwgs), dim3(256), 0, s, p);
+        hipLaunchKernelGGL(finalize_multi_kernel<ENC>, dim3((p.n_chains + 3) / 4), dim3(256), 0, s, p);
     return hipGetLastError();
+}
+
+hipError_t launch_gcm(const GcmLaunch &p, bool encrypt, int num_cu, hipStream_t s)
+{
+    return encrypt ? launch_gcm_t<true>(p, num_cu, s) : launch_gcm_t<false>(p, num_cu, s);
 }
 
 hipError_t launch_seq_ghash(const GcmLaunch &p, bool encrypt, hipStream_t s)

@@ -31,9 +31,10 @@ struct KeyCtx {
     uint32_t t0[256];           // T0[x] = {02}S(x) | S(x)<<8 | S(x)<<16 | {03}S(x)<<24
     uint8_t sbox[256];
     uint32_t h[4];              // H = AES_K(0^128)
-    uint32_t hp[kMaxPow + 1][4];      // hp[e] = H^e, e = 0..64 (hp[0] = 1)
+    uint32_t hp[kMaxPow + 2][4];      // hp[e] = H^e, e = 0..65 (hp[0] = 1)
     uint32_t hsq[kSquares][4];        // hsq[t] = H^(2^t)
-    Tab4 pow_tab[kMaxPow];      // pow_tab[e-1]: table of H^e, e = 1..64
+    Tab4 h1_tab;                // table of H
+    Tab4 lane_tab[kMaxPow];     // lane_tab[l]: table of H^(65-l), the lane-combine weight of lane l
     Tab4 sq_tab[kSquares];      // sq_tab[t]: table of H^(2^t)
     uint32_t g8[16][256][4];    // 8-bit positional table of H^64: g8[k][v] = (byte v at byte k) . H^64
 };
