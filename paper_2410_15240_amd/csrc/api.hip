@@ -189,7 +189,11 @@ uint32_t ceil_log2(uint64_t x)
     return r;
 }
 
-// Split `len` bytes (chains chain_base ..) into (chain, segment) work items.
+// Split `len` bytes (chains chain_base ..) into (chain, segment) work items and
+// pick the lanes per item. The aim is one item per resident wave-slot: short
+// chains get 16 or 32 lanes each (so one wave works on several chains and the
+// per-item lane combine is amortised over more blocks per lane); long chains
+// get 64 lanes and are cut into segments.
 void make_plan(uint64_t len, uint64_t chain_bytes, uint64_t chain_base, int num_cu, GcmLaunch &p)
 {
     const uint64_t n = (len + chain_bytes - 1) / chain_bytes;
@@ -200,12 +204,22 @@ void make_plan(uint64_t len, uint64_t chain_bytes, uint64_t chain_base, int num_
     p.qc = (uint32_t)qc;
     p.last_len = len - (n - 1) * chain_bytes;
     p.q_last = (uint32_t)((p.last_len + 15) / 16);
+    const uint64_t slots = (uint64_t)num_cu * 16;            // resident waves
     uint32_t lg = ceil_log2(qc);
     if (lg > 31)
         lg = 31;
-    const uint64_t target = (uint64_t)num_cu * 16 * 2;   // two items per resident wave
-    while (lg > (uint32_t)kMinSegLog2 && n * ((qc + (1ull << lg) - 1) >> lg) < target)
-        --lg;
+    uint32_t ll = 0;
+    for (uint32_t cand = 4; cand <= 6; ++cand)
+        if (qc >= (4ull << cand) && ((n << cand) + 63) / 64 >= slots) {
+            ll = cand;
+            break;
+        }
+    if (ll == 0)   // short chains keep few lanes each; otherwise 64 lanes
+        ll = qc >= 256 ? 6 : (qc >= 128 ? 5 : 4);
+    if (ll == 6)   // too few whole chains to fill the GPU: cut them into segments
+        while (lg > (uint32_t)kMinSegLog2 && n * ((qc + (1ull << lg) - 1) >> lg) < slots)
+            --lg;
+    p.lanes_log2 = ll;
     p.seg_log2 = lg;
     p.segs_full = (uint32_t)((qc + (1ull << lg) - 1) >> lg);
     p.segs_last = (uint32_t)((p.q_last + (1ull << lg) - 1) >> lg);

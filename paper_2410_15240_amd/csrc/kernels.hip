@@ -73,7 +73,7 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
     __shared__ uint32_t s_rk[60];
     __shared__ u4 s_hp[kMaxPow + 2];
     __shared__ u4 s_hsq[kSquares];
-    __shared__ u4 s_basis[128];
+    __shared__ u4 s_basis[3][128];
     __shared__ Tab4 s_tab;
     const int tid = threadIdx.x;
 
@@ -153,19 +153,20 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
             build_tab4_row(s_hsq[tbl - 1 - kMaxPow], p, &ctx->sq_tab[tbl - 1 - kMaxPow]);
     }
 
-    // 8-bit positional table of H^64: g8[k][v] = (byte v at byte k) . H^64, v's bit 7 = degree 8k.
-    if (tid < 128)
-        s_basis[tid] = be_mul_xk_any(to_be(s_hp[kMaxPow]), tid);
+    // 8-bit positional tables of H^16, H^32, H^64:
+    // g8[i][k][v] = (byte v at byte k) . H^(16 << i), v's bit 7 = degree 8k.
+    if (tid < 3 * 128)
+        s_basis[tid >> 7][tid & 127] = be_mul_xk_any(to_be(s_hp[16 << (tid >> 7)]), tid & 127);
     __syncthreads();
-    for (int ent = tid; ent < 16 * 256; ent += blockDim.x) {
-        int k = ent >> 8, v = ent & 255;
+    for (int ent = tid; ent < 3 * 16 * 256; ent += blockDim.x) {
+        const int i = ent >> 12, k = (ent >> 8) & 15, v = ent & 255;
         u4 e = {{0u, 0u, 0u, 0u}};
         for (int b = 0; b < 8; ++b)
             if (v & (0x80 >> b))
-                e = xor4(e, s_basis[8 * k + b]);
-        u4 le = from_be(e);
+                e = xor4(e, s_basis[i][8 * k + b]);
+        const u4 le = from_be(e);
         for (int j = 0; j < 4; ++j)
-            ctx->g8[k][v][j] = le.w[j];
+            ctx->g8[i][k][v][j] = le.w[j];
     }
 }
 
@@ -271,15 +272,23 @@ __device__ __forceinline__ uint32_t in_vgpr(uint32_t x)
     return r;
 }
 
-template <bool ENC>
+// Lanes per item L = 2^LL. Item slot g of a wave (lanes g*L .. g*L+L-1) takes
+// L consecutive blocks of its segment per iteration; each lane keeps a Horner
+// accumulator with multiplier H^L, and lane j's accumulator carries the weight
+// H^(L-j) in its segment (times one more H for the tag).
+template <bool ENC, int LL>
 __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
 {
+    constexpr uint32_t L = 1u << LL;
+    constexpr uint32_t G = 64u >> LL;
     // Static, so its LDS address is a compile-time constant and a v_perm result
     // can be used as the ds_read address with no further add.
     __shared__ uint4 lds4[kLdsBytes / 16];
     const char *lds = reinterpret_cast<const char *>(lds4);
     const int tid = threadIdx.x;
     const uint32_t lane = tid & 63;
+    const uint32_t jl = lane & (L - 1);      // lane within the item
+    const uint32_t gs = lane >> LL;          // item slot within the wave
     const KeyCtx *__restrict__ c = p.ctx;
 
     {
@@ -287,7 +296,7 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
         for (int i = tid; i < 16384; i += kThreads)
             t[i] = c->t0[i >> 6];
         if (p.do_ghash) {
-            const uint4 *g = reinterpret_cast<const uint4 *>(c->g8);
+            const uint4 *g = reinterpret_cast<const uint4 *>(c->g8[LL - 4]);
             for (int i = tid; i < 4096; i += kThreads)
                 lds4[i] = g[i];
         }
@@ -302,8 +311,13 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
 
     const uint64_t nwaves = (uint64_t)gridDim.x * kWavesPerWg;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerWg + (tid >> 6));
-    for (uint64_t item = wave; item < p.n_items; item += nwaves) {
-        const ItemPos ip = item_pos(p, item);
+    const uint64_t n_wave_items = (p.n_items + G - 1) / G;
+    const uint32_t seg = 1u << p.seg_log2;
+    const uint32_t Ku = ((seg < p.qc ? seg : p.qc) + L - 1) >> LL;   // iterations per item, uniform
+    for (uint64_t wi = wave; wi < n_wave_items; wi += nwaves) {
+        const uint64_t item = wi * G + gs;
+        const bool valid = item < p.n_items;
+        const ItemPos ip = item_pos(p, valid ? item : p.n_items - 1);
         const uint64_t gchain = p.chain_base + ip.chain;
         uint32_t iv[3];
         chain_iv(p, gchain, iv);
@@ -322,14 +336,12 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
         uint8_t *dst = p.out + (uint64_t)ip.chain * p.chain_bytes;
         const bool last_chain = ip.chain == p.n_chains - 1;
         const uint32_t tail = last_chain ? (uint32_t)(p.last_len & 15) : 0u;   // bytes of a final partial block
-        const uint32_t nblk = ip.e - ip.b;
-        const uint32_t K = (nblk + 63) >> 6;
-        const int pad = (int)((K << 6) - nblk);
+        const int pad = (int)((Ku << LL) - (ip.e - ip.b));                   // zero blocks in front
 
         u4 acc = zero4();
-        for (uint32_t k = 0; k < K; ++k) {
-            const int v = (int)(k << 6) + (int)lane - pad;
-            const bool active = v >= 0;
+        for (uint32_t k = 0; k < Ku; ++k) {
+            const int v = (int)(k << LL) + (int)jl - pad;
+            const bool active = valid && v >= 0;
             const uint32_t t = ip.b + (uint32_t)v;                 // block index inside the chain
             const bool partial = active && tail != 0 && t == ip.q - 1;
             u4 d = zero4();
@@ -402,7 +414,7 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
                 if (k == 0) {
                     acc = g;
                 } else {
-                    // acc <- acc . H^64 xor g, 16 lookups into the 8-bit table.
+                    // acc <- acc . H^L xor g, 16 lookups into the 8-bit table.
                     u4 z = g;
 #pragma unroll
                     for (int kb = 0; kb < 16; kb += 2) {
@@ -420,11 +432,14 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
             }
         }
         if (p.do_ghash) {
-            // Lane l's Horner chain carries weight H^(64-l) in its segment; one more H for the tag.
-            acc = mul_tab4(acc, &c->lane_tab[lane]);
-            const u4 g = wave_xor(acc);
-            if (lane == 0)
-                p.partials[item] = make_uint4(g.w[0], g.w[1], g.w[2], g.w[3]);
+            // Lane j's chain carries weight H^(L-j) in its segment; one more H for the tag.
+            acc = mul_tab4(acc, &c->lane_tab[64 - L + jl]);
+#pragma unroll
+            for (uint32_t off = L / 2; off >= 1; off >>= 1)
+                for (int w = 0; w < 4; ++w)
+                    acc.w[w] ^= __shfl_xor(acc.w[w], off, 64);
+            if (jl == 0 && valid)
+                p.partials[item] = make_uint4(acc.w[0], acc.w[1], acc.w[2], acc.w[3]);
         }
     }
 }
@@ -575,10 +590,17 @@ static hipError_t launch_gcm_t(const GcmLaunch &p, int num_cu, hipStream_t s)
 {
     if (p.n_items == 0)
         return hipSuccess;
-    uint64_t wgs = (p.n_items + kWavesPerWg - 1) / kWavesPerWg;
+    const uint64_t per_wave = 64u >> p.lanes_log2;
+    const uint64_t waves = (p.n_items + per_wave - 1) / per_wave;
+    uint64_t wgs = (waves + kWavesPerWg - 1) / kWavesPerWg;
     if (wgs > (uint64_t)num_cu)
         wgs = (uint64_t)num_cu;
-    hipLaunchKernelGGL(gcm_kernel<ENC>, dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+    if (p.lanes_log2 == 4)
+        hipLaunchKernelGGL((gcm_kernel<ENC, 4>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+    else if (p.lanes_log2 == 5)
+        hipLaunchKernelGGL((gcm_kernel<ENC, 5>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+    else
+        hipLaunchKernelGGL((gcm_kernel<ENC, 6>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !p.do_ghash)
         return e;

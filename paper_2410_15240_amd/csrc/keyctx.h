@@ -36,7 +36,9 @@ struct KeyCtx {
     Tab4 h1_tab;                // table of H
     Tab4 lane_tab[kMaxPow];     // lane_tab[l]: table of H^(65-l), the lane-combine weight of lane l
     Tab4 sq_tab[kSquares];      // sq_tab[t]: table of H^(2^t)
-    uint32_t g8[16][256][4];    // 8-bit positional table of H^64: g8[k][v] = (byte v at byte k) . H^64
+    // 8-bit positional tables of the Horner multipliers H^16, H^32 and H^64 (lanes per
+    // chain 16, 32, 64): g8[i][k][v] = (byte v at byte k) . H^(16 << i)
+    uint32_t g8[3][16][256][4];
 };
 
 }  // namespace fastrack

@@ -11,6 +11,8 @@ namespace fastrack {
 // One launch of the streaming kernel over `n_chains` consecutive chains.
 // The work is split into items (chain, segment); a segment is a run of
 // 2^seg_log2 blocks aligned to the END of its chain (segment 0 may be short).
+// Each item is handled by 2^lanes_log2 lanes of a wave; a wave takes
+// 64 >> lanes_log2 consecutive items at a time.
 struct GcmLaunch {
     const KeyCtx *ctx;
     const uint8_t *in;          // 16-byte aligned; chain 0 of this launch starts here
@@ -23,6 +25,7 @@ struct GcmLaunch {
     uint32_t qc;                // blocks in a full chain
     uint32_t q_last;            // blocks in the last chain (a partial block counts as one)
     uint32_t seg_log2;
+    uint32_t lanes_log2;        // lanes per item: 4 (16), 5 (32) or 6 (64); the Horner stride
     uint32_t segs_full;         // segments of a full chain
     uint32_t segs_last;         // segments of the last chain
     uint32_t iv[3];             // base IV as little-endian words
