@@ -244,16 +244,22 @@ __device__ __forceinline__ ItemPos item_pos(const GcmLaunch &p, uint64_t item)
 // The streaming kernel
 // ===========================================================================
 //
-// LDS layout (128 KiB, one workgroup per CU):
-//   [0, 64 KiB)        g8: the 8-bit table of H^64, entry (k, v) at (k*256 + v)*16
-//   [64 KiB, 128 KiB)  T0 replicated 64 times: T0[x] for lane l at 64 KiB + x*256 + l*4,
-//                      so every lane reads its own bank and lookups never conflict.
-// A T0 address is built with one v_perm_b32: byte 0 = lane*4, byte 1 = the state
-// byte, byte 2 = 1 (the 64 KiB base), byte 3 = 0.
+// LDS layout (160 KiB, one workgroup per CU):
+//   [0, 64 KiB)        region 0: row x (256 B) = T0[x] for lanes 0..31 | T1[x] for lanes 0..31
+//   [64, 128 KiB)      region 1: row x        = T2[x] ...              | T3[x] ...
+//   [128, 160 KiB)     positions 0..7 of the 8-bit table of H^L: entry (k, v) at 128 KiB + (k*256 + v)*16
+// T_r[x] = rotl(T0[x], 8r). Lanes l and l+32 share a copy: the LDS serves a wave's
+// 32-bit reads 32 lanes at a time, so the 32 copies make every lookup
+// conflict-free. A T_r address is one v_perm_b32: byte 0 = (lane%32)*4 + 128*(r&1),
+// byte 1 = the state byte, byte 2 = r>>1 (the region), byte 3 = 0.
+// GHASH multiplies by H^L with the byte positions 8..15 folded onto 0..7: the
+// entry for byte position k+8 is the entry for position k times x^64, so
+//   X . H^L = sum_{k<8} E_k[x_k]  xor  (sum_{k<8} E_k[x_(k+8)]) . x^64.
 
 constexpr int kThreads = 1024;
 constexpr int kWavesPerWg = kThreads / 64;
-constexpr uint32_t kLdsBytes = 128 * 1024;
+constexpr uint32_t kLdsBytes = 160 * 1024;
+constexpr uint32_t kG8Base = 8192;           // uint4 index of the GHASH table in LDS
 
 #define FT_SEL(k) (0x0C020400u + ((uint32_t)(k) << 8))
 
@@ -269,6 +275,23 @@ __device__ __forceinline__ uint32_t in_vgpr(uint32_t x)
 {
     uint32_t r;
     asm("v_mov_b32 %0, %1" : "=v"(r) : "s"(x));
+    return r;
+}
+
+// Y . x^64 in little-endian-word form: bytes 0..7 move to bytes 8..15 and the
+// bytes that pass degree 127, F, come back as F . (1 + x + x^2 + x^7).
+__device__ __forceinline__ u4 mul_x64(const u4 &y)
+{
+    const uint32_t fh = bswap32(y.w[2]), fl = bswap32(y.w[3]);   // F big-endian: degree d at bit 63-d
+    const uint32_t rh = xor3(fh, fh >> 1, xor3(fh >> 2, fh >> 7, 0u));
+    const uint32_t rl = xor3(fl, __builtin_amdgcn_alignbit(fh, fl, 1),
+                             xor3(__builtin_amdgcn_alignbit(fh, fl, 2), __builtin_amdgcn_alignbit(fh, fl, 7), 0u));
+    const uint32_t ro = xor3(fl << 31, fl << 30, fl << 25);      // degrees 64..70 of F . R
+    u4 r;
+    r.w[0] = bswap32(rh);
+    r.w[1] = bswap32(rl);
+    r.w[2] = y.w[0] ^ bswap32(ro);
+    r.w[3] = y.w[1];
     return r;
 }
 
@@ -292,22 +315,30 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
     const KeyCtx *__restrict__ c = p.ctx;
 
     {
-        uint32_t *t = reinterpret_cast<uint32_t *>(lds4) + 16384;
-        for (int i = tid; i < 16384; i += kThreads)
-            t[i] = c->t0[i >> 6];
+        uint32_t *t = reinterpret_cast<uint32_t *>(lds4);
+        for (int i = tid; i < 32768; i += kThreads) {
+            const uint32_t region = i >> 14, row = (i >> 6) & 255, tab = region * 2 + ((i >> 5) & 1);
+            const uint32_t v = c->t0[row];
+            t[i] = tab == 0 ? v : rotl32(v, 8 * tab);
+        }
         if (p.do_ghash) {
             const uint4 *g = reinterpret_cast<const uint4 *>(c->g8[LL - 4]);
-            for (int i = tid; i < 4096; i += kThreads)
-                lds4[i] = g[i];
+            for (int i = tid; i < 2048; i += kThreads)
+                lds4[kG8Base + i] = g[i];
         }
     }
     __syncthreads();
 
-    const uint32_t lanec = 0x10000u | (lane << 2);
+    const uint32_t lb = (lane & 31) << 2;
+    const uint32_t lc0 = lb, lc1 = lb | 0x80u, lc2 = lb | 0x10000u, lc3 = lb | 0x10080u;
+    // Round keys 0..2 and 4..7 are used once per item (scalar registers); the
+    // rest once per block (vector registers).
     uint32_t rk[60];
 #pragma unroll
-    for (int i = 0; i < 60; ++i)
-        rk[i] = in_vgpr(__builtin_amdgcn_readfirstlane(c->rk[i]));
+    for (int i = 0; i < 60; ++i) {
+        const uint32_t w = __builtin_amdgcn_readfirstlane(c->rk[i]);
+        rk[i] = (i < 8 && i != 3) ? w : in_vgpr(w);
+    }
 
     const uint64_t nwaves = (uint64_t)gridDim.x * kWavesPerWg;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerWg + (tid >> 6));
@@ -324,14 +355,14 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
         // Counter mode: columns 0..2 of the state after AddRoundKey are the IV and
         // fixed for the whole chain, so 12 of round 1's 16 lookups are too.
         const uint32_t c0 = iv[0] ^ rk[0], c1 = iv[1] ^ rk[1], c2 = iv[2] ^ rk[2];
-        const uint32_t p0 = xor3(tlk(lds, c0, lanec, FT_SEL(0)), rotl32(tlk(lds, c1, lanec, FT_SEL(1)), 8),
-                                 xor3(rotl32(tlk(lds, c2, lanec, FT_SEL(2)), 16), rk[4], 0u));
-        const uint32_t p1 = xor3(tlk(lds, c1, lanec, FT_SEL(0)), rotl32(tlk(lds, c2, lanec, FT_SEL(1)), 8),
-                                 xor3(rotl32(tlk(lds, c0, lanec, FT_SEL(3)), 24), rk[5], 0u));
-        const uint32_t p2 = xor3(tlk(lds, c2, lanec, FT_SEL(0)), rotl32(tlk(lds, c0, lanec, FT_SEL(2)), 16),
-                                 xor3(rotl32(tlk(lds, c1, lanec, FT_SEL(3)), 24), rk[6], 0u));
-        const uint32_t p3 = xor3(rotl32(tlk(lds, c0, lanec, FT_SEL(1)), 8), rotl32(tlk(lds, c1, lanec, FT_SEL(2)), 16),
-                                 xor3(rotl32(tlk(lds, c2, lanec, FT_SEL(3)), 24), rk[7], 0u));
+        const uint32_t p0 = xor3(tlk(lds, c0, lc0, FT_SEL(0)), tlk(lds, c1, lc1, FT_SEL(1)),
+                                 xor3(tlk(lds, c2, lc2, FT_SEL(2)), rk[4], 0u));
+        const uint32_t p1 = xor3(tlk(lds, c1, lc0, FT_SEL(0)), tlk(lds, c2, lc1, FT_SEL(1)),
+                                 xor3(tlk(lds, c0, lc3, FT_SEL(3)), rk[5], 0u));
+        const uint32_t p2 = xor3(tlk(lds, c2, lc0, FT_SEL(0)), tlk(lds, c0, lc2, FT_SEL(2)),
+                                 xor3(tlk(lds, c1, lc3, FT_SEL(3)), rk[6], 0u));
+        const uint32_t p3 = xor3(tlk(lds, c0, lc1, FT_SEL(1)), tlk(lds, c1, lc2, FT_SEL(2)),
+                                 xor3(tlk(lds, c2, lc3, FT_SEL(3)), rk[7], 0u));
         const uint8_t *src = p.in + (uint64_t)ip.chain * p.chain_bytes;
         uint8_t *dst = p.out + (uint64_t)ip.chain * p.chain_bytes;
         const bool last_chain = ip.chain == p.n_chains - 1;
@@ -356,38 +387,34 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
             // Counter block IV_i || [t + 2]_32 (data blocks start at inc32(J0)).
             const uint32_t s3i = bswap32(t + 2u) ^ rk[3];
             // Round 1: only the counter column varies; it feeds row 3-j of output column j.
-            uint32_t s0 = xor3(p0, rotl32(tlk(lds, s3i, lanec, FT_SEL(3)), 24), 0u);
-            uint32_t s1 = xor3(p1, rotl32(tlk(lds, s3i, lanec, FT_SEL(2)), 16), 0u);
-            uint32_t s2 = xor3(p2, rotl32(tlk(lds, s3i, lanec, FT_SEL(1)), 8), 0u);
-            uint32_t s3 = xor3(p3, tlk(lds, s3i, lanec, FT_SEL(0)), 0u);
+            uint32_t s0 = p0 ^ tlk(lds, s3i, lc3, FT_SEL(3));
+            uint32_t s1 = p1 ^ tlk(lds, s3i, lc2, FT_SEL(2));
+            uint32_t s2 = p2 ^ tlk(lds, s3i, lc1, FT_SEL(1));
+            uint32_t s3 = p3 ^ tlk(lds, s3i, lc0, FT_SEL(0));
 #pragma unroll
             for (int r = 2; r < 14; ++r) {
-                const uint32_t n0 = xor3(tlk(lds, s0, lanec, FT_SEL(0)), rotl32(tlk(lds, s1, lanec, FT_SEL(1)), 8),
-                                         xor3(rotl32(tlk(lds, s2, lanec, FT_SEL(2)), 16),
-                                              rotl32(tlk(lds, s3, lanec, FT_SEL(3)), 24), rk[4 * r + 0]));
-                const uint32_t n1 = xor3(tlk(lds, s1, lanec, FT_SEL(0)), rotl32(tlk(lds, s2, lanec, FT_SEL(1)), 8),
-                                         xor3(rotl32(tlk(lds, s3, lanec, FT_SEL(2)), 16),
-                                              rotl32(tlk(lds, s0, lanec, FT_SEL(3)), 24), rk[4 * r + 1]));
-                const uint32_t n2 = xor3(tlk(lds, s2, lanec, FT_SEL(0)), rotl32(tlk(lds, s3, lanec, FT_SEL(1)), 8),
-                                         xor3(rotl32(tlk(lds, s0, lanec, FT_SEL(2)), 16),
-                                              rotl32(tlk(lds, s1, lanec, FT_SEL(3)), 24), rk[4 * r + 2]));
-                const uint32_t n3 = xor3(tlk(lds, s3, lanec, FT_SEL(0)), rotl32(tlk(lds, s0, lanec, FT_SEL(1)), 8),
-                                         xor3(rotl32(tlk(lds, s1, lanec, FT_SEL(2)), 16),
-                                              rotl32(tlk(lds, s2, lanec, FT_SEL(3)), 24), rk[4 * r + 3]));
+                const uint32_t n0 = xor3(tlk(lds, s0, lc0, FT_SEL(0)), tlk(lds, s1, lc1, FT_SEL(1)),
+                                         xor3(tlk(lds, s2, lc2, FT_SEL(2)), tlk(lds, s3, lc3, FT_SEL(3)), rk[4 * r + 0]));
+                const uint32_t n1 = xor3(tlk(lds, s1, lc0, FT_SEL(0)), tlk(lds, s2, lc1, FT_SEL(1)),
+                                         xor3(tlk(lds, s3, lc2, FT_SEL(2)), tlk(lds, s0, lc3, FT_SEL(3)), rk[4 * r + 1]));
+                const uint32_t n2 = xor3(tlk(lds, s2, lc0, FT_SEL(0)), tlk(lds, s3, lc1, FT_SEL(1)),
+                                         xor3(tlk(lds, s0, lc2, FT_SEL(2)), tlk(lds, s1, lc3, FT_SEL(3)), rk[4 * r + 2]));
+                const uint32_t n3 = xor3(tlk(lds, s3, lc0, FT_SEL(0)), tlk(lds, s0, lc1, FT_SEL(1)),
+                                         xor3(tlk(lds, s1, lc2, FT_SEL(2)), tlk(lds, s2, lc3, FT_SEL(3)), rk[4 * r + 3]));
                 s0 = n0; s1 = n1; s2 = n2; s3 = n3;
             }
-            // Final round: S(x) is byte 1 of T0[x]; assemble four of them with v_perm.
+            // Final round: S(x) is byte (1+r)&3 of T_r[x]; assemble four of them with v_perm.
             u4 o;
             {
                 const uint32_t st[4] = {s0, s1, s2, s3};
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    const uint32_t a0 = tlk(lds, st[j], lanec, FT_SEL(0));
-                    const uint32_t a1 = tlk(lds, st[(j + 1) & 3], lanec, FT_SEL(1));
-                    const uint32_t a2 = tlk(lds, st[(j + 2) & 3], lanec, FT_SEL(2));
-                    const uint32_t a3 = tlk(lds, st[(j + 3) & 3], lanec, FT_SEL(3));
-                    const uint32_t lo = __builtin_amdgcn_perm(a1, a0, 0x0C0C0501u);
-                    const uint32_t hi = __builtin_amdgcn_perm(a3, a2, 0x05010C0Cu);
+                    const uint32_t a0 = tlk(lds, st[j], lc0, FT_SEL(0));
+                    const uint32_t a1 = tlk(lds, st[(j + 1) & 3], lc1, FT_SEL(1));
+                    const uint32_t a2 = tlk(lds, st[(j + 2) & 3], lc2, FT_SEL(2));
+                    const uint32_t a3 = tlk(lds, st[(j + 3) & 3], lc3, FT_SEL(3));
+                    const uint32_t lo = __builtin_amdgcn_perm(a1, a0, 0x0C0C0601u);
+                    const uint32_t hi = __builtin_amdgcn_perm(a3, a2, 0x04030C0Cu);
                     o.w[j] = xor3(lo, hi, rk[56 + j] ^ d.w[j]);
                 }
             }
@@ -414,20 +441,28 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
                 if (k == 0) {
                     acc = g;
                 } else {
-                    // acc <- acc . H^L xor g, 16 lookups into the 8-bit table.
-                    u4 z = g;
+                    // acc <- acc . H^L xor g: positions 0..7 directly, 8..15 through x^64.
+                    u4 lo = g, hi = zero4();
 #pragma unroll
-                    for (int kb = 0; kb < 16; kb += 2) {
-                        const uint32_t ba = (acc.w[kb >> 2] >> (8 * (kb & 3))) & 0xFFu;
-                        const uint32_t bb = (acc.w[(kb + 1) >> 2] >> (8 * ((kb + 1) & 3))) & 0xFFu;
-                        const uint4 ea = lds4[(kb << 8) | ba];
-                        const uint4 eb = lds4[((kb + 1) << 8) | bb];
-                        z.w[0] = xor3(z.w[0], ea.x, eb.x);
-                        z.w[1] = xor3(z.w[1], ea.y, eb.y);
-                        z.w[2] = xor3(z.w[2], ea.z, eb.z);
-                        z.w[3] = xor3(z.w[3], ea.w, eb.w);
+                    for (int kb = 0; kb < 8; kb += 2) {
+                        const uint32_t a0 = (acc.w[kb >> 2] >> (8 * (kb & 3))) & 0xFFu;
+                        const uint32_t a1 = (acc.w[kb >> 2] >> (8 * ((kb + 1) & 3))) & 0xFFu;
+                        const uint32_t b0 = (acc.w[2 + (kb >> 2)] >> (8 * (kb & 3))) & 0xFFu;
+                        const uint32_t b1 = (acc.w[2 + (kb >> 2)] >> (8 * ((kb + 1) & 3))) & 0xFFu;
+                        const uint4 ea = lds4[kG8Base + ((kb << 8) | a0)];
+                        const uint4 eb = lds4[kG8Base + (((kb + 1) << 8) | a1)];
+                        const uint4 fa = lds4[kG8Base + ((kb << 8) | b0)];
+                        const uint4 fb = lds4[kG8Base + (((kb + 1) << 8) | b1)];
+                        lo.w[0] = xor3(lo.w[0], ea.x, eb.x);
+                        lo.w[1] = xor3(lo.w[1], ea.y, eb.y);
+                        lo.w[2] = xor3(lo.w[2], ea.z, eb.z);
+                        lo.w[3] = xor3(lo.w[3], ea.w, eb.w);
+                        hi.w[0] = xor3(hi.w[0], fa.x, fb.x);
+                        hi.w[1] = xor3(hi.w[1], fa.y, fb.y);
+                        hi.w[2] = xor3(hi.w[2], fa.z, fb.z);
+                        hi.w[3] = xor3(hi.w[3], fa.w, fb.w);
                     }
-                    acc = z;
+                    acc = xor4(lo, mul_x64(hi));
                 }
             }
         }
