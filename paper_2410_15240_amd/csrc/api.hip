@@ -204,7 +204,7 @@ void make_plan(uint64_t len, uint64_t chain_bytes, uint64_t chain_base, int num_
     p.qc = (uint32_t)qc;
     p.last_len = len - (n - 1) * chain_bytes;
     p.q_last = (uint32_t)((p.last_len + 15) / 16);
-    const uint64_t slots = (uint64_t)num_cu * 16;            // resident waves
+    const uint64_t slots = (uint64_t)num_cu * kGcmWavesPerWg;   // resident waves
     uint32_t lg = ceil_log2(qc);
     if (lg > 31)
         lg = 31;
@@ -216,6 +216,8 @@ void make_plan(uint64_t len, uint64_t chain_bytes, uint64_t chain_base, int num_
         }
     if (ll == 0)   // short chains keep few lanes each; otherwise 64 lanes
         ll = qc >= 256 ? 6 : (qc >= 128 ? 5 : 4);
+    // Only items of 64 lanes may be segments of a longer chain (the streaming
+    // kernel weights segments with a wave-cooperative multiply).
     if (ll == 6)   // too few whole chains to fill the GPU: cut them into segments
         while (lg > (uint32_t)kMinSegLog2 && n * ((qc + (1ull << lg) - 1) >> lg) < slots)
             --lg;
@@ -305,6 +307,7 @@ int run_gcm(bool encrypt, const KeyCtx *ctx, const uint8_t *base_iv, uint64_t ch
         return FASTRACK_OK;
     }
     p.do_ghash = 1;
+    p.aad_in_stream = ((aad_bytes + 15) / 16) <= (1u << p.lanes_log2) ? 1u : 0u;
     {
         void *sc = nullptr;
         int rc = scratch_for(dev, s, (size_t)p.n_items * 16, &sc);

@@ -28,8 +28,11 @@
 // block [len A]_64 || [len C]_64 (lengths in bits):
 //     GHASH(A || C || L) = G_C . H  xor  GHASH(A) . H^(q+1)  xor  L . H
 //     T = GHASH(A || C || L) xor AES_K(J0),   J0 = IV_i || 0^31 || 1.
-// The streaming kernel produces G_C . H; everything else depends only on the
-// AAD, the lengths and the IV, and is added per chain by the finalize kernel.
+// The streaming kernel produces G_C . H, with the AAD blocks folded into the
+// same Horner streams (they are the blocks that precede the first ciphertext
+// block) and, for a chain cut into segments, each segment's weight inside the
+// chain applied. The finalize kernel XORs a chain's partials and adds L . H and
+// AES_K(J0).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -256,8 +259,8 @@ __device__ __forceinline__ ItemPos item_pos(const GcmLaunch &p, uint64_t item)
 // entry for byte position k+8 is the entry for position k times x^64, so
 //   X . H^L = sum_{k<8} E_k[x_k]  xor  (sum_{k<8} E_k[x_(k+8)]) . x^64.
 
-constexpr int kThreads = 1024;
-constexpr int kWavesPerWg = kThreads / 64;
+constexpr int kThreads = kGcmThreads;
+constexpr int kWavesPerWg = kGcmWavesPerWg;
 constexpr uint32_t kLdsBytes = 160 * 1024;
 constexpr uint32_t kG8Base = 8192;           // uint4 index of the GHASH table in LDS
 
@@ -293,6 +296,29 @@ __device__ __forceinline__ u4 mul_x64(const u4 &y)
     r.w[2] = y.w[0] ^ bswap32(ro);
     r.w[3] = y.w[1];
     return r;
+}
+
+// X . Y for a wave-uniform X: lanes 0..31 each look up one nibble position of
+// Y's 4-bit table and the wave XOR sums the 32 entries. Every lane receives the
+// product.
+__device__ inline u4 coop_mul_tab4(const u4 &x, const Tab4 *__restrict__ t, uint32_t lane)
+{
+    u4 r = zero4();
+    if (lane < 32) {
+        const uint32_t w = lane < 8 ? x.w[0] : (lane < 16 ? x.w[1] : (lane < 24 ? x.w[2] : x.w[3]));
+        const uint32_t byte = (w >> (8 * ((lane >> 1) & 3))) & 0xFFu;
+        const uint32_t nib = (lane & 1) ? (byte & 0xFu) : (byte >> 4);
+        const uint4 e = *reinterpret_cast<const uint4 *>(t->e[lane][nib]);
+        r.w[0] = e.x; r.w[1] = e.y; r.w[2] = e.z; r.w[3] = e.w;
+    }
+    return wave_xor(r);
+}
+
+// AAD block u of a chain's AAD (zero-padded).
+__device__ __forceinline__ u4 aad_block(const uint8_t *aad, uint32_t u, uint32_t aad_bytes)
+{
+    const uint32_t left = aad_bytes - 16u * u;
+    return load_bytes(aad + 16u * u, left < 16u ? left : 16u);
 }
 
 // Lanes per item L = 2^LL. Item slot g of a wave (lanes g*L .. g*L+L-1) takes
@@ -368,8 +394,26 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
         const bool last_chain = ip.chain == p.n_chains - 1;
         const uint32_t tail = last_chain ? (uint32_t)(p.last_len & 15) : 0u;   // bytes of a final partial block
         const int pad = (int)((Ku << LL) - (ip.e - ip.b));                   // zero blocks in front
-
-        u4 acc = zero4();
+        // The AAD blocks precede ciphertext block 0 of the chain in GHASH order, so in
+        // segment 0 AAD block u takes virtual slot (a - u) before it: a padding slot, or
+        // a slot of a virtual iteration -1 that seeds the accumulator.
+        // With at most L AAD blocks each lane holds at most one: the block whose slot
+        // is congruent to the lane, at block index va in [-na, 0) of iteration ka.
+        const int na = (p.aad_in_stream && ip.s == 0 && valid) ? (int)((p.aad_bytes + 15) >> 4) : 0;
+        const int rr = ((int)jl - pad) & (int)(L - 1);
+        const int va = rr == 0 ? -(int)L : rr - (int)L;
+        const bool has_aad = va >= -na;
+        const int ka = (va + pad - (int)jl) >> LL;        // -1 seeds the accumulator
+        u4 aadv = zero4();
+        if (has_aad)
+            aadv = aad_block(p.aad + gchain * p.aad_bytes, (uint32_t)(va + na), p.aad_bytes);
+        u4 acc = (has_aad && ka < 0) ? aadv : zero4();
+        const bool seeded = __any(na > pad);   // some lane starts from an AAD block
+        // Last iteration that carries an AAD block in any lane of the wave.
+        int ka_w = has_aad ? ka : -2;
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1)
+            ka_w = max(ka_w, __shfl_xor(ka_w, off, 64));
         for (uint32_t k = 0; k < Ku; ++k) {
             const int v = (int)(k << LL) + (int)jl - pad;
             const bool active = valid && v >= 0;
@@ -438,7 +482,9 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
                         }
                     }
                 }
-                if (k == 0) {
+                if ((int)k <= ka_w && has_aad && (int)k == ka)   // an AAD block in a padding slot
+                    g = aadv;
+                if (k == 0 && !seeded) {
                     acc = g;
                 } else {
                     // acc <- acc . H^L xor g: positions 0..7 directly, 8..15 through x^64.
@@ -473,6 +519,16 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
             for (uint32_t off = L / 2; off >= 1; off >>= 1)
                 for (int w = 0; w < 4; ++w)
                     acc.w[w] ^= __shfl_xor(acc.w[w], off, 64);
+            if (LL == 6) {
+                // A chain cut into S segments (only with 64 lanes per item): segment s
+                // carries the weight H^((S-1-s) . 2^seg_log2) inside its chain.
+                uint32_t m = ip.S - 1 - ip.s;
+                while (m) {
+                    const uint32_t b = __builtin_ctz(m);
+                    acc = coop_mul_tab4(acc, &c->sq_tab[p.seg_log2 + b], lane);
+                    m &= m - 1;
+                }
+            }
             if (jl == 0 && valid)
                 p.partials[item] = make_uint4(acc.w[0], acc.w[1], acc.w[2], acc.w[3]);
         }
@@ -483,23 +539,26 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
 // Per-chain tag: T = G_C.H xor GHASH(A).H^(q+1) xor L.H xor AES_K(J0)
 // ===========================================================================
 
-// GHASH(A) . H^(q+1) xor L . H for global chain `gchain` of length len_i (q blocks).
-__device__ inline u4 aad_len_term(const GcmLaunch &p, uint64_t gchain, uint64_t len_i, uint32_t q)
+// GHASH(A) . H^(q+1) for global chain `gchain` (q ciphertext blocks).
+__device__ inline u4 aad_term(const GcmLaunch &p, uint64_t gchain, uint32_t q)
 {
     const KeyCtx *c = p.ctx;
     u4 y = zero4();
-    if (p.aad_bytes) {
-        const uint8_t *a = p.aad + gchain * p.aad_bytes;
-        for (uint32_t off = 0; off < p.aad_bytes; off += 16) {
-            const uint32_t n = p.aad_bytes - off < 16 ? p.aad_bytes - off : 16;
-            y = mul_tab4(xor4(y, load_bytes(a + off, n)), &c->h1_tab);
-        }
-        y = mul_hpow(y, q + 1u, c);
+    const uint8_t *a = p.aad + gchain * p.aad_bytes;
+    for (uint32_t off = 0; off < p.aad_bytes; off += 16) {
+        const uint32_t n = p.aad_bytes - off < 16 ? p.aad_bytes - off : 16;
+        y = mul_tab4(xor4(y, load_bytes(a + off, n)), &c->h1_tab);
     }
+    return mul_hpow(y, q + 1u, c);
+}
+
+// L . H, L = [len A]_64 || [len C]_64 in bits.
+__device__ inline u4 len_term(const GcmLaunch &p, uint64_t len_i)
+{
     const uint64_t abits = (uint64_t)p.aad_bytes * 8, cbits = len_i * 8;
     const u4 lens = {{bswap32((uint32_t)(abits >> 32)), bswap32((uint32_t)abits), bswap32((uint32_t)(cbits >> 32)),
                       bswap32((uint32_t)cbits)}};
-    return xor4(y, mul_tab4(lens, &c->h1_tab));
+    return mul_tab4(lens, &p.ctx->h1_tab);
 }
 
 template <class LK>
@@ -524,9 +583,10 @@ __device__ inline void emit_tag(const GcmLaunch &p, uint64_t gchain, const u4 &t
     }
 }
 
-// One thread per chain, for chains that were one segment each.
+// One thread per chain: the XOR of the chain's (already weighted) partials,
+// the AAD term when the AAD did not ride in the stream, L . H and AES_K(J0).
 template <bool ENC>
-__global__ __launch_bounds__(256) void finalize_single_kernel(GcmLaunch p)
+__global__ __launch_bounds__(256) void finalize_kernel(GcmLaunch p)
 {
     __shared__ uint32_t s_t0[256];
     s_t0[threadIdx.x] = p.ctx->t0[threadIdx.x];
@@ -538,47 +598,16 @@ __global__ __launch_bounds__(256) void finalize_single_kernel(GcmLaunch p)
     const bool last = chain == p.n_chains - 1;
     const uint64_t len_i = last ? p.last_len : p.chain_bytes;
     const uint32_t q = last ? p.q_last : p.qc;
-    const uint4 g = p.partials[chain];
-    u4 tag = {{g.x, g.y, g.z, g.w}};
-    tag = xor4(tag, aad_len_term(p, gchain, len_i, q));
-    tag = xor4(tag, j0_mask(p, gchain, [&](uint32_t x) { return s_t0[x]; }));
-    emit_tag<ENC>(p, gchain, tag);
-}
-
-// One wave per chain, for chains split into several segments: lanes weight the
-// segment partials by H^((S-1-s) . 2^seg_log2); lane 62 adds the AAD/length
-// term and lane 63 the J0 mask; the wave XOR is the tag.
-template <bool ENC>
-__global__ __launch_bounds__(256) void finalize_multi_kernel(GcmLaunch p)
-{
-    __shared__ uint32_t s_t0[256];
-    s_t0[threadIdx.x] = p.ctx->t0[threadIdx.x];
-    __syncthreads();
-    const uint32_t chain = blockIdx.x * 4 + (threadIdx.x >> 6);
-    const uint32_t lane = threadIdx.x & 63;
-    if (chain >= p.n_chains)
-        return;
-    const KeyCtx *__restrict__ c = p.ctx;
-    const uint64_t gchain = p.chain_base + chain;
-    const bool last = chain == p.n_chains - 1;
     const uint32_t S = last ? p.segs_last : p.segs_full;
-    const uint64_t len_i = last ? p.last_len : p.chain_bytes;
-    const uint32_t q = last ? p.q_last : p.qc;
-    u4 acc = zero4();
-    for (uint32_t s = lane; s < S; s += 62) {
-        if (lane >= 62)
-            break;
-        const uint4 g = p.partials[(uint64_t)chain * p.segs_full + s];
-        const u4 gv = {{g.x, g.y, g.z, g.w}};
-        acc = xor4(acc, mul_hpow(gv, (S - 1 - s) << p.seg_log2, c));
+    u4 tag = xor4(len_term(p, len_i), j0_mask(p, gchain, [&](uint32_t x) { return s_t0[x]; }));
+    const uint4 *part = p.partials + (uint64_t)chain * p.segs_full;
+    for (uint32_t s = 0; s < S; ++s) {
+        const uint4 g = part[s];
+        tag.w[0] ^= g.x; tag.w[1] ^= g.y; tag.w[2] ^= g.z; tag.w[3] ^= g.w;
     }
-    if (lane == 62)
-        acc = aad_len_term(p, gchain, len_i, q);
-    if (lane == 63)
-        acc = j0_mask(p, gchain, [&](uint32_t x) { return s_t0[x]; });
-    const u4 tag = wave_xor(acc);
-    if (lane == 0)
-        emit_tag<ENC>(p, gchain, tag);
+    if (p.aad_bytes && !p.aad_in_stream)
+        tag = xor4(tag, aad_term(p, gchain, q));
+    emit_tag<ENC>(p, gchain, tag);
 }
 
 // The paper's baseline authentication: one thread per chain, Horner with H over
@@ -639,10 +668,7 @@ static hipError_t launch_gcm_t(const GcmLaunch &p, int num_cu, hipStream_t s)
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !p.do_ghash)
         return e;
-    if (p.segs_full == 1)
-        hipLaunchKernelGGL(finalize_single_kernel<ENC>, dim3((p.n_chains + 255) / 256), dim3(256), 0, s, p);
-    else
-        hipLaunchKernelGGL(finalize_multi_kernel<ENC>, dim3((p.n_chains + 3) / 4), dim3(256), 0, s, p);
+    hipLaunchKernelGGL(finalize_kernel<ENC>, dim3((p.n_chains + 255) / 256), dim3(256), 0, s, p);
     return hipGetLastError();
 }
 

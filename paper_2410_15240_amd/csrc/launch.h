@@ -8,6 +8,14 @@
 
 namespace fastrack {
 
+// Threads per workgroup of the streaming kernel. Its 160 KiB of LDS allow one
+// workgroup per CU, so this is also the number of resident threads per CU.
+#ifndef FT_GCM_THREADS
+#define FT_GCM_THREADS 512
+#endif
+constexpr int kGcmThreads = FT_GCM_THREADS;
+constexpr int kGcmWavesPerWg = kGcmThreads / 64;
+
 // One launch of the streaming kernel over `n_chains` consecutive chains.
 // The work is split into items (chain, segment); a segment is a run of
 // 2^seg_log2 blocks aligned to the END of its chain (segment 0 may be short).
@@ -34,8 +42,9 @@ struct GcmLaunch {
     const uint8_t *tags_in;     // decrypt: received tags, global chain i at tags_in + 16 i
     uint8_t *tags_out;          // encrypt: produced tags
     uint8_t *ok;                // decrypt: ok[global chain] = 1 accept / 0 reject
-    uint4 *partials;            // per-item GHASH partials when a chain has several segments
+    uint4 *partials;            // per-item GHASH partials, already weighted within their chain
     uint32_t do_ghash;          // 0: keystream only (the sequential-GHASH variant tags separately)
+    uint32_t aad_in_stream;     // 1: the AAD blocks ride in the streaming kernel's GHASH (AAD <= 16 L bytes)
 };
 
 hipError_t launch_key_setup(const uint32_t key_words[8], KeyCtx *ctx, hipStream_t s);
