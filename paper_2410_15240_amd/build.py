@@ -28,6 +28,10 @@ def build(verbose: bool = False) -> str:
     cmd = [hipcc(), "--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-shared", "-fvisibility=hidden",
            # keep hipcc from forming packed-FP32 instructions (this code has no FP, the flag is policy)
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           # LLVM's iterative max-occupancy scheduler keeps 4-8 table lookups in
+           # flight per wave in the AES rounds; the default strategy serialises
+           # them to 1-2 once the kernel's live state grows.
+           "-mllvm", "--amdgpu-sched-strategy=iterative-maxocc",
            "-I", os.path.join(ROOT, "include"), "-I", CSRC]
     cmd += [os.path.join(CSRC, s) for s in SOURCES]
     cmd += ["-o", tmp, "-Wl,-rpath,/opt/rocm/lib"]

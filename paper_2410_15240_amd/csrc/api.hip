@@ -150,34 +150,42 @@ int key_ctx(const uint8_t *key, hipStream_t s, int dev, const KeyCtx **out)
     return FASTRACK_OK;
 }
 
-// Scratch of at least `bytes` private to (device, stream): work on one stream is ordered.
+// Scratch of at least `bytes` private to (device, stream): work on one stream
+// is ordered. Zeroed when (re)allocated; every launch rewrites what it reads.
 int scratch_for(int dev, hipStream_t s, size_t bytes, void **out)
 {
-    for (auto &e : g_scratch)
-        if (e.dev == dev && e.stream == s) {
-            if (e.bytes >= bytes) {
-                *out = e.ptr;
-                return FASTRACK_OK;
-            }
-            hipError_t he = hipStreamSynchronize(s);   // earlier launches may still use the old area
-            if (he != hipSuccess)
-                return hip_fail(he, "hipStreamSynchronize");
-            (void)hipFree(e.ptr);
-            e.ptr = nullptr;
-            e.bytes = 0;
-            he = hipMalloc(&e.ptr, bytes);
-            if (he != hipSuccess)
-                return fail(FASTRACK_ENOMEM, "hipMalloc(%zu) for scratch: %s", bytes, hipGetErrorString(he));
-            e.bytes = bytes;
-            *out = e.ptr;
-            return FASTRACK_OK;
-        }
-    ScratchEntry e{dev, s, nullptr, bytes};
-    hipError_t he = hipMalloc(&e.ptr, bytes);
-    if (he != hipSuccess)
+    ScratchEntry *e = nullptr;
+    for (auto &x : g_scratch)
+        if (x.dev == dev && x.stream == s)
+            e = &x;
+    if (e && e->bytes >= bytes) {
+        *out = e->ptr;
+        return FASTRACK_OK;
+    }
+    if (!e) {
+        g_scratch.push_back(ScratchEntry{dev, s, nullptr, 0});
+        e = &g_scratch.back();
+    } else {
+        hipError_t he = hipStreamSynchronize(s);   // earlier launches may still use the old area
+        if (he != hipSuccess)
+            return hip_fail(he, "hipStreamSynchronize");
+        (void)hipFree(e->ptr);
+        e->ptr = nullptr;
+        e->bytes = 0;
+    }
+    hipError_t he = hipMalloc(&e->ptr, bytes);
+    if (he != hipSuccess) {
+        e->ptr = nullptr;
         return fail(FASTRACK_ENOMEM, "hipMalloc(%zu) for scratch: %s", bytes, hipGetErrorString(he));
-    g_scratch.push_back(e);
-    *out = e.ptr;
+    }
+    he = hipMemsetAsync(e->ptr, 0, bytes, s);
+    if (he != hipSuccess) {
+        (void)hipFree(e->ptr);
+        e->ptr = nullptr;
+        return hip_fail(he, "hipMemsetAsync of scratch");
+    }
+    e->bytes = bytes;
+    *out = e->ptr;
     return FASTRACK_OK;
 }
 
@@ -307,13 +315,14 @@ int run_gcm(bool encrypt, const KeyCtx *ctx, const uint8_t *base_iv, uint64_t ch
         return FASTRACK_OK;
     }
     p.do_ghash = 1;
-    p.aad_in_stream = ((aad_bytes + 15) / 16) <= (1u << p.lanes_log2) ? 1u : 0u;
-    {
+    p.split = p.n_items > p.n_chains ? 1u : 0u;
+    if (p.split) {   // chains cut into segments: per-item partials and per-chain masks
         void *sc = nullptr;
-        int rc = scratch_for(dev, s, (size_t)p.n_items * 16, &sc);
+        int rc = scratch_for(dev, s, (size_t)(p.n_items + p.n_chains) * 16, &sc);
         if (rc)
             return rc;
         p.partials = reinterpret_cast<uint4 *>(sc);
+        p.masks = p.partials + p.n_items;
     }
     he = launch_gcm(p, encrypt, num_cu, s);
     if (he != hipSuccess)

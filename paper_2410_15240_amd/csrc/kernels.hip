@@ -6,9 +6,8 @@
 //                      powers of H and the GF(2^128) multiplication tables.
 //   gcm_kernel<ENC>    the streaming hot path: AES-256-CTR keystream XOR the
 //                      data (section 3.2, AES-CTR) fused with GHASH over the
-//                      ciphertext, parallel INSIDE each chain.
-//   finalize_kernel    combines the per-segment GHASH partials of chains that
-//                      were split over several waves, then tags / verifies.
+//                      AAD and ciphertext, parallel INSIDE each chain, and the
+//                      per-chain tag / verification at the end of each chain.
 //   seq_ghash_kernel   the paper's baseline authentication: one sequential
 //                      Horner chain per tag (kept for comparison).
 //
@@ -28,11 +27,11 @@
 // block [len A]_64 || [len C]_64 (lengths in bits):
 //     GHASH(A || C || L) = G_C . H  xor  GHASH(A) . H^(q+1)  xor  L . H
 //     T = GHASH(A || C || L) xor AES_K(J0),   J0 = IV_i || 0^31 || 1.
-// The streaming kernel produces G_C . H, with the AAD blocks folded into the
-// same Horner streams (they are the blocks that precede the first ciphertext
-// block) and, for a chain cut into segments, each segment's weight inside the
-// chain applied. The finalize kernel XORs a chain's partials and adds L . H and
-// AES_K(J0).
+// The AAD blocks ride in the same Horner streams (they are the blocks that
+// precede the first ciphertext block), so a chain's streams sum to
+// GHASH(A || C) . H = G_C . H xor GHASH(A) . H^(q+1). A chain cut into segments
+// applies each segment's weight inside the chain and gathers the segments by
+// atomic XOR; whoever holds the complete sum adds L . H and AES_K(J0).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -314,18 +313,141 @@ __device__ inline u4 coop_mul_tab4(const u4 &x, const Tab4 *__restrict__ t, uint
     return wave_xor(r);
 }
 
-// AAD block u of a chain's AAD (zero-padded).
+// AAD block u of a chain's AAD (zero-padded); one vector load when it is whole and aligned.
 __device__ __forceinline__ u4 aad_block(const uint8_t *aad, uint32_t u, uint32_t aad_bytes)
 {
     const uint32_t left = aad_bytes - 16u * u;
-    return load_bytes(aad + 16u * u, left < 16u ? left : 16u);
+    const uint8_t *a = aad + 16u * u;
+    if (left >= 16u && ((uintptr_t)a & 15) == 0) {
+        const uint4 x = *reinterpret_cast<const uint4 *>(a);
+        const u4 r = {{x.x, x.y, x.z, x.w}};
+        return r;
+    }
+    return load_bytes(a, left < 16u ? left : 16u);
+}
+
+// L . H for the two length blocks of a launch, L = [len A]_64 || [len C]_64 in
+// bits, with len C the full chain length (lanes 0..31) or the last chain's
+// (lanes 32..63). Each lane looks up one nibble position of its L in the 4-bit
+// table of H, and each half of the wave XOR-sums its 32 entries.
+struct LenTerms {
+    u4 full, last;
+};
+__device__ inline LenTerms len_terms(const GcmLaunch &p, uint32_t lane)
+{
+    const uint64_t abits = (uint64_t)p.aad_bytes * 8;
+    const uint64_t cbits = (lane < 32 ? p.chain_bytes : p.last_len) * 8;
+    const uint32_t pos = lane & 31;                         // nibble position: degrees 4 pos .. 4 pos + 3
+    const uint64_t half = pos < 16 ? abits : cbits;         // bytes 0..7 hold len A, 8..15 len C (big-endian)
+    const uint32_t byte = (uint32_t)(half >> (8 * (7 - ((pos >> 1) & 7)))) & 0xFFu;
+    const uint32_t nib = (pos & 1) ? (byte & 0xFu) : (byte >> 4);
+    const uint4 e = *reinterpret_cast<const uint4 *>(p.ctx->h1_tab.e[pos][nib]);
+    u4 r = {{e.x, e.y, e.z, e.w}};
+#pragma unroll
+    for (int off = 16; off >= 1; off >>= 1)
+        for (int w = 0; w < 4; ++w)
+            r.w[w] ^= __shfl_xor(r.w[w], off, 64);
+    LenTerms t;
+    for (int w = 0; w < 4; ++w) {
+        t.full.w[w] = __builtin_amdgcn_readlane(r.w[w], 0);
+        t.last.w[w] = __builtin_amdgcn_readlane(r.w[w], 32);
+    }
+    return t;
+}
+
+// 16 bytes at p, read as one vector load when p is 16-byte aligned.
+__device__ __forceinline__ u4 load16(const uint8_t *p)
+{
+    if (((uintptr_t)p & 15) == 0) {
+        const uint4 x = *reinterpret_cast<const uint4 *>(p);
+        const u4 r = {{x.x, x.y, x.z, x.w}};
+        return r;
+    }
+    return load_bytes(p, 16);
+}
+
+// Encrypt: store the tag. Decrypt: ok = (tag == the received tag `got`).
+template <bool ENC>
+__device__ inline void emit_tag(const GcmLaunch &p, uint64_t gchain, const u4 &tag, const u4 &got)
+{
+    if (ENC) {
+        uint8_t *dst = p.tags_out + 16 * gchain;
+        if (((uintptr_t)dst & 15) == 0)
+            *reinterpret_cast<uint4 *>(dst) = make_uint4(tag.w[0], tag.w[1], tag.w[2], tag.w[3]);
+        else
+            store_bytes(dst, tag, 16);
+    } else {
+        const uint32_t d = (got.w[0] ^ tag.w[0]) | (got.w[1] ^ tag.w[1]) | (got.w[2] ^ tag.w[2]) |
+                           (got.w[3] ^ tag.w[3]);
+        p.ok[gchain] = d == 0 ? 1 : 0;
+    }
+}
+
+// AES-256 of one block x (before the first AddRoundKey) with the streaming
+// kernel's LDS T-tables: every lane encrypts its own block.
+__device__ inline u4 aes_block_lds(const char *lds, const uint32_t *rk, const u4 &x, uint32_t lc0, uint32_t lc1,
+                                   uint32_t lc2, uint32_t lc3)
+{
+    uint32_t s0 = x.w[0] ^ rk[0], s1 = x.w[1] ^ rk[1], s2 = x.w[2] ^ rk[2], s3 = x.w[3] ^ rk[3];
+#pragma unroll
+    for (int r = 1; r < 14; ++r) {
+        const uint32_t n0 = xor3(tlk(lds, s0, lc0, FT_SEL(0)), tlk(lds, s1, lc1, FT_SEL(1)),
+                                 xor3(tlk(lds, s2, lc2, FT_SEL(2)), tlk(lds, s3, lc3, FT_SEL(3)), rk[4 * r + 0]));
+        const uint32_t n1 = xor3(tlk(lds, s1, lc0, FT_SEL(0)), tlk(lds, s2, lc1, FT_SEL(1)),
+                                 xor3(tlk(lds, s3, lc2, FT_SEL(2)), tlk(lds, s0, lc3, FT_SEL(3)), rk[4 * r + 1]));
+        const uint32_t n2 = xor3(tlk(lds, s2, lc0, FT_SEL(0)), tlk(lds, s3, lc1, FT_SEL(1)),
+                                 xor3(tlk(lds, s0, lc2, FT_SEL(2)), tlk(lds, s1, lc3, FT_SEL(3)), rk[4 * r + 2]));
+        const uint32_t n3 = xor3(tlk(lds, s3, lc0, FT_SEL(0)), tlk(lds, s0, lc1, FT_SEL(1)),
+                                 xor3(tlk(lds, s1, lc2, FT_SEL(2)), tlk(lds, s2, lc3, FT_SEL(3)), rk[4 * r + 3]));
+        s0 = n0; s1 = n1; s2 = n2; s3 = n3;
+    }
+    const uint32_t st[4] = {s0, s1, s2, s3};
+    u4 o;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const uint32_t a0 = tlk(lds, st[j], lc0, FT_SEL(0));
+        const uint32_t a1 = tlk(lds, st[(j + 1) & 3], lc1, FT_SEL(1));
+        const uint32_t a2 = tlk(lds, st[(j + 2) & 3], lc2, FT_SEL(2));
+        const uint32_t a3 = tlk(lds, st[(j + 3) & 3], lc3, FT_SEL(3));
+        o.w[j] = xor3(__builtin_amdgcn_perm(a1, a0, 0x0C0C0601u), __builtin_amdgcn_perm(a3, a2, 0x04030C0Cu),
+                      rk[56 + j]);
+    }
+    return o;
+}
+
+// acc . H^L xor g with the 8-bit table of H^L in LDS: byte positions 0..7
+// directly, 8..15 through x^64.
+__device__ __forceinline__ u4 ghash_step(const uint4 *lds4, const u4 &acc, const u4 &g)
+{
+    u4 lo = g, hi = zero4();
+#pragma unroll
+    for (int kb = 0; kb < 8; kb += 2) {
+        const uint32_t a0 = (acc.w[kb >> 2] >> (8 * (kb & 3))) & 0xFFu;
+        const uint32_t a1 = (acc.w[kb >> 2] >> (8 * ((kb + 1) & 3))) & 0xFFu;
+        const uint32_t b0 = (acc.w[2 + (kb >> 2)] >> (8 * (kb & 3))) & 0xFFu;
+        const uint32_t b1 = (acc.w[2 + (kb >> 2)] >> (8 * ((kb + 1) & 3))) & 0xFFu;
+        const uint4 ea = lds4[kG8Base + ((kb << 8) | a0)];
+        const uint4 eb = lds4[kG8Base + (((kb + 1) << 8) | a1)];
+        const uint4 fa = lds4[kG8Base + ((kb << 8) | b0)];
+        const uint4 fb = lds4[kG8Base + (((kb + 1) << 8) | b1)];
+        lo.w[0] = xor3(lo.w[0], ea.x, eb.x);
+        lo.w[1] = xor3(lo.w[1], ea.y, eb.y);
+        lo.w[2] = xor3(lo.w[2], ea.z, eb.z);
+        lo.w[3] = xor3(lo.w[3], ea.w, eb.w);
+        hi.w[0] = xor3(hi.w[0], fa.x, fb.x);
+        hi.w[1] = xor3(hi.w[1], fa.y, fb.y);
+        hi.w[2] = xor3(hi.w[2], fa.z, fb.z);
+        hi.w[3] = xor3(hi.w[3], fa.w, fb.w);
+    }
+    return xor4(lo, mul_x64(hi));
 }
 
 // Lanes per item L = 2^LL. Item slot g of a wave (lanes g*L .. g*L+L-1) takes
 // L consecutive blocks of its segment per iteration; each lane keeps a Horner
 // accumulator with multiplier H^L, and lane j's accumulator carries the weight
-// H^(L-j) in its segment (times one more H for the tag).
-template <bool ENC, int LL>
+// H^(L-j) in its segment (times one more H for the tag). SPLIT (64 lanes only):
+// chains are cut into segments whose partials a second kernel sums.
+template <bool ENC, int LL, bool SPLIT>
 __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
 {
     constexpr uint32_t L = 1u << LL;
@@ -357,13 +479,13 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
 
     const uint32_t lb = (lane & 31) << 2;
     const uint32_t lc0 = lb, lc1 = lb | 0x80u, lc2 = lb | 0x10000u, lc3 = lb | 0x10080u;
-    // Round keys 0..2 and 4..7 are used once per item (scalar registers); the
-    // rest once per block (vector registers).
+    // The 60 round-key words live in vector registers: the scalar file is
+    // taken by the launch parameters and per-item state.
     uint32_t rk[60];
 #pragma unroll
     for (int i = 0; i < 60; ++i) {
         const uint32_t w = __builtin_amdgcn_readfirstlane(c->rk[i]);
-        rk[i] = (i < 8 && i != 3) ? w : in_vgpr(w);
+        rk[i] = in_vgpr(w);
     }
 
     const uint64_t nwaves = (uint64_t)gridDim.x * kWavesPerWg;
@@ -371,7 +493,23 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
     const uint64_t n_wave_items = (p.n_items + G - 1) / G;
     const uint32_t seg = 1u << p.seg_log2;
     const uint32_t Ku = ((seg < p.qc ? seg : p.qc) + L - 1) >> LL;   // iterations per item, uniform
-    for (uint64_t wi = wave; wi < n_wave_items; wi += nwaves) {
+    // The tag mask AES_K(J0) xor L . H of the chains of this wave's next L
+    // wave-items, one per lane: lane b*G + g holds the mask of slot g of the b-th
+    // of them. One lane-parallel AES pass serves L wave-items.
+    u4 jmask = zero4();
+    uint32_t it = 0;   // wave-items done by this wave
+    for (uint64_t wi = wave; wi < n_wave_items; wi += nwaves, ++it) {
+        const uint32_t bi = it & (L - 1);
+        if (p.do_ghash && bi == 0) {
+            const uint64_t bitem = (wi + (uint64_t)(lane >> (6 - LL)) * nwaves) * G + (lane & (G - 1));
+            const ItemPos bp = item_pos(p, bitem < p.n_items ? bitem : p.n_items - 1);
+            uint32_t biv[3];
+            chain_iv(p, p.chain_base + bp.chain, biv);
+            const u4 j0 = {{biv[0], biv[1], biv[2], bswap32(1u)}};   // J0 = IV_i || 0^31 || 1
+            const LenTerms lt = len_terms(p, lane);
+            jmask = xor4(aes_block_lds(lds, rk, j0, lc0, lc1, lc2, lc3),
+                         bp.chain == p.n_chains - 1 ? lt.last : lt.full);
+        }
         const uint64_t item = wi * G + gs;
         const bool valid = item < p.n_items;
         const ItemPos ip = item_pos(p, valid ? item : p.n_items - 1);
@@ -394,26 +532,43 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
         const bool last_chain = ip.chain == p.n_chains - 1;
         const uint32_t tail = last_chain ? (uint32_t)(p.last_len & 15) : 0u;   // bytes of a final partial block
         const int pad = (int)((Ku << LL) - (ip.e - ip.b));                   // zero blocks in front
-        // The AAD blocks precede ciphertext block 0 of the chain in GHASH order, so in
-        // segment 0 AAD block u takes virtual slot (a - u) before it: a padding slot, or
-        // a slot of a virtual iteration -1 that seeds the accumulator.
-        // With at most L AAD blocks each lane holds at most one: the block whose slot
-        // is congruent to the lane, at block index va in [-na, 0) of iteration ka.
-        const int na = (p.aad_in_stream && ip.s == 0 && valid) ? (int)((p.aad_bytes + 15) >> 4) : 0;
-        const int rr = ((int)jl - pad) & (int)(L - 1);
-        const int va = rr == 0 ? -(int)L : rr - (int)L;
-        const bool has_aad = va >= -na;
-        const int ka = (va + pad - (int)jl) >> LL;        // -1 seeds the accumulator
-        u4 aadv = zero4();
-        if (has_aad)
-            aadv = aad_block(p.aad + gchain * p.aad_bytes, (uint32_t)(va + na), p.aad_bytes);
-        u4 acc = (has_aad && ka < 0) ? aadv : zero4();
-        const bool seeded = __any(na > pad);   // some lane starts from an AAD block
-        // Last iteration that carries an AAD block in any lane of the wave.
-        int ka_w = has_aad ? ka : -2;
+        // The AAD blocks precede ciphertext block 0 of the chain in GHASH order: in
+        // segment 0, AAD block u takes the slot v = u - na just before it. Lane jl
+        // holds the slots v = k L + jl - pad, so its AAD blocks fall in iterations
+        // k_lo..k_hi; those below 0 are extra iterations ahead of the data that only
+        // feed GHASH, the others are padding slots of the first iterations.
+        const int na = (ip.s == 0 && valid && p.do_ghash) ? (int)((p.aad_bytes + 15) >> 4) : 0;
+        const uint8_t *aad_c = p.aad + gchain * p.aad_bytes;
+        int k_lo = 0, k_hi = -1;
+        if (na) {
+            k_lo = (pad - na - (int)jl + (int)L - 1) >> LL;   // ceil((pad - na - jl) / L)
+            k_hi = (pad - 1 - (int)jl) >> LL;                 // floor((pad - 1 - jl) / L)
+            if (k_lo > k_hi) {
+                k_lo = 0;
+                k_hi = -1;
+            }
+        }
+        int kmin = k_lo < 0 ? k_lo : 0, kmax = k_hi;
 #pragma unroll
-        for (int off = 32; off >= 1; off >>= 1)
-            ka_w = max(ka_w, __shfl_xor(ka_w, off, 64));
+        for (int off = 32; off >= 1; off >>= 1) {
+            kmin = min(kmin, __shfl_xor(kmin, off, 64));
+            kmax = max(kmax, __shfl_xor(kmax, off, 64));
+        }
+        kmin = __builtin_amdgcn_readfirstlane(kmin);
+        kmax = __builtin_amdgcn_readfirstlane(kmax);
+        u4 acc = zero4();
+        if (kmin == -1) {
+            // One extra iteration (at most L AAD blocks in front): its blocks seed the
+            // accumulators directly, and the loads complete under the first iteration.
+            if (k_lo == -1)
+                acc = aad_block(aad_c, (uint32_t)(jl - (int)L - pad + na), p.aad_bytes);
+        } else {
+            for (int k = kmin; k < 0; ++k) {
+                const int v = k * (int)L + (int)jl - pad;
+                const u4 g = v >= -na ? aad_block(aad_c, (uint32_t)(v + na), p.aad_bytes) : zero4();
+                acc = k == kmin ? g : ghash_step(lds4, acc, g);
+            }
+        }
         for (uint32_t k = 0; k < Ku; ++k) {
             const int v = (int)(k << LL) + (int)jl - pad;
             const bool active = valid && v >= 0;
@@ -482,34 +637,9 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
                         }
                     }
                 }
-                if ((int)k <= ka_w && has_aad && (int)k == ka)   // an AAD block in a padding slot
-                    g = aadv;
-                if (k == 0 && !seeded) {
-                    acc = g;
-                } else {
-                    // acc <- acc . H^L xor g: positions 0..7 directly, 8..15 through x^64.
-                    u4 lo = g, hi = zero4();
-#pragma unroll
-                    for (int kb = 0; kb < 8; kb += 2) {
-                        const uint32_t a0 = (acc.w[kb >> 2] >> (8 * (kb & 3))) & 0xFFu;
-                        const uint32_t a1 = (acc.w[kb >> 2] >> (8 * ((kb + 1) & 3))) & 0xFFu;
-                        const uint32_t b0 = (acc.w[2 + (kb >> 2)] >> (8 * (kb & 3))) & 0xFFu;
-                        const uint32_t b1 = (acc.w[2 + (kb >> 2)] >> (8 * ((kb + 1) & 3))) & 0xFFu;
-                        const uint4 ea = lds4[kG8Base + ((kb << 8) | a0)];
-                        const uint4 eb = lds4[kG8Base + (((kb + 1) << 8) | a1)];
-                        const uint4 fa = lds4[kG8Base + ((kb << 8) | b0)];
-                        const uint4 fb = lds4[kG8Base + (((kb + 1) << 8) | b1)];
-                        lo.w[0] = xor3(lo.w[0], ea.x, eb.x);
-                        lo.w[1] = xor3(lo.w[1], ea.y, eb.y);
-                        lo.w[2] = xor3(lo.w[2], ea.z, eb.z);
-                        lo.w[3] = xor3(lo.w[3], ea.w, eb.w);
-                        hi.w[0] = xor3(hi.w[0], fa.x, fb.x);
-                        hi.w[1] = xor3(hi.w[1], fa.y, fb.y);
-                        hi.w[2] = xor3(hi.w[2], fa.z, fb.z);
-                        hi.w[3] = xor3(hi.w[3], fa.w, fb.w);
-                    }
-                    acc = xor4(lo, mul_x64(hi));
-                }
+                if ((int)k <= kmax && v < 0 && v >= -na)        // an AAD block in a padding slot
+                    g = aad_block(aad_c, (uint32_t)(v + na), p.aad_bytes);
+                acc = (k == 0 && kmin == 0) ? g : ghash_step(lds4, acc, g);
             }
         }
         if (p.do_ghash) {
@@ -519,47 +649,62 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
             for (uint32_t off = L / 2; off >= 1; off >>= 1)
                 for (int w = 0; w < 4; ++w)
                     acc.w[w] ^= __shfl_xor(acc.w[w], off, 64);
-            if (LL == 6) {
+            if (SPLIT) {
                 // A chain cut into S segments (only with 64 lanes per item): segment s
-                // carries the weight H^((S-1-s) . 2^seg_log2) inside its chain.
+                // carries the weight H^((S-1-s) . 2^seg_log2) inside its chain. The
+                // partials and segment 0's mask go to memory; the chain kernel sums them.
                 uint32_t m = ip.S - 1 - ip.s;
                 while (m) {
                     const uint32_t b = __builtin_ctz(m);
                     acc = coop_mul_tab4(acc, &c->sq_tab[p.seg_log2 + b], lane);
                     m &= m - 1;
                 }
+                const uint32_t src_lane = bi * G + gs;
+                u4 e;
+                for (int w = 0; w < 4; ++w)
+                    e.w[w] = __shfl(jmask.w[w], (int)src_lane, 64);
+                if (lane == 0) {
+                    p.partials[item] = make_uint4(acc.w[0], acc.w[1], acc.w[2], acc.w[3]);
+                    if (ip.s == 0)
+                        p.masks[ip.chain] = make_uint4(e.w[0], e.w[1], e.w[2], e.w[3]);
+                }
+            } else {
+                // The slot holds its chain's whole GHASH(A || C) . H:
+                // T = GHASH(A || C) . H xor L . H xor AES_K(J0).
+                u4 e;
+                for (int w = 0; w < 4; ++w)
+                    e.w[w] = __shfl(jmask.w[w], (int)(bi * G + gs), 64);
+                if (valid && jl == 0)
+                    emit_tag<ENC>(p, gchain, xor4(acc, e), ENC ? zero4() : load16(p.tags_in + 16 * gchain));
             }
-            if (jl == 0 && valid)
-                p.partials[item] = make_uint4(acc.w[0], acc.w[1], acc.w[2], acc.w[3]);
         }
     }
 }
 
-// ===========================================================================
-// Per-chain tag: T = G_C.H xor GHASH(A).H^(q+1) xor L.H xor AES_K(J0)
-// ===========================================================================
-
-// GHASH(A) . H^(q+1) for global chain `gchain` (q ciphertext blocks).
-__device__ inline u4 aad_term(const GcmLaunch &p, uint64_t gchain, uint32_t q)
+// Chains cut into segments: T = mask xor the XOR of the chain's weighted
+// partials, one thread per chain.
+template <bool ENC>
+__global__ __launch_bounds__(256) void chain_tag_kernel(GcmLaunch p)
 {
-    const KeyCtx *c = p.ctx;
-    u4 y = zero4();
-    const uint8_t *a = p.aad + gchain * p.aad_bytes;
-    for (uint32_t off = 0; off < p.aad_bytes; off += 16) {
-        const uint32_t n = p.aad_bytes - off < 16 ? p.aad_bytes - off : 16;
-        y = mul_tab4(xor4(y, load_bytes(a + off, n)), &c->h1_tab);
+    const uint32_t chain = blockIdx.x * blockDim.x + threadIdx.x;
+    if (chain >= p.n_chains)
+        return;
+    const uint64_t gchain = p.chain_base + chain;
+    const uint32_t S = chain == p.n_chains - 1 ? p.segs_last : p.segs_full;
+    const u4 got = ENC ? zero4() : load16(p.tags_in + 16 * gchain);
+    const uint4 m = p.masks[chain];
+    u4 tag = {{m.x, m.y, m.z, m.w}};
+    const uint4 *part = p.partials + (uint64_t)chain * p.segs_full;
+    for (uint32_t s = 0; s < S; ++s) {
+        const uint4 g = part[s];
+        tag.w[0] ^= g.x; tag.w[1] ^= g.y; tag.w[2] ^= g.z; tag.w[3] ^= g.w;
     }
-    return mul_hpow(y, q + 1u, c);
+    emit_tag<ENC>(p, gchain, tag, got);
 }
 
-// L . H, L = [len A]_64 || [len C]_64 in bits.
-__device__ inline u4 len_term(const GcmLaunch &p, uint64_t len_i)
-{
-    const uint64_t abits = (uint64_t)p.aad_bytes * 8, cbits = len_i * 8;
-    const u4 lens = {{bswap32((uint32_t)(abits >> 32)), bswap32((uint32_t)abits), bswap32((uint32_t)(cbits >> 32)),
-                      bswap32((uint32_t)cbits)}};
-    return mul_tab4(lens, &p.ctx->h1_tab);
-}
+// ===========================================================================
+// Baseline: sequential GHASH
+// ===========================================================================
 
 template <class LK>
 __device__ inline u4 j0_mask(const GcmLaunch &p, uint64_t gchain, LK T)
@@ -568,46 +713,6 @@ __device__ inline u4 j0_mask(const GcmLaunch &p, uint64_t gchain, LK T)
     chain_iv(p, gchain, iv);
     const u4 j0 = {{iv[0], iv[1], iv[2], bswap32(1u)}};
     return aes256_encrypt_tt(j0, p.ctx->rk, T);
-}
-
-template <bool ENC>
-__device__ inline void emit_tag(const GcmLaunch &p, uint64_t gchain, const u4 &tag)
-{
-    if (ENC) {
-        store_bytes(p.tags_out + 16 * gchain, tag, 16);
-    } else {
-        const u4 got = load_bytes(p.tags_in + 16 * gchain, 16);
-        const uint32_t d = (got.w[0] ^ tag.w[0]) | (got.w[1] ^ tag.w[1]) | (got.w[2] ^ tag.w[2]) |
-                           (got.w[3] ^ tag.w[3]);
-        p.ok[gchain] = d == 0 ? 1 : 0;
-    }
-}
-
-// One thread per chain: the XOR of the chain's (already weighted) partials,
-// the AAD term when the AAD did not ride in the stream, L . H and AES_K(J0).
-template <bool ENC>
-__global__ __launch_bounds__(256) void finalize_kernel(GcmLaunch p)
-{
-    __shared__ uint32_t s_t0[256];
-    s_t0[threadIdx.x] = p.ctx->t0[threadIdx.x];
-    __syncthreads();
-    const uint32_t chain = blockIdx.x * blockDim.x + threadIdx.x;
-    if (chain >= p.n_chains)
-        return;
-    const uint64_t gchain = p.chain_base + chain;
-    const bool last = chain == p.n_chains - 1;
-    const uint64_t len_i = last ? p.last_len : p.chain_bytes;
-    const uint32_t q = last ? p.q_last : p.qc;
-    const uint32_t S = last ? p.segs_last : p.segs_full;
-    u4 tag = xor4(len_term(p, len_i), j0_mask(p, gchain, [&](uint32_t x) { return s_t0[x]; }));
-    const uint4 *part = p.partials + (uint64_t)chain * p.segs_full;
-    for (uint32_t s = 0; s < S; ++s) {
-        const uint4 g = part[s];
-        tag.w[0] ^= g.x; tag.w[1] ^= g.y; tag.w[2] ^= g.z; tag.w[3] ^= g.w;
-    }
-    if (p.aad_bytes && !p.aad_in_stream)
-        tag = xor4(tag, aad_term(p, gchain, q));
-    emit_tag<ENC>(p, gchain, tag);
 }
 
 // The paper's baseline authentication: one thread per chain, Horner with H over
@@ -646,7 +751,7 @@ __global__ __launch_bounds__(256) void seq_ghash_kernel(GcmLaunch p)
                       bswap32((uint32_t)cbits)}};
     y = mul_tab4(xor4(y, lens), hT);
     const u4 tag = xor4(y, j0_mask(p, gchain, [&](uint32_t x) { return s_t0[x]; }));
-    emit_tag<ENC>(p, gchain, tag);
+    emit_tag<ENC>(p, gchain, tag, ENC ? zero4() : load16(p.tags_in + 16 * gchain));
 }
 
 template <bool ENC>
@@ -660,15 +765,17 @@ static hipError_t launch_gcm_t(const GcmLaunch &p, int num_cu, hipStream_t s)
     if (wgs > (uint64_t)num_cu)
         wgs = (uint64_t)num_cu;
     if (p.lanes_log2 == 4)
-        hipLaunchKernelGGL((gcm_kernel<ENC, 4>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+        hipLaunchKernelGGL((gcm_kernel<ENC, 4, false>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
     else if (p.lanes_log2 == 5)
-        hipLaunchKernelGGL((gcm_kernel<ENC, 5>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+        hipLaunchKernelGGL((gcm_kernel<ENC, 5, false>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+    else if (!p.split)
+        hipLaunchKernelGGL((gcm_kernel<ENC, 6, false>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
     else
-        hipLaunchKernelGGL((gcm_kernel<ENC, 6>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+        hipLaunchKernelGGL((gcm_kernel<ENC, 6, true>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || !p.do_ghash)
+    if (e != hipSuccess || !p.do_ghash || !p.split)
         return e;
-    hipLaunchKernelGGL(finalize_kernel<ENC>, dim3((p.n_chains + 255) / 256), dim3(256), 0, s, p);
+    hipLaunchKernelGGL(chain_tag_kernel<ENC>, dim3((p.n_chains + 255) / 256), dim3(256), 0, s, p);
     return hipGetLastError();
 }
 

@@ -42,9 +42,14 @@ struct GcmLaunch {
     const uint8_t *tags_in;     // decrypt: received tags, global chain i at tags_in + 16 i
     uint8_t *tags_out;          // encrypt: produced tags
     uint8_t *ok;                // decrypt: ok[global chain] = 1 accept / 0 reject
-    uint4 *partials;            // per-item GHASH partials, already weighted within their chain
+    // Launches that cut chains into several segments (split = 1) leave each
+    // item's weighted GHASH partial in partials[item] and, from segment 0, the
+    // chain's mask AES_K(J0) xor L . H in masks[chain]; a per-chain kernel then
+    // sums them into the tag. Otherwise every item is a whole chain and tags it.
+    uint4 *partials;
+    uint4 *masks;
+    uint32_t split;
     uint32_t do_ghash;          // 0: keystream only (the sequential-GHASH variant tags separately)
-    uint32_t aad_in_stream;     // 1: the AAD blocks ride in the streaming kernel's GHASH (AAD <= 16 L bytes)
 };
 
 hipError_t launch_key_setup(const uint32_t key_words[8], KeyCtx *ctx, hipStream_t s);

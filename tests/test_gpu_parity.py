@@ -72,6 +72,9 @@ SMALL = [
     (16, 16, 0), (17, 16, 0), (1, 1024, 0), (15, 4096, 1), (4096, 4096, 0), (1000, 64, 1), (5000, 1024, 32),
     (65536 + 48, 4096, 0), (100000 + 5, 16384, 13), (1 << 20, 65536, 0), (3 * 65536 + 16, 65536, 32),
     ((1 << 20) + 7, 1 << 20, 0), (777777, 1 << 20, 32), (2 * MiB + 100, 256 * KiB, 16),
+    # AAD longer than one iteration of lanes: GHASH-only iterations ahead of the data
+    (3 * 4096 + 5, 4096, 1000), (3 * 65536 + 16, 65536, 2000), (2 * MiB + 100, 256 * KiB, 5003),
+    (40, 16, 100),
 ]
 
 
