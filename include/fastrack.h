@@ -91,21 +91,26 @@ int fastrack_gcm_encrypt_tag(const uint8_t *key, const uint8_t *base_iv, uint64_
                              const uint8_t *d_pt, uint64_t len, const uint8_t *d_aad, uint32_t aad_bytes,
                              uint8_t *d_ct, uint8_t *d_tags, uint32_t flags, void *stream);
 
-/* Bytes of device staging that fastrack_pipeline_h2d needs for these sizes. */
+/* Bytes of device staging that fastrack_pipeline_h2d needs for these sizes
+ * (0 for an invalid depth or chain_bytes = 0). */
 uint64_t fastrack_pipeline_stage_bytes(uint64_t len, uint64_t chain_bytes, uint32_t aad_bytes,
                                        uint64_t chunk_bytes, int depth);
 
 /*
  * Pipelined host-to-device decrypt + verify (paper section 5.3, decryption
  * pipeline): ciphertext in a pinned host "bounce buffer" (section 3.1) is
- * copied in chunks of chunk_bytes on copy_stream into a ring of `depth`
- * device staging slots, and each chunk's chains are decrypted and verified on
- * compute_stream while the next chunks are in flight.
+ * copied in chunks of chunk_bytes on copy_stream, and each chunk's chains are
+ * decrypted and verified on compute_stream while the next chunks are in flight.
  *   h_ct         [len] ciphertext, PINNED host memory (ENOTPINNED otherwise)
  *   h_tags       [n][16] host tags; h_aad [n][aad_bytes] host AAD (or NULL)
  *   chunk_bytes  a nonzero multiple of chain_bytes
- *   depth        2 or 3
- *   d_stage      device workspace of stage_bytes >= fastrack_pipeline_stage_bytes(...)
+ *   depth        0: each chunk is copied to its place in d_pt and decrypted in
+ *                place (no slot is reused, so the copies never wait);
+ *                2..8: a ring of `depth` device staging slots in d_stage, the
+ *                copy into a slot waiting for the decrypt that last used it
+ *   d_stage      device workspace, 256-byte aligned, of
+ *                stage_bytes >= fastrack_pipeline_stage_bytes(...): the ring
+ *                (depth > 0), then the tags and the AAD
  *   d_pt, d_ok   device outputs as in fastrack_gcm_decrypt_verify
  * Results are valid once compute_stream has completed (it waits on the copies).
  * EINVAL additionally covers chunk_bytes, depth and an undersized d_stage.

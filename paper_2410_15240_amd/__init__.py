@@ -137,7 +137,7 @@ def encrypt_tag(key, base_iv, chain_bytes, pt, aad=None, out=None, tags=None, fl
     return out, tags
 
 
-def pipeline_h2d(key, base_iv, chain_bytes, h_ct, h_tags, h_aad=None, chunk_bytes=8 << 20, depth=2, stage=None,
+def pipeline_h2d(key, base_iv, chain_bytes, h_ct, h_tags, h_aad=None, chunk_bytes=8 << 20, depth=0, stage=None,
                  out=None, ok=None, copy_stream=None, compute_stream=None, device=None):
     """Chunked H2D copy of pinned ciphertext overlapped with decrypt + verify. Returns (pt, ok) on the device."""
     if not (isinstance(h_ct, _torch.Tensor) and h_ct.device.type == "cpu" and h_ct.dtype == _torch.uint8):

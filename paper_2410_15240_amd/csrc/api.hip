@@ -41,6 +41,7 @@ int hip_fail(hipError_t e, const char *what)
 constexpr uint64_t kMaxChainBlocks = 0xFFFFFFFEull;   // GCM: at most 2^32 - 2 blocks per message
 constexpr size_t kMaxKeys = 8;
 constexpr int kMinSegLog2 = 8;                          // segments of >= 256 blocks (4 per lane)
+constexpr int kMaxPipelineDepth = 8;                    // staging-ring slots
 
 struct KeyEntry {
     int dev;
@@ -397,7 +398,7 @@ FT_EXPORT int fastrack_gcm_encrypt_tag(const uint8_t *key, const uint8_t *base_i
 FT_EXPORT uint64_t fastrack_pipeline_stage_bytes(uint64_t len, uint64_t chain_bytes, uint32_t aad_bytes,
                                                  uint64_t chunk_bytes, int depth)
 {
-    if (chain_bytes == 0 || depth < 1)
+    if (chain_bytes == 0 || depth < 0 || depth == 1 || depth > kMaxPipelineDepth)
         return 0;
     const uint64_t n = (len + chain_bytes - 1) / chain_bytes;
     return (uint64_t)depth * round256(chunk_bytes) + round256(16 * n) + round256((uint64_t)aad_bytes * n);
@@ -417,8 +418,8 @@ FT_EXPORT int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, 
         return fail(FASTRACK_EINVAL, "h_tags, d_ok and d_stage must be non-NULL");
     if (chunk_bytes == 0 || chunk_bytes % chain_bytes != 0)
         return fail(FASTRACK_EINVAL, "chunk_bytes must be a nonzero multiple of chain_bytes");
-    if (depth != 2 && depth != 3)
-        return fail(FASTRACK_EINVAL, "depth must be 2 or 3");
+    if (depth < 0 || depth == 1 || depth > kMaxPipelineDepth)
+        return fail(FASTRACK_EINVAL, "depth must be 0 (in place) or 2..%d (staging ring)", kMaxPipelineDepth);
     if ((uintptr_t)d_stage & 255)
         return fail(FASTRACK_EINVAL, "d_stage must be 256-byte aligned");
     const uint64_t need = fastrack_pipeline_stage_bytes(len, chain_bytes, aad_bytes, chunk_bytes, depth);
@@ -448,12 +449,16 @@ FT_EXPORT int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, 
     uint8_t *d_tags = d_stage + (uint64_t)depth * slot_bytes;
     uint8_t *d_aad = d_tags + round256(16 * n);
 
+    // Event pools: copied[k % P] is waited on by the compute stream right after
+    // it is recorded, freed[k % P] at most two chunks later, so P = 4 suffices
+    // (a wait takes the event's state at the time it is enqueued).
+    constexpr int P = 4;
     std::vector<hipEvent_t> ev;
     auto cleanup = [&]() {
         for (auto e : ev)
             (void)hipEventDestroy(e);
     };
-    for (int i = 0; i < 2 * depth + 1; ++i) {
+    for (int i = 0; i < 2 * P + 1; ++i) {
         hipEvent_t e;
         he = hipEventCreateWithFlags(&e, hipEventDisableTiming);
         if (he != hipSuccess) {
@@ -463,7 +468,7 @@ FT_EXPORT int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, 
         ev.push_back(e);
     }
     hipEvent_t meta = ev[0];
-    hipEvent_t *copied = &ev[1], *freed = &ev[1 + depth];
+    hipEvent_t *copied = &ev[1], *freed = &ev[1 + P];
 
     he = hipMemcpyAsync(d_tags, h_tags, 16 * n, hipMemcpyHostToDevice, cs);
     if (he == hipSuccess && aad_bytes)
@@ -476,35 +481,45 @@ FT_EXPORT int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, 
         cleanup();
         return hip_fail(he, "pipeline tag/AAD upload");
     }
+    // depth 0: each chunk is copied straight to its place in d_pt and decrypted
+    // there, so no buffer is reused and the copy stream never waits. A ring of
+    // `depth` slots must not overwrite slot k % depth before chunk k - depth is
+    // decrypted; the copy stream waits for the decrypt two chunks back, which
+    // covers the next depth - 1 copies and, with decrypts faster than copies,
+    // has finished by then (a wait on copy_stream costs the copy engine time).
     const uint64_t nchunks = (len + chunk_bytes - 1) / chunk_bytes;
     const uint64_t cpc = chunk_bytes / chain_bytes;
+    int64_t covered = -1;   // copies up to this chunk index have their slot's wait enqueued
     for (uint64_t k = 0; k < nchunks; ++k) {
-        const int slot = (int)(k % (uint64_t)depth);
         const uint64_t off = k * chunk_bytes;
         const uint64_t bytes = len - off < chunk_bytes ? len - off : chunk_bytes;
-        uint8_t *stage = d_stage + (uint64_t)slot * slot_bytes;
-        if (k >= (uint64_t)depth)
-            he = hipStreamWaitEvent(cs, freed[slot], 0);   // the slot's previous chunk has been decrypted
+        uint8_t *buf = depth == 0 ? d_pt + off : d_stage + (k % (uint64_t)depth) * slot_bytes;
+        if (depth && k >= (uint64_t)depth && (int64_t)k > covered) {
+            he = hipStreamWaitEvent(cs, freed[(k - 2) % P], 0);
+            covered = (int64_t)k + depth - 2;
+        }
         if (he == hipSuccess)
-            he = hipMemcpyAsync(stage, h_ct + off, bytes, hipMemcpyHostToDevice, cs);
+            he = hipMemcpyAsync(buf, h_ct + off, bytes, hipMemcpyHostToDevice, cs);
         if (he == hipSuccess)
-            he = hipEventRecord(copied[slot], cs);
+            he = hipEventRecord(copied[k % P], cs);
         if (he == hipSuccess)
-            he = hipStreamWaitEvent(ks, copied[slot], 0);
+            he = hipStreamWaitEvent(ks, copied[k % P], 0);
         if (he != hipSuccess) {
             cleanup();
             return hip_fail(he, "pipeline copy");
         }
-        rc = run_gcm(false, ctx, base_iv, chain_bytes, k * cpc, stage, bytes, d_pt + off, aad_bytes ? d_aad : nullptr,
+        rc = run_gcm(false, ctx, base_iv, chain_bytes, k * cpc, buf, bytes, d_pt + off, aad_bytes ? d_aad : nullptr,
                      aad_bytes, d_tags, nullptr, d_ok, 0, dev, ncu, ks);
         if (rc) {
             cleanup();
             return rc;
         }
-        he = hipEventRecord(freed[slot], ks);
-        if (he != hipSuccess) {
-            cleanup();
-            return hip_fail(he, "hipEventRecord");
+        if (depth) {
+            he = hipEventRecord(freed[k % P], ks);
+            if (he != hipSuccess) {
+                cleanup();
+                return hip_fail(he, "hipEventRecord");
+            }
         }
     }
     cleanup();

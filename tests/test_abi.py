@@ -96,11 +96,23 @@ def pipe(L, chain=1 << 20, length=16 << 20, chunk=8 << 20, depth=2, stage=0x1000
                                    stage_bytes, 0x300000000, 0x400000000, None, None)
 
 
-@pytest.mark.parametrize("kw", [dict(depth=1), dict(depth=4), dict(chunk=(8 << 20) + 16), dict(chunk=0),
+@pytest.mark.parametrize("kw", [dict(depth=1), dict(depth=9), dict(depth=-1), dict(chunk=(8 << 20) + 16), dict(chunk=0),
                                 dict(stage_bytes=1024), dict(stage=0x100000010), dict(stage=None),
                                 dict(h_tags=None)])
 def test_pipeline_rejects_bad_arguments(L, kw):
     assert pipe(L, **kw) == -1
+
+
+def test_pipeline_stage_bytes(L):
+    n, tags = 16, 256
+    # in place: only the tags and the AAD (each rounded to 256 bytes)
+    assert L.fastrack_pipeline_stage_bytes(16 << 20, 1 << 20, 0, 8 << 20, 0) == tags
+    assert L.fastrack_pipeline_stage_bytes(16 << 20, 1 << 20, 32, 8 << 20, 0) == tags + 512
+    # a ring of depth slots of chunk_bytes (rounded to 256) in front
+    assert L.fastrack_pipeline_stage_bytes(16 << 20, 1 << 20, 0, 8 << 20, 3) == 3 * (8 << 20) + tags
+    assert L.fastrack_pipeline_stage_bytes(n * 4096 - 5, 4096, 1, 4096, 2) == 2 * 4096 + 256 + 256
+    for bad in (1, 9, -1):
+        assert L.fastrack_pipeline_stage_bytes(16 << 20, 1 << 20, 0, 8 << 20, bad) == 0
 
 
 def test_binding_fails_loudly_without_the_library(monkeypatch):

@@ -154,7 +154,7 @@ def test_config4_gradients_encrypt(F):
     check_encrypt(F, w.key, w.base_iv, chain, w.payload, None, 0, label="config4")
 
 
-@pytest.mark.parametrize("depth", [2, 3])
+@pytest.mark.parametrize("depth", [0, 2, 3])
 def test_config5_pipeline_small(F, depth):
     """The pipeline on 64 MiB with a ragged last chunk and AAD, vs the oracle."""
     import torch
@@ -194,7 +194,7 @@ def config5_data():
     del h_pt, h_ct
 
 
-@pytest.mark.parametrize("depth", [2, 3])
+@pytest.mark.parametrize("depth", [0, 2, 3])
 def test_config5_pipeline_4gib(F, config5_data, depth):
     import torch
     w, h_pt, h_ct, tags, want = config5_data
