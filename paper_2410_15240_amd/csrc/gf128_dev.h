@@ -112,17 +112,6 @@ __device__ inline u4 mul_tab4(const u4 &x, const Tab4 *__restrict__ t)
     return z;
 }
 
-// X . H^e for 0 <= e < 2^32 using the squares tables H^(2^t).
-__device__ inline u4 mul_hpow(u4 x, uint32_t e, const KeyCtx *__restrict__ c)
-{
-    while (e) {
-        int t = __builtin_ctz(e);
-        x = mul_tab4(x, &c->sq_tab[t]);
-        e &= e - 1;
-    }
-    return x;
-}
-
 __device__ __forceinline__ u4 xor4(const u4 &a, const u4 &b)
 {
     u4 r;
