@@ -241,6 +241,53 @@ def extras(F, W, torch, np, dev, stream, args):
     res["config1_1MiB"] = seq
     log("1 MiB:", seq)
 
+    # eager evaluation: plaintext released before the tag check (64 MiB image batch, 64 KiB chains)
+    w2 = W.config2()
+    chain2 = 64 * KiB
+    p2 = torch.from_numpy(w2.payload).to(dev)
+    a2 = torch.from_numpy(w2.aad(chain2)).to(dev)
+    c2, t2 = F.encrypt_tag(w2.key, w2.base_iv, chain2, p2, a2)
+    o2 = torch.empty_like(c2)
+    k2 = torch.empty(t2.shape[0], dtype=torch.uint8, device=dev)
+    fused_ms = time_calls(torch, stream, lambda: F.decrypt_verify(w2.key, w2.base_iv, chain2, c2, t2, a2, out=o2,
+                                                                  ok=k2), 20)
+    vstream = torch.cuda.Stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    pt_ms, ok_ms = [], []
+    for rep in range(21):
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        e = F.decrypt_eager(w2.key, w2.base_iv, chain2, c2, t2, a2, out=o2, ok=k2, decrypt_stream=stream,
+                            verify_stream=vstream)
+        ev[1].record(stream)
+        ev[2].record(vstream)
+        torch.cuda.synchronize()
+        if rep:
+            pt_ms.append(ev[0].elapsed_time(ev[1]))
+            ok_ms.append(ev[0].elapsed_time(ev[2]))
+    assert not e.rejected() and torch.equal(o2, p2)
+    res["eager"] = {"workload": "image-batch-64MiB, 64 KiB chains, 32-byte AAD",
+                    "fused_us": round(fused_ms * 1e3, 1), "plaintext_ready_us": round(float(np.median(pt_ms)) * 1e3, 1),
+                    "verified_us": round(float(np.median(ok_ms)) * 1e3, 1)}
+    log("eager:", res["eager"])
+
+    # one-time-pad precompute: what is left once an 8 MiB chunk (1 MiB chains) has arrived
+    chunk = 8 * MiB
+    p5 = p2[:chunk]
+    c5, t5 = F.encrypt_tag(w2.key, w2.base_iv, MiB, p5)
+    o5 = torch.empty_like(c5)
+    k5 = torch.empty(t5.shape[0], dtype=torch.uint8, device=dev)
+    ks5 = F.keystream(w2.key, w2.base_iv, MiB, chunk)
+    ks_ms = time_calls(torch, stream, lambda: F.keystream(w2.key, w2.base_iv, MiB, chunk, out=ks5), 50)
+    apply_ms = time_calls(torch, stream, lambda: F.apply_verify(w2.key, w2.base_iv, MiB, c5, ks5, t5, out=o5, ok=k5), 50)
+    assert bool(k5.all()) and torch.equal(o5, p5)
+    fused5_ms = time_calls(torch, stream, lambda: F.decrypt_verify(w2.key, w2.base_iv, MiB, c5, t5, out=o5, ok=k5), 50)
+    res["otp"] = {"workload": "8 MiB chunk, 1 MiB chains", "keystream_us": round(ks_ms * 1e3, 1),
+                  "after_arrival_fused_us": round(fused5_ms * 1e3, 1),
+                  "after_arrival_apply_us": round(apply_ms * 1e3, 1)}
+    log("otp:", res["otp"])
+    del p2, a2, c2, t2, o2, k2, c5, t5, o5, k5, ks5
+
     # per-key setup (first call with a new key)
     key2 = bytes(range(32))
     t = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -277,18 +324,23 @@ def pipeline(F, W, torch, np, dev):
     stage = torch.empty(F.stage_bytes(length, chain, 0, chunk, 3), dtype=torch.uint8, device=dev)
     out = torch.empty(length, dtype=torch.uint8, device=dev)
     ok = torch.empty(n, dtype=torch.uint8, device=dev)
-    cs, ks = torch.cuda.Stream(), torch.cuda.Stream()
-    for depth in (0, 2, 3):
-        F.pipeline_h2d(key, iv, chain, h_ct, h_tags, None, chunk, depth, stage, out, ok, cs, ks)
+    cs, ks, vs = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    for name, mode, depth in (("depth0", 0, 0), ("depth2", 0, 2), ("depth3", 0, 3), ("eager_depth2", 1, 2),
+                              ("otp_depth2", 2, 2)):
+        run = lambda: F.pipeline_h2d(key, iv, chain, h_ct, h_tags, None, chunk, depth, stage, out, ok, cs, ks,
+                                     mode=mode, verify_stream=vs)
+        run()
         torch.cuda.synchronize()
+        ok.zero_()
         t0 = time.perf_counter()
-        F.pipeline_h2d(key, iv, chain, h_ct, h_tags, None, chunk, depth, stage, out, ok, cs, ks)
+        run()
         ks.synchronize()
+        vs.synchronize()
         cs.synchronize()
         dt = time.perf_counter() - t0
         assert bool(ok.all()) and torch.equal(out, d_pt), "pipeline produced wrong output"
-        res["depth%d_gbps" % depth] = round(length / dt / 1e9, 2)
-        log("pipeline depth %d: %.2f GB/s" % (depth, length / dt / 1e9))
+        res["%s_gbps" % name] = round(length / dt / 1e9, 2)
+        log("pipeline %s: %.2f GB/s" % (name, length / dt / 1e9))
     # plain pinned copy of the same bytes in the same chunks on one stream
     with torch.cuda.stream(cs):
         for rep in range(2):

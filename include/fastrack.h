@@ -57,6 +57,11 @@ enum fastrack_status {
 #define FASTRACK_F_SEQ_GHASH 1u  /* the paper's baseline authentication: one sequential
                                     GHASH chain per tag (section 5.2); same output */
 
+/* pipeline modes (fastrack_pipeline_h2d_mode) */
+#define FASTRACK_PIPE_FUSED 0u   /* decrypt + verify each chunk in one kernel */
+#define FASTRACK_PIPE_EAGER 1u   /* plaintext first, the tag check beside it (section 5.3) */
+#define FASTRACK_PIPE_OTP   2u   /* keystream of the next chunk while it is in flight (section 5.3) */
+
 /* Number of chains, ceil(len / chain_bytes); 0 when chain_bytes is 0. */
 uint64_t fastrack_num_chains(uint64_t len, uint64_t chain_bytes);
 
@@ -91,6 +96,41 @@ int fastrack_gcm_encrypt_tag(const uint8_t *key, const uint8_t *base_iv, uint64_
                              const uint8_t *d_pt, uint64_t len, const uint8_t *d_aad, uint32_t aad_bytes,
                              uint8_t *d_ct, uint8_t *d_tags, uint32_t flags, void *stream);
 
+/*
+ * Eager evaluation (paper section 5.3, "Eager evaluation"): the plaintext is
+ * released before the tags are checked. AES-CTR writes d_pt on decrypt_stream;
+ * GHASH over d_ct and the tag comparison run on verify_stream, which first
+ * waits for the work already queued on decrypt_stream. d_pt is valid when
+ * decrypt_stream completes, d_ok when verify_stream completes; a caller that
+ * used the plaintext discards that work for every chain with ok[i] = 0.
+ * Arguments as in fastrack_gcm_decrypt_verify (no flags); d_pt may not be
+ * d_ct (EINVAL), since the ciphertext is read by the verification.
+ */
+int fastrack_gcm_decrypt_eager(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                               const uint8_t *d_ct, uint64_t len, const uint8_t *d_tags, const uint8_t *d_aad,
+                               uint32_t aad_bytes, uint8_t *d_pt, uint8_t *d_ok, void *decrypt_stream,
+                               void *verify_stream);
+
+/*
+ * One-time-pad precompute (paper section 5.3, "Parallel AES evaluation"): the
+ * CTR keystream depends only on the key, the IVs and the counters, so it can
+ * be generated before the ciphertext arrives.
+ * fastrack_gcm_keystream writes to d_ks[len] the keystream of the chains
+ * chain_base, chain_base+1, ... that cover len bytes (chain chain_base + i at
+ * d_ks + i*chain_bytes; the last chain may be short). d_ks is 16-byte aligned.
+ * fastrack_gcm_apply_verify then computes d_pt = d_ct XOR d_ks and verifies
+ * the same chains: tags, AAD and ok flags are indexed by GLOBAL chain index,
+ * d_tags + 16*(chain_base + i), d_aad + aad_bytes*(chain_base + i),
+ * d_ok[chain_base + i], so they point at the arrays of the whole message.
+ * d_pt may equal d_ct or d_ks exactly; partial overlaps are EINVAL.
+ */
+int fastrack_gcm_keystream(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes, uint64_t chain_base,
+                           uint64_t len, uint8_t *d_ks, void *stream);
+int fastrack_gcm_apply_verify(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes, uint64_t chain_base,
+                              const uint8_t *d_ct, uint64_t len, const uint8_t *d_ks, const uint8_t *d_tags,
+                              const uint8_t *d_aad, uint32_t aad_bytes, uint8_t *d_pt, uint8_t *d_ok,
+                              void *stream);
+
 /* Bytes of device staging that fastrack_pipeline_h2d needs for these sizes
  * (0 for an invalid depth or chain_bytes = 0). */
 uint64_t fastrack_pipeline_stage_bytes(uint64_t len, uint64_t chain_bytes, uint32_t aad_bytes,
@@ -120,6 +160,28 @@ int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, uint64_t c
                           uint32_t aad_bytes, uint64_t chunk_bytes, int depth, uint8_t *d_stage,
                           uint64_t stage_bytes, uint8_t *d_pt, uint8_t *d_ok, void *copy_stream,
                           void *compute_stream);
+
+/*
+ * fastrack_pipeline_h2d with a mode:
+ *   FASTRACK_PIPE_FUSED  as fastrack_pipeline_h2d (verify_stream unused)
+ *   FASTRACK_PIPE_EAGER  chunks land in a ring of depth >= 2 staging slots; each
+ *                        chunk's plaintext is written on compute_stream as soon
+ *                        as it has arrived, and its tags are checked on
+ *                        verify_stream beside the next copies. d_pt is valid
+ *                        when compute_stream completes, d_ok when verify_stream
+ *                        completes.
+ *   FASTRACK_PIPE_OTP    chunks are copied to their place in d_pt; the keystream
+ *                        of chunk k+1 is generated on compute_stream into one of
+ *                        depth >= 2 slots while chunk k+1 is in flight, so once
+ *                        it lands only the XOR and the tag check remain.
+ * d_stage is sized by fastrack_pipeline_stage_bytes(..., depth) for every mode.
+ * EINVAL additionally covers an unknown mode and depth 0 with EAGER or OTP.
+ */
+int fastrack_pipeline_h2d_mode(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                               const uint8_t *h_ct, uint64_t len, const uint8_t *h_tags, const uint8_t *h_aad,
+                               uint32_t aad_bytes, uint64_t chunk_bytes, int depth, uint32_t mode,
+                               uint8_t *d_stage, uint64_t stage_bytes, uint8_t *d_pt, uint8_t *d_ok,
+                               void *copy_stream, void *compute_stream, void *verify_stream);
 
 /* Message of the last failure on this thread ("" if none). */
 const char *fastrack_last_error(void);

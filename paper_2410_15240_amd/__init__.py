@@ -14,10 +14,12 @@ import torch as _torch  # loads the HIP runtime that the library then shares
 
 from . import build as _build
 
-__all__ = ["FastrackError", "decrypt_verify", "encrypt_tag", "pipeline_h2d", "num_chains", "stage_bytes",
-           "shutdown", "library_path", "F_SEQ_GHASH"]
+__all__ = ["FastrackError", "decrypt_verify", "encrypt_tag", "decrypt_eager", "Eager", "keystream", "apply_verify",
+           "pipeline_h2d", "num_chains", "stage_bytes", "shutdown", "library_path", "F_SEQ_GHASH", "PIPE_FUSED",
+           "PIPE_EAGER", "PIPE_OTP"]
 
 F_SEQ_GHASH = 1
+PIPE_FUSED, PIPE_EAGER, PIPE_OTP = 0, 1, 2
 
 OK, EINVAL, EHIP, ENOTPINNED, ENOMEM = 0, -1, -2, -3, -4
 _NAMES = {EINVAL: "EINVAL", EHIP: "EHIP", ENOTPINNED: "ENOTPINNED", ENOMEM: "ENOMEM"}
@@ -56,6 +58,15 @@ def lib():
         L.fastrack_pipeline_h2d.argtypes = [u8p, u8p, u64, u8p, u64, u8p, u8p, u32, u64, _ct.c_int, u8p, u64, u8p,
                                             u8p, vp, vp]
         L.fastrack_pipeline_h2d.restype = _ct.c_int
+        L.fastrack_pipeline_h2d_mode.argtypes = [u8p, u8p, u64, u8p, u64, u8p, u8p, u32, u64, _ct.c_int, u32, u8p,
+                                                 u64, u8p, u8p, vp, vp, vp]
+        L.fastrack_pipeline_h2d_mode.restype = _ct.c_int
+        L.fastrack_gcm_decrypt_eager.argtypes = [u8p, u8p, u64, u8p, u64, u8p, u8p, u32, u8p, u8p, vp, vp]
+        L.fastrack_gcm_decrypt_eager.restype = _ct.c_int
+        L.fastrack_gcm_keystream.argtypes = [u8p, u8p, u64, u64, u64, u8p, vp]
+        L.fastrack_gcm_keystream.restype = _ct.c_int
+        L.fastrack_gcm_apply_verify.argtypes = [u8p, u8p, u64, u64, u8p, u64, u8p, u8p, u8p, u32, u8p, u8p, vp]
+        L.fastrack_gcm_apply_verify.restype = _ct.c_int
         L.fastrack_last_error.restype = _ct.c_char_p
         L.fastrack_shutdown.restype = None
         _lib = L
@@ -137,9 +148,99 @@ def encrypt_tag(key, base_iv, chain_bytes, pt, aad=None, out=None, tags=None, fl
     return out, tags
 
 
+class Eager:
+    """Plaintext released before its tags are checked (the paper's eager evaluation).
+
+    `plaintext` is usable once the decrypt stream has reached the launch; `ok` is
+    final once `verified` (an event on the verify stream) has completed. A caller
+    that already consumed the plaintext rolls back the work of rejected chains."""
+
+    def __init__(self, plaintext, ok, verified):
+        self.plaintext, self.ok, self.verified = plaintext, ok, verified
+
+    def done(self):
+        """True once the tag check has finished (does not block)."""
+        return self.verified.query()
+
+    def rejected(self):
+        """Block until the tags are checked; the indices of the chains whose tag failed."""
+        self.verified.synchronize()
+        return _torch.nonzero(self.ok == 0).flatten().tolist()
+
+    def settle(self, commit, rollback):
+        """Block until verified, then call commit() if every chain passed, else rollback(rejected)."""
+        bad = self.rejected()
+        return rollback(bad) if bad else commit()
+
+
+def decrypt_eager(key, base_iv, chain_bytes, ct, tags, aad=None, out=None, ok=None, decrypt_stream=None,
+                  verify_stream=None):
+    """Decrypt on decrypt_stream and check the tags on verify_stream. Returns an Eager."""
+    _u8_dev(ct, "ct")
+    n = num_chains(ct.numel(), chain_bytes)
+    _u8_dev(tags, "tags")
+    aad_bytes = 0 if aad is None else aad.numel() // max(n, 1)
+    if aad is not None:
+        _u8_dev(aad, "aad")
+    if out is None:
+        out = _torch.empty_like(ct)
+    if ok is None:
+        ok = _torch.empty(n, dtype=_torch.uint8, device=ct.device)
+    ds = decrypt_stream if decrypt_stream is not None else _torch.cuda.current_stream(ct.device)
+    vs = verify_stream if verify_stream is not None else ds
+    _check(lib().fastrack_gcm_decrypt_eager(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
+                                            chain_bytes, _dptr(ct), ct.numel(), _dptr(tags), _dptr(aad), aad_bytes,
+                                            _dptr(out), _dptr(ok), _stream(ds), _stream(vs)))
+    ev = _torch.cuda.Event()
+    ev.record(vs)
+    return Eager(out, ok, ev)
+
+
+def keystream(key, base_iv, chain_bytes, length, chain_base=0, out=None, stream=None, device=None):
+    """The CTR keystream of chains chain_base.. covering `length` bytes (a uint8 CUDA tensor)."""
+    if out is None:
+        device = _torch.device("cuda", _torch.cuda.current_device()) if device is None else _torch.device(device)
+        out = _torch.empty(length, dtype=_torch.uint8, device=device)
+    _u8_dev(out, "out")
+    if out.numel() < length:
+        raise ValueError("out holds %d bytes, need %d" % (out.numel(), length))
+    _check(lib().fastrack_gcm_keystream(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
+                                        chain_bytes, chain_base, length, _dptr(out), _stream(stream)))
+    return out
+
+
+def apply_verify(key, base_iv, chain_bytes, ct, ks, tags, aad=None, aad_bytes=None, chain_base=0, out=None, ok=None,
+                 stream=None):
+    """pt = ct XOR ks and the tag check of chains chain_base.. of ct. tags, aad and ok
+    are the whole message's arrays, indexed by global chain index. Returns (pt, ok)."""
+    _u8_dev(ct, "ct")
+    _u8_dev(ks, "ks")
+    _u8_dev(tags, "tags")
+    total = tags.numel() // 16
+    n = num_chains(ct.numel(), chain_bytes)
+    if chain_base + n > total:
+        raise ValueError("tags hold %d chains, need %d" % (total, chain_base + n))
+    if aad is not None:
+        _u8_dev(aad, "aad")
+        aad_bytes = aad.numel() // max(total, 1) if aad_bytes is None else aad_bytes
+    else:
+        aad_bytes = 0
+    if out is None:
+        out = _torch.empty_like(ct)
+    if ok is None:
+        ok = _torch.empty(total, dtype=_torch.uint8, device=ct.device)
+    _check(lib().fastrack_gcm_apply_verify(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
+                                           chain_bytes, chain_base, _dptr(ct), ct.numel(), _dptr(ks), _dptr(tags),
+                                           _dptr(aad), aad_bytes, _dptr(out), _dptr(ok), _stream(stream)))
+    return out, ok
+
+
 def pipeline_h2d(key, base_iv, chain_bytes, h_ct, h_tags, h_aad=None, chunk_bytes=8 << 20, depth=0, stage=None,
-                 out=None, ok=None, copy_stream=None, compute_stream=None, device=None):
-    """Chunked H2D copy of pinned ciphertext overlapped with decrypt + verify. Returns (pt, ok) on the device."""
+                 out=None, ok=None, copy_stream=None, compute_stream=None, device=None, mode=PIPE_FUSED,
+                 verify_stream=None):
+    """Chunked H2D copy of pinned ciphertext overlapped with decrypt + verify. Returns (pt, ok) on the device.
+    mode PIPE_EAGER checks the tags on verify_stream; PIPE_OTP generates each chunk's keystream while it is
+    in flight. Both need depth >= 2."""
     if not (isinstance(h_ct, _torch.Tensor) and h_ct.device.type == "cpu" and h_ct.dtype == _torch.uint8):
         raise ValueError("h_ct must be a uint8 CPU tensor in pinned memory")
     device = _torch.device("cuda", _torch.cuda.current_device()) if device is None else _torch.device(device)
@@ -158,10 +259,11 @@ def pipeline_h2d(key, base_iv, chain_bytes, h_ct, h_tags, h_aad=None, chunk_byte
         h_aad = h_aad.contiguous()
     cs = _stream(copy_stream)
     ks = _stream(compute_stream)
-    _check(lib().fastrack_pipeline_h2d(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"), chain_bytes,
-                                       h_ct.data_ptr(), length, h_tags.data_ptr(), _dptr(h_aad), aad_bytes,
-                                       chunk_bytes, depth, _dptr(stage), stage.numel(), _dptr(out), _dptr(ok), cs,
-                                       ks))
+    vs = _stream(verify_stream) if verify_stream is not None else ks
+    _check(lib().fastrack_pipeline_h2d_mode(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
+                                            chain_bytes, h_ct.data_ptr(), length, h_tags.data_ptr(), _dptr(h_aad),
+                                            aad_bytes, chunk_bytes, depth, mode, _dptr(stage), stage.numel(),
+                                            _dptr(out), _dptr(ok), cs, ks, vs))
     return out, ok
 
 

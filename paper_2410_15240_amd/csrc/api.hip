@@ -49,6 +49,7 @@ struct KeyEntry {
     KeyCtx *ctx;
     hipEvent_t ready;
     uint64_t last_use;
+    bool done = false;   // `ready` has been observed complete
 };
 
 struct ScratchEntry {
@@ -100,9 +101,15 @@ int key_ctx(const uint8_t *key, hipStream_t s, int dev, const KeyCtx **out)
     for (auto &e : g_keys)
         if (e.dev == dev && e.key == k) {
             e.last_use = ++g_tick;
-            hipError_t he = hipStreamWaitEvent(s, e.ready, 0);
-            if (he != hipSuccess)
-                return hip_fail(he, "hipStreamWaitEvent");
+            if (!e.done) {   // the setup may still be running on the stream it was enqueued on
+                if (hipEventQuery(e.ready) == hipSuccess) {
+                    e.done = true;
+                } else {
+                    hipError_t he = hipStreamWaitEvent(s, e.ready, 0);
+                    if (he != hipSuccess)
+                        return hip_fail(he, "hipStreamWaitEvent");
+                }
+            }
             *out = e.ctx;
             return FASTRACK_OK;
         }
@@ -279,17 +286,18 @@ void iv_words(const uint8_t *iv, uint32_t w[3])
                ((uint32_t)iv[4 * j + 3] << 24);
 }
 
-// Enqueue one decrypt/encrypt over [in, in+len) covering chains chain_base.. .
-int run_gcm(bool encrypt, const KeyCtx *ctx, const uint8_t *base_iv, uint64_t chain_bytes, uint64_t chain_base,
-            const uint8_t *in, uint64_t len, uint8_t *out, const uint8_t *aad, uint32_t aad_bytes,
-            const uint8_t *tags_in, uint8_t *tags_out, uint8_t *ok, uint32_t flags, int dev, int num_cu,
-            hipStream_t s)
+// Enqueue one launch of `mode` over [in, in+len) covering chains chain_base.. .
+int run_gcm(bool encrypt, GcmMode mode, const KeyCtx *ctx, const uint8_t *base_iv, uint64_t chain_bytes,
+            uint64_t chain_base, const uint8_t *in, const uint8_t *ks, uint64_t len, uint8_t *out,
+            const uint8_t *aad, uint32_t aad_bytes, const uint8_t *tags_in, uint8_t *tags_out, uint8_t *ok,
+            uint32_t flags, int dev, int num_cu, hipStream_t s)
 {
     GcmLaunch p;
     std::memset(&p, 0, sizeof p);
     make_plan(len, chain_bytes, chain_base, num_cu, p);
     p.ctx = ctx;
     p.in = in;
+    p.ks = ks;
     p.out = out;
     iv_words(base_iv, p.iv);
     p.aad = aad;
@@ -298,14 +306,13 @@ int run_gcm(bool encrypt, const KeyCtx *ctx, const uint8_t *base_iv, uint64_t ch
     p.tags_out = tags_out;
     p.ok = ok;
     hipError_t he;
-    if (flags & FASTRACK_F_SEQ_GHASH) {
-        p.do_ghash = 0;
+    if (mode == kFused && (flags & FASTRACK_F_SEQ_GHASH)) {
         if (!encrypt) {   // tag over the ciphertext before an in-place decrypt overwrites it
             he = launch_seq_ghash(p, false, s);
             if (he != hipSuccess)
                 return hip_fail(he, "sequential GHASH launch");
         }
-        he = launch_gcm(p, encrypt, num_cu, s);
+        he = launch_gcm(p, false, kCtr, num_cu, s);
         if (he != hipSuccess)
             return hip_fail(he, "CTR launch");
         if (encrypt) {
@@ -315,8 +322,8 @@ int run_gcm(bool encrypt, const KeyCtx *ctx, const uint8_t *base_iv, uint64_t ch
         }
         return FASTRACK_OK;
     }
-    p.do_ghash = 1;
-    p.split = p.n_items > p.n_chains ? 1u : 0u;
+    const bool ghash = mode == kFused || mode == kVerify || mode == kApplyKs;
+    p.split = ghash && p.n_items > p.n_chains ? 1u : 0u;
     if (p.split) {   // chains cut into segments: per-item partials and per-chain masks
         void *sc = nullptr;
         int rc = scratch_for(dev, s, (size_t)(p.n_items + p.n_chains) * 16, &sc);
@@ -325,7 +332,7 @@ int run_gcm(bool encrypt, const KeyCtx *ctx, const uint8_t *base_iv, uint64_t ch
         p.partials = reinterpret_cast<uint4 *>(sc);
         p.masks = p.partials + p.n_items;
     }
-    he = launch_gcm(p, encrypt, num_cu, s);
+    he = launch_gcm(p, encrypt, mode, num_cu, s);
     if (he != hipSuccess)
         return hip_fail(he, "GCM launch");
     return FASTRACK_OK;
@@ -369,7 +376,7 @@ FT_EXPORT int fastrack_gcm_decrypt_verify(const uint8_t *key, const uint8_t *bas
     const KeyCtx *ctx;
     if ((rc = key_ctx(key, s, dev, &ctx)))
         return rc;
-    return run_gcm(false, ctx, base_iv, chain_bytes, 0, d_ct, len, d_pt, aad_bytes ? d_aad : nullptr, aad_bytes,
+    return run_gcm(false, kFused, ctx, base_iv, chain_bytes, 0, d_ct, nullptr, len, d_pt, aad_bytes ? d_aad : nullptr, aad_bytes,
                    d_tags, nullptr, d_ok, flags, dev, ncu, s);
 }
 
@@ -391,8 +398,100 @@ FT_EXPORT int fastrack_gcm_encrypt_tag(const uint8_t *key, const uint8_t *base_i
     const KeyCtx *ctx;
     if ((rc = key_ctx(key, s, dev, &ctx)))
         return rc;
-    return run_gcm(true, ctx, base_iv, chain_bytes, 0, d_pt, len, d_ct, aad_bytes ? d_aad : nullptr, aad_bytes,
+    return run_gcm(true, kFused, ctx, base_iv, chain_bytes, 0, d_pt, nullptr, len, d_ct, aad_bytes ? d_aad : nullptr, aad_bytes,
                    nullptr, d_tags, nullptr, flags, dev, ncu, s);
+}
+
+FT_EXPORT int fastrack_gcm_decrypt_eager(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                                         const uint8_t *d_ct, uint64_t len, const uint8_t *d_tags,
+                                         const uint8_t *d_aad, uint32_t aad_bytes, uint8_t *d_pt, uint8_t *d_ok,
+                                         void *decrypt_stream, void *verify_stream)
+{
+    g_err.clear();
+    int rc = check_common(key, base_iv, chain_bytes, len, d_ct, d_pt, d_aad, aad_bytes, 0);
+    if (rc || len == 0)
+        return rc;
+    if (!d_tags || !d_ok)
+        return fail(FASTRACK_EINVAL, "d_tags and d_ok must be non-NULL");
+    if (static_cast<const void *>(d_ct) == static_cast<const void *>(d_pt))
+        return fail(FASTRACK_EINVAL, "d_pt may not be d_ct: the ciphertext is verified while it is decrypted");
+    std::lock_guard<std::mutex> lk(g_mu);
+    int dev, ncu;
+    if ((rc = current_device(&dev, &ncu)))
+        return rc;
+    hipStream_t ds = reinterpret_cast<hipStream_t>(decrypt_stream);
+    hipStream_t vs = reinterpret_cast<hipStream_t>(verify_stream);
+    const KeyCtx *ctx;
+    if ((rc = key_ctx(key, ds, dev, &ctx)))
+        return rc;
+    if (vs != ds) {
+        // The verify stream starts after the work already queued on the decrypt stream
+        // (which may be what wrote d_ct).
+        hipEvent_t e;
+        hipError_t he = hipEventCreateWithFlags(&e, hipEventDisableTiming);
+        if (he == hipSuccess) {
+            he = hipEventRecord(e, ds);
+            if (he == hipSuccess)
+                he = hipStreamWaitEvent(vs, e, 0);
+            (void)hipEventDestroy(e);
+        }
+        if (he != hipSuccess)
+            return hip_fail(he, "decrypt -> verify stream ordering");
+        if ((rc = key_ctx(key, vs, dev, &ctx)))
+            return rc;
+    }
+    rc = run_gcm(false, kCtr, ctx, base_iv, chain_bytes, 0, d_ct, nullptr, len, d_pt, nullptr, 0, nullptr, nullptr,
+                 nullptr, 0, dev, ncu, ds);
+    if (rc)
+        return rc;
+    return run_gcm(false, kVerify, ctx, base_iv, chain_bytes, 0, d_ct, nullptr, len, nullptr,
+                   aad_bytes ? d_aad : nullptr, aad_bytes, d_tags, nullptr, d_ok, 0, dev, ncu, vs);
+}
+
+FT_EXPORT int fastrack_gcm_keystream(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                                     uint64_t chain_base, uint64_t len, uint8_t *d_ks, void *stream)
+{
+    g_err.clear();
+    int rc = check_common(key, base_iv, chain_bytes, len, d_ks, d_ks, nullptr, 0, 0);
+    if (rc || len == 0)
+        return rc;
+    std::lock_guard<std::mutex> lk(g_mu);
+    int dev, ncu;
+    if ((rc = current_device(&dev, &ncu)))
+        return rc;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const KeyCtx *ctx;
+    if ((rc = key_ctx(key, s, dev, &ctx)))
+        return rc;
+    return run_gcm(false, kKeystream, ctx, base_iv, chain_bytes, chain_base, nullptr, nullptr, len, d_ks, nullptr, 0,
+                   nullptr, nullptr, nullptr, 0, dev, ncu, s);
+}
+
+FT_EXPORT int fastrack_gcm_apply_verify(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                                        uint64_t chain_base, const uint8_t *d_ct, uint64_t len, const uint8_t *d_ks,
+                                        const uint8_t *d_tags, const uint8_t *d_aad, uint32_t aad_bytes,
+                                        uint8_t *d_pt, uint8_t *d_ok, void *stream)
+{
+    g_err.clear();
+    int rc = check_common(key, base_iv, chain_bytes, len, d_ct, d_pt, d_aad, aad_bytes, 0);
+    if (rc || len == 0)
+        return rc;
+    if (!d_ks || ((uintptr_t)d_ks & 15))
+        return fail(FASTRACK_EINVAL, "d_ks must be a non-NULL 16-byte-aligned device pointer");
+    if (overlap_bad(d_ks, d_pt, len))
+        return fail(FASTRACK_EINVAL, "d_ks and d_pt overlap partially");
+    if (!d_tags || !d_ok)
+        return fail(FASTRACK_EINVAL, "d_tags and d_ok must be non-NULL");
+    std::lock_guard<std::mutex> lk(g_mu);
+    int dev, ncu;
+    if ((rc = current_device(&dev, &ncu)))
+        return rc;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const KeyCtx *ctx;
+    if ((rc = key_ctx(key, s, dev, &ctx)))
+        return rc;
+    return run_gcm(false, kApplyKs, ctx, base_iv, chain_bytes, chain_base, d_ct, d_ks, len, d_pt,
+                   aad_bytes ? d_aad : nullptr, aad_bytes, d_tags, nullptr, d_ok, 0, dev, ncu, s);
 }
 
 FT_EXPORT uint64_t fastrack_pipeline_stage_bytes(uint64_t len, uint64_t chain_bytes, uint32_t aad_bytes,
@@ -404,11 +503,12 @@ FT_EXPORT uint64_t fastrack_pipeline_stage_bytes(uint64_t len, uint64_t chain_by
     return (uint64_t)depth * round256(chunk_bytes) + round256(16 * n) + round256((uint64_t)aad_bytes * n);
 }
 
-FT_EXPORT int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
-                                    const uint8_t *h_ct, uint64_t len, const uint8_t *h_tags, const uint8_t *h_aad,
-                                    uint32_t aad_bytes, uint64_t chunk_bytes, int depth, uint8_t *d_stage,
-                                    uint64_t stage_bytes, uint8_t *d_pt, uint8_t *d_ok, void *copy_stream,
-                                    void *compute_stream)
+namespace {
+
+int pipeline_impl(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes, const uint8_t *h_ct, uint64_t len,
+                  const uint8_t *h_tags, const uint8_t *h_aad, uint32_t aad_bytes, uint64_t chunk_bytes, int depth,
+                  uint32_t mode, uint8_t *d_stage, uint64_t stage_bytes, uint8_t *d_pt, uint8_t *d_ok,
+                  void *copy_stream, void *compute_stream, void *verify_stream)
 {
     g_err.clear();
     int rc = check_common(key, base_iv, chain_bytes, len, h_ct, d_pt, h_aad, aad_bytes, 0);
@@ -418,8 +518,12 @@ FT_EXPORT int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, 
         return fail(FASTRACK_EINVAL, "h_tags, d_ok and d_stage must be non-NULL");
     if (chunk_bytes == 0 || chunk_bytes % chain_bytes != 0)
         return fail(FASTRACK_EINVAL, "chunk_bytes must be a nonzero multiple of chain_bytes");
+    if (mode > FASTRACK_PIPE_OTP)
+        return fail(FASTRACK_EINVAL, "unknown pipeline mode %u", mode);
     if (depth < 0 || depth == 1 || depth > kMaxPipelineDepth)
         return fail(FASTRACK_EINVAL, "depth must be 0 (in place) or 2..%d (staging ring)", kMaxPipelineDepth);
+    if (mode != FASTRACK_PIPE_FUSED && depth == 0)
+        return fail(FASTRACK_EINVAL, "the eager and keystream pipelines need depth >= 2 staging slots");
     if ((uintptr_t)d_stage & 255)
         return fail(FASTRACK_EINVAL, "d_stage must be 256-byte aligned");
     const uint64_t need = fastrack_pipeline_stage_bytes(len, chain_bytes, aad_bytes, chunk_bytes, depth);
@@ -440,17 +544,21 @@ FT_EXPORT int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, 
         return rc;
     hipStream_t cs = reinterpret_cast<hipStream_t>(copy_stream);
     hipStream_t ks = reinterpret_cast<hipStream_t>(compute_stream);
+    hipStream_t vs = mode == FASTRACK_PIPE_EAGER ? reinterpret_cast<hipStream_t>(verify_stream) : ks;
     const KeyCtx *ctx;
     if ((rc = key_ctx(key, ks, dev, &ctx)))
+        return rc;
+    if (vs != ks && (rc = key_ctx(key, vs, dev, &ctx)))
         return rc;
 
     const uint64_t n = (len + chain_bytes - 1) / chain_bytes;
     const uint64_t slot_bytes = round256(chunk_bytes);
     uint8_t *d_tags = d_stage + (uint64_t)depth * slot_bytes;
     uint8_t *d_aad = d_tags + round256(16 * n);
+    const uint8_t *aad = aad_bytes ? d_aad : nullptr;
 
-    // Event pools: copied[k % P] is waited on by the compute stream right after
-    // it is recorded, freed[k % P] at most two chunks later, so P = 4 suffices
+    // Event pools: copied[k % P] is waited on right after it is recorded, decrypted[k % P]
+    // at once by the verify stream, freed[k % P] at most two chunks later; P = 4 suffices
     // (a wait takes the event's state at the time it is enqueued).
     constexpr int P = 4;
     std::vector<hipEvent_t> ev;
@@ -458,7 +566,7 @@ FT_EXPORT int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, 
         for (auto e : ev)
             (void)hipEventDestroy(e);
     };
-    for (int i = 0; i < 2 * P + 1; ++i) {
+    for (int i = 0; i < 3 * P + 1; ++i) {
         hipEvent_t e;
         he = hipEventCreateWithFlags(&e, hipEventDisableTiming);
         if (he != hipSuccess) {
@@ -468,7 +576,7 @@ FT_EXPORT int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, 
         ev.push_back(e);
     }
     hipEvent_t meta = ev[0];
-    hipEvent_t *copied = &ev[1], *freed = &ev[1 + P];
+    hipEvent_t *copied = &ev[1], *freed = &ev[1 + P], *decrypted = &ev[1 + 2 * P];
 
     he = hipMemcpyAsync(d_tags, h_tags, 16 * n, hipMemcpyHostToDevice, cs);
     if (he == hipSuccess && aad_bytes)
@@ -477,24 +585,40 @@ FT_EXPORT int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, 
         he = hipEventRecord(meta, cs);
     if (he == hipSuccess)
         he = hipStreamWaitEvent(ks, meta, 0);
+    if (he == hipSuccess && vs != ks)
+        he = hipStreamWaitEvent(vs, meta, 0);
     if (he != hipSuccess) {
         cleanup();
         return hip_fail(he, "pipeline tag/AAD upload");
     }
-    // depth 0: each chunk is copied straight to its place in d_pt and decrypted
-    // there, so no buffer is reused and the copy stream never waits. A ring of
-    // `depth` slots must not overwrite slot k % depth before chunk k - depth is
-    // decrypted; the copy stream waits for the decrypt two chunks back, which
-    // covers the next depth - 1 copies and, with decrypts faster than copies,
-    // has finished by then (a wait on copy_stream costs the copy engine time).
     const uint64_t nchunks = (len + chunk_bytes - 1) / chunk_bytes;
     const uint64_t cpc = chunk_bytes / chain_bytes;
+    auto chunk_len = [&](uint64_t k) { return len - k * chunk_bytes < chunk_bytes ? len - k * chunk_bytes : chunk_bytes; };
+    auto slot = [&](uint64_t k) { return d_stage + (k % (uint64_t)depth) * slot_bytes; };
+    if (mode == FASTRACK_PIPE_OTP) {
+        // The keystream of chunk 0 before anything arrives; that of chunk k+1 while
+        // chunk k+1 is on the bus, in ring slot (k+1) % depth. A slot is rewritten only
+        // after the XOR that read it, earlier on the same stream.
+        rc = run_gcm(false, kKeystream, ctx, base_iv, chain_bytes, 0, nullptr, nullptr, chunk_len(0), slot(0), nullptr,
+                     0, nullptr, nullptr, nullptr, 0, dev, ncu, ks);
+        if (rc) {
+            cleanup();
+            return rc;
+        }
+    }
+    // depth 0: each chunk is copied straight to its place in d_pt and decrypted
+    // there, so no buffer is reused and the copy stream never waits. A ring of
+    // `depth` slots must not overwrite slot k % depth before chunk k - depth has
+    // been read; the copy stream waits for the release two chunks back, which
+    // covers the next depth - 1 copies and, with decrypts faster than copies,
+    // has happened by then (a wait on copy_stream costs the copy engine time).
+    const bool ring = mode != FASTRACK_PIPE_OTP && depth > 0;
     int64_t covered = -1;   // copies up to this chunk index have their slot's wait enqueued
     for (uint64_t k = 0; k < nchunks; ++k) {
         const uint64_t off = k * chunk_bytes;
-        const uint64_t bytes = len - off < chunk_bytes ? len - off : chunk_bytes;
-        uint8_t *buf = depth == 0 ? d_pt + off : d_stage + (k % (uint64_t)depth) * slot_bytes;
-        if (depth && k >= (uint64_t)depth && (int64_t)k > covered) {
+        const uint64_t bytes = chunk_len(k);
+        uint8_t *buf = ring ? slot(k) : d_pt + off;
+        if (ring && k >= (uint64_t)depth && (int64_t)k > covered) {
             he = hipStreamWaitEvent(cs, freed[(k - 2) % P], 0);
             covered = (int64_t)k + depth - 2;
         }
@@ -502,20 +626,56 @@ FT_EXPORT int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, 
             he = hipMemcpyAsync(buf, h_ct + off, bytes, hipMemcpyHostToDevice, cs);
         if (he == hipSuccess)
             he = hipEventRecord(copied[k % P], cs);
-        if (he == hipSuccess)
-            he = hipStreamWaitEvent(ks, copied[k % P], 0);
         if (he != hipSuccess) {
             cleanup();
             return hip_fail(he, "pipeline copy");
         }
-        rc = run_gcm(false, ctx, base_iv, chain_bytes, k * cpc, buf, bytes, d_pt + off, aad_bytes ? d_aad : nullptr,
-                     aad_bytes, d_tags, nullptr, d_ok, 0, dev, ncu, ks);
+        if (mode == FASTRACK_PIPE_OTP && k + 1 < nchunks) {
+            rc = run_gcm(false, kKeystream, ctx, base_iv, chain_bytes, (k + 1) * cpc, nullptr, nullptr, chunk_len(k + 1),
+                         slot(k + 1), nullptr, 0, nullptr, nullptr, nullptr, 0, dev, ncu, ks);
+            if (rc) {
+                cleanup();
+                return rc;
+            }
+        }
+        he = hipStreamWaitEvent(ks, copied[k % P], 0);
+        if (he != hipSuccess) {
+            cleanup();
+            return hip_fail(he, "hipStreamWaitEvent");
+        }
+        if (mode == FASTRACK_PIPE_FUSED) {
+            rc = run_gcm(false, kFused, ctx, base_iv, chain_bytes, k * cpc, buf, nullptr, bytes, d_pt + off, aad, aad_bytes,
+                         d_tags, nullptr, d_ok, 0, dev, ncu, ks);
+        } else if (mode == FASTRACK_PIPE_OTP) {
+            rc = run_gcm(false, kApplyKs, ctx, base_iv, chain_bytes, k * cpc, buf, slot(k), bytes, d_pt + off, aad,
+                         aad_bytes, d_tags, nullptr, d_ok, 0, dev, ncu, ks);
+        } else {   // eager: plaintext on the compute stream, the tag check beside it
+            rc = run_gcm(false, kCtr, ctx, base_iv, chain_bytes, k * cpc, buf, nullptr, bytes, d_pt + off, nullptr, 0,
+                         nullptr, nullptr, nullptr, 0, dev, ncu, ks);
+            if (!rc) {
+                he = hipEventRecord(decrypted[k % P], ks);
+                if (he == hipSuccess)
+                    he = hipStreamWaitEvent(vs, copied[k % P], 0);
+                if (he != hipSuccess) {
+                    cleanup();
+                    return hip_fail(he, "eager pipeline events");
+                }
+                rc = run_gcm(false, kVerify, ctx, base_iv, chain_bytes, k * cpc, buf, nullptr, bytes, nullptr, aad,
+                             aad_bytes, d_tags, nullptr, d_ok, 0, dev, ncu, vs);
+                if (!rc)
+                    he = hipStreamWaitEvent(vs, decrypted[k % P], 0);   // the slot is free once both have read it
+                if (!rc && he != hipSuccess) {
+                    cleanup();
+                    return hip_fail(he, "hipStreamWaitEvent");
+                }
+            }
+        }
         if (rc) {
             cleanup();
             return rc;
         }
-        if (depth) {
-            he = hipEventRecord(freed[k % P], ks);
+        if (ring) {
+            he = hipEventRecord(freed[k % P], vs);
             if (he != hipSuccess) {
                 cleanup();
                 return hip_fail(he, "hipEventRecord");
@@ -524,6 +684,29 @@ FT_EXPORT int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, 
     }
     cleanup();
     return FASTRACK_OK;
+}
+
+}  // namespace
+
+FT_EXPORT int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                                    const uint8_t *h_ct, uint64_t len, const uint8_t *h_tags, const uint8_t *h_aad,
+                                    uint32_t aad_bytes, uint64_t chunk_bytes, int depth, uint8_t *d_stage,
+                                    uint64_t stage_bytes, uint8_t *d_pt, uint8_t *d_ok, void *copy_stream,
+                                    void *compute_stream)
+{
+    return pipeline_impl(key, base_iv, chain_bytes, h_ct, len, h_tags, h_aad, aad_bytes, chunk_bytes, depth,
+                         FASTRACK_PIPE_FUSED, d_stage, stage_bytes, d_pt, d_ok, copy_stream, compute_stream,
+                         compute_stream);
+}
+
+FT_EXPORT int fastrack_pipeline_h2d_mode(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                                         const uint8_t *h_ct, uint64_t len, const uint8_t *h_tags,
+                                         const uint8_t *h_aad, uint32_t aad_bytes, uint64_t chunk_bytes, int depth,
+                                         uint32_t mode, uint8_t *d_stage, uint64_t stage_bytes, uint8_t *d_pt,
+                                         uint8_t *d_ok, void *copy_stream, void *compute_stream, void *verify_stream)
+{
+    return pipeline_impl(key, base_iv, chain_bytes, h_ct, len, h_tags, h_aad, aad_bytes, chunk_bytes, depth, mode,
+                         d_stage, stage_bytes, d_pt, d_ok, copy_stream, compute_stream, verify_stream);
 }
 
 FT_EXPORT void fastrack_shutdown(void)

@@ -446,10 +446,15 @@ __device__ __forceinline__ u4 ghash_step(const uint4 *lds4, const u4 &acc, const
 // L consecutive blocks of its segment per iteration; each lane keeps a Horner
 // accumulator with multiplier H^L, and lane j's accumulator carries the weight
 // H^(L-j) in its segment (times one more H for the tag). SPLIT (64 lanes only):
-// chains are cut into segments whose partials a second kernel sums.
-template <bool ENC, int LL, bool SPLIT>
+// chains are cut into segments whose partials a second kernel sums. MODE is a
+// GcmMode: which of keystream, data XOR and GHASH + tag the launch computes.
+template <bool ENC, int LL, bool SPLIT, int MODE>
 __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
 {
+    constexpr bool kGhash = MODE == kFused || MODE == kVerify || MODE == kApplyKs;   // GHASH + tag
+    constexpr bool kAes = MODE == kFused || MODE == kCtr || MODE == kKeystream;      // keystream by AES
+    constexpr bool kRead = MODE != kKeystream;                                        // reads `in`
+    constexpr bool kWrite = MODE != kVerify;                                          // writes `out`
     constexpr uint32_t L = 1u << LL;
     constexpr uint32_t G = 64u >> LL;
     // Static, so its LDS address is a compile-time constant and a v_perm result
@@ -469,7 +474,7 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
             const uint32_t v = c->t0[row];
             t[i] = tab == 0 ? v : rotl32(v, 8 * tab);
         }
-        if (p.do_ghash) {
+        if (kGhash) {
             const uint4 *g = reinterpret_cast<const uint4 *>(c->g8[LL - 4]);
             for (int i = tid; i < 2048; i += kThreads)
                 lds4[kG8Base + i] = g[i];
@@ -500,7 +505,7 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
     uint32_t it = 0;   // wave-items done by this wave
     for (uint64_t wi = wave; wi < n_wave_items; wi += nwaves, ++it) {
         const uint32_t bi = it & (L - 1);
-        if (p.do_ghash && bi == 0) {
+        if (kGhash && bi == 0) {
             const uint64_t bitem = (wi + (uint64_t)(lane >> (6 - LL)) * nwaves) * G + (lane & (G - 1));
             const ItemPos bp = item_pos(p, bitem < p.n_items ? bitem : p.n_items - 1);
             uint32_t biv[3];
@@ -527,8 +532,9 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
                                  xor3(tlk(lds, c1, lc3, FT_SEL(3)), rk[6], 0u));
         const uint32_t p3 = xor3(tlk(lds, c0, lc1, FT_SEL(1)), tlk(lds, c1, lc2, FT_SEL(2)),
                                  xor3(tlk(lds, c2, lc3, FT_SEL(3)), rk[7], 0u));
-        const uint8_t *src = p.in + (uint64_t)ip.chain * p.chain_bytes;
-        uint8_t *dst = p.out + (uint64_t)ip.chain * p.chain_bytes;
+        const uint8_t *src = kRead ? p.in + (uint64_t)ip.chain * p.chain_bytes : nullptr;
+        uint8_t *dst = kWrite ? p.out + (uint64_t)ip.chain * p.chain_bytes : nullptr;
+        const uint8_t *ksrc = MODE == kApplyKs ? p.ks + (uint64_t)ip.chain * p.chain_bytes : nullptr;
         const bool last_chain = ip.chain == p.n_chains - 1;
         const uint32_t tail = last_chain ? (uint32_t)(p.last_len & 15) : 0u;   // bytes of a final partial block
         const int pad = (int)((Ku << LL) - (ip.e - ip.b));                   // zero blocks in front
@@ -537,7 +543,7 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
         // holds the slots v = k L + jl - pad, so its AAD blocks fall in iterations
         // k_lo..k_hi; those below 0 are extra iterations ahead of the data that only
         // feed GHASH, the others are padding slots of the first iterations.
-        const int na = (ip.s == 0 && valid && p.do_ghash) ? (int)((p.aad_bytes + 15) >> 4) : 0;
+        const int na = (kGhash && ip.s == 0 && valid) ? (int)((p.aad_bytes + 15) >> 4) : 0;
         const uint8_t *aad_c = p.aad + gchain * p.aad_bytes;
         int k_lo = 0, k_hi = -1;
         if (na) {
@@ -575,7 +581,7 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
             const uint32_t t = ip.b + (uint32_t)v;                 // block index inside the chain
             const bool partial = active && tail != 0 && t == ip.q - 1;
             u4 d = zero4();
-            if (active) {
+            if (kRead && active) {
                 if (!partial) {
                     const uint4 x = reinterpret_cast<const uint4 *>(src)[t];
                     d.w[0] = x.x; d.w[1] = x.y; d.w[2] = x.z; d.w[3] = x.w;
@@ -583,48 +589,63 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
                     d = load_bytes(src + 16ull * t, tail);
                 }
             }
-            // Counter block IV_i || [t + 2]_32 (data blocks start at inc32(J0)).
-            const uint32_t s3i = bswap32(t + 2u) ^ rk[3];
-            // Round 1: only the counter column varies; it feeds row 3-j of output column j.
-            uint32_t s0 = p0 ^ tlk(lds, s3i, lc3, FT_SEL(3));
-            uint32_t s1 = p1 ^ tlk(lds, s3i, lc2, FT_SEL(2));
-            uint32_t s2 = p2 ^ tlk(lds, s3i, lc1, FT_SEL(1));
-            uint32_t s3 = p3 ^ tlk(lds, s3i, lc0, FT_SEL(0));
-#pragma unroll
-            for (int r = 2; r < 14; ++r) {
-                const uint32_t n0 = xor3(tlk(lds, s0, lc0, FT_SEL(0)), tlk(lds, s1, lc1, FT_SEL(1)),
-                                         xor3(tlk(lds, s2, lc2, FT_SEL(2)), tlk(lds, s3, lc3, FT_SEL(3)), rk[4 * r + 0]));
-                const uint32_t n1 = xor3(tlk(lds, s1, lc0, FT_SEL(0)), tlk(lds, s2, lc1, FT_SEL(1)),
-                                         xor3(tlk(lds, s3, lc2, FT_SEL(2)), tlk(lds, s0, lc3, FT_SEL(3)), rk[4 * r + 1]));
-                const uint32_t n2 = xor3(tlk(lds, s2, lc0, FT_SEL(0)), tlk(lds, s3, lc1, FT_SEL(1)),
-                                         xor3(tlk(lds, s0, lc2, FT_SEL(2)), tlk(lds, s1, lc3, FT_SEL(3)), rk[4 * r + 2]));
-                const uint32_t n3 = xor3(tlk(lds, s3, lc0, FT_SEL(0)), tlk(lds, s0, lc1, FT_SEL(1)),
-                                         xor3(tlk(lds, s1, lc2, FT_SEL(2)), tlk(lds, s2, lc3, FT_SEL(3)), rk[4 * r + 3]));
-                s0 = n0; s1 = n1; s2 = n2; s3 = n3;
-            }
-            // Final round: S(x) is byte (1+r)&3 of T_r[x]; assemble four of them with v_perm.
             u4 o;
-            {
-                const uint32_t st[4] = {s0, s1, s2, s3};
+            if constexpr (kAes) {
+                // Counter block IV_i || [t + 2]_32 (data blocks start at inc32(J0)).
+                const uint32_t s3i = bswap32(t + 2u) ^ rk[3];
+                // Round 1: only the counter column varies; it feeds row 3-j of output column j.
+                uint32_t s0 = p0 ^ tlk(lds, s3i, lc3, FT_SEL(3));
+                uint32_t s1 = p1 ^ tlk(lds, s3i, lc2, FT_SEL(2));
+                uint32_t s2 = p2 ^ tlk(lds, s3i, lc1, FT_SEL(1));
+                uint32_t s3 = p3 ^ tlk(lds, s3i, lc0, FT_SEL(0));
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const uint32_t a0 = tlk(lds, st[j], lc0, FT_SEL(0));
-                    const uint32_t a1 = tlk(lds, st[(j + 1) & 3], lc1, FT_SEL(1));
-                    const uint32_t a2 = tlk(lds, st[(j + 2) & 3], lc2, FT_SEL(2));
-                    const uint32_t a3 = tlk(lds, st[(j + 3) & 3], lc3, FT_SEL(3));
-                    const uint32_t lo = __builtin_amdgcn_perm(a1, a0, 0x0C0C0601u);
-                    const uint32_t hi = __builtin_amdgcn_perm(a3, a2, 0x04030C0Cu);
-                    o.w[j] = xor3(lo, hi, rk[56 + j] ^ d.w[j]);
+                for (int r = 2; r < 14; ++r) {
+                    const uint32_t n0 = xor3(tlk(lds, s0, lc0, FT_SEL(0)), tlk(lds, s1, lc1, FT_SEL(1)),
+                                             xor3(tlk(lds, s2, lc2, FT_SEL(2)), tlk(lds, s3, lc3, FT_SEL(3)), rk[4 * r + 0]));
+                    const uint32_t n1 = xor3(tlk(lds, s1, lc0, FT_SEL(0)), tlk(lds, s2, lc1, FT_SEL(1)),
+                                             xor3(tlk(lds, s3, lc2, FT_SEL(2)), tlk(lds, s0, lc3, FT_SEL(3)), rk[4 * r + 1]));
+                    const uint32_t n2 = xor3(tlk(lds, s2, lc0, FT_SEL(0)), tlk(lds, s3, lc1, FT_SEL(1)),
+                                             xor3(tlk(lds, s0, lc2, FT_SEL(2)), tlk(lds, s1, lc3, FT_SEL(3)), rk[4 * r + 2]));
+                    const uint32_t n3 = xor3(tlk(lds, s3, lc0, FT_SEL(0)), tlk(lds, s0, lc1, FT_SEL(1)),
+                                             xor3(tlk(lds, s1, lc2, FT_SEL(2)), tlk(lds, s2, lc3, FT_SEL(3)), rk[4 * r + 3]));
+                    s0 = n0; s1 = n1; s2 = n2; s3 = n3;
                 }
+                // Final round: S(x) is byte (1+r)&3 of T_r[x]; assemble four of them with v_perm.
+                {
+                    const uint32_t st[4] = {s0, s1, s2, s3};
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const uint32_t a0 = tlk(lds, st[j], lc0, FT_SEL(0));
+                        const uint32_t a1 = tlk(lds, st[(j + 1) & 3], lc1, FT_SEL(1));
+                        const uint32_t a2 = tlk(lds, st[(j + 2) & 3], lc2, FT_SEL(2));
+                        const uint32_t a3 = tlk(lds, st[(j + 3) & 3], lc3, FT_SEL(3));
+                        const uint32_t lo = __builtin_amdgcn_perm(a1, a0, 0x0C0C0601u);
+                        const uint32_t hi = __builtin_amdgcn_perm(a3, a2, 0x04030C0Cu);
+                        o.w[j] = xor3(lo, hi, rk[56 + j] ^ d.w[j]);
+                    }
+                }
+            } else if constexpr (MODE == kApplyKs) {
+                u4 k4 = zero4();
+                if (active) {
+                    if (!partial) {
+                        const uint4 x = reinterpret_cast<const uint4 *>(ksrc)[t];
+                        k4.w[0] = x.x; k4.w[1] = x.y; k4.w[2] = x.z; k4.w[3] = x.w;
+                    } else {
+                        k4 = load_bytes(ksrc + 16ull * t, tail);
+                    }
+                }
+                o = xor4(d, k4);
+            } else {
+                o = d;
             }
-            if (active) {
+            if (kWrite && active) {
                 if (!partial) {
                     reinterpret_cast<uint4 *>(dst)[t] = make_uint4(o.w[0], o.w[1], o.w[2], o.w[3]);
                 } else {
                     store_bytes(dst + 16ull * t, o, tail);
                 }
             }
-            if (p.do_ghash) {
+            if constexpr (kGhash) {
                 u4 g = ENC ? o : d;
                 if (ENC) {
                     if (!active) {
@@ -642,7 +663,7 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
                 acc = (k == 0 && kmin == 0) ? g : ghash_step(lds4, acc, g);
             }
         }
-        if (p.do_ghash) {
+        if constexpr (kGhash) {
             // Lane j's chain carries weight H^(L-j) in its segment; one more H for the tag.
             acc = mul_tab4(acc, &c->lane_tab[64 - L + jl]);
 #pragma unroll
@@ -754,9 +775,10 @@ __global__ __launch_bounds__(256) void seq_ghash_kernel(GcmLaunch p)
     emit_tag<ENC>(p, gchain, tag, ENC ? zero4() : load16(p.tags_in + 16 * gchain));
 }
 
-template <bool ENC>
-static hipError_t launch_gcm_t(const GcmLaunch &p, int num_cu, hipStream_t s)
+template <bool ENC, int MODE>
+static hipError_t launch_mode(const GcmLaunch &p, int num_cu, hipStream_t s)
 {
+    constexpr bool ghash = MODE == kFused || MODE == kVerify || MODE == kApplyKs;
     if (p.n_items == 0)
         return hipSuccess;
     const uint64_t per_wave = 64u >> p.lanes_log2;
@@ -765,23 +787,35 @@ static hipError_t launch_gcm_t(const GcmLaunch &p, int num_cu, hipStream_t s)
     if (wgs > (uint64_t)num_cu)
         wgs = (uint64_t)num_cu;
     if (p.lanes_log2 == 4)
-        hipLaunchKernelGGL((gcm_kernel<ENC, 4, false>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+        hipLaunchKernelGGL((gcm_kernel<ENC, 4, false, MODE>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
     else if (p.lanes_log2 == 5)
-        hipLaunchKernelGGL((gcm_kernel<ENC, 5, false>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
-    else if (!p.split)
-        hipLaunchKernelGGL((gcm_kernel<ENC, 6, false>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+        hipLaunchKernelGGL((gcm_kernel<ENC, 5, false, MODE>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+    else if (!ghash || !p.split)
+        hipLaunchKernelGGL((gcm_kernel<ENC, 6, false, MODE>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
     else
-        hipLaunchKernelGGL((gcm_kernel<ENC, 6, true>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+        hipLaunchKernelGGL((gcm_kernel<ENC, 6, ghash, MODE>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || !p.do_ghash || !p.split)
+    if (e != hipSuccess || !ghash || !p.split)
         return e;
     hipLaunchKernelGGL(chain_tag_kernel<ENC>, dim3((p.n_chains + 255) / 256), dim3(256), 0, s, p);
     return hipGetLastError();
 }
 
-hipError_t launch_gcm(const GcmLaunch &p, bool encrypt, int num_cu, hipStream_t s)
+hipError_t launch_gcm(const GcmLaunch &p, bool encrypt, GcmMode mode, int num_cu, hipStream_t s)
 {
-    return encrypt ? launch_gcm_t<true>(p, num_cu, s) : launch_gcm_t<false>(p, num_cu, s);
+    switch (mode) {
+    case kFused:
+        return encrypt ? launch_mode<true, kFused>(p, num_cu, s) : launch_mode<false, kFused>(p, num_cu, s);
+    case kCtr:
+        return launch_mode<false, kCtr>(p, num_cu, s);   // CTR is its own inverse
+    case kVerify:
+        return launch_mode<false, kVerify>(p, num_cu, s);
+    case kKeystream:
+        return launch_mode<false, kKeystream>(p, num_cu, s);
+    case kApplyKs:
+        return launch_mode<false, kApplyKs>(p, num_cu, s);
+    }
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_seq_ghash(const GcmLaunch &p, bool encrypt, hipStream_t s)

@@ -16,6 +16,15 @@ namespace fastrack {
 constexpr int kGcmThreads = FT_GCM_THREADS;
 constexpr int kGcmWavesPerWg = kGcmThreads / 64;
 
+// What a launch of the streaming kernel computes.
+enum GcmMode : int {
+    kFused = 0,       // AES-CTR XOR the data and GHASH over the ciphertext, then the tag
+    kCtr = 1,         // AES-CTR XOR the data only (plaintext released before verification)
+    kVerify = 2,      // GHASH over the ciphertext and the tag check only (no data written)
+    kKeystream = 3,   // the CTR keystream alone, written to `out` (no data read)
+    kApplyKs = 4,     // out = in XOR a precomputed keystream `ks`, GHASH over `in`, tag check
+};
+
 // One launch of the streaming kernel over `n_chains` consecutive chains.
 // The work is split into items (chain, segment); a segment is a run of
 // 2^seg_log2 blocks aligned to the END of its chain (segment 0 may be short).
@@ -24,6 +33,7 @@ constexpr int kGcmWavesPerWg = kGcmThreads / 64;
 struct GcmLaunch {
     const KeyCtx *ctx;
     const uint8_t *in;          // 16-byte aligned; chain 0 of this launch starts here
+    const uint8_t *ks;          // kApplyKs: the keystream, laid out like `in`
     uint8_t *out;               // 16-byte aligned; may equal `in`
     uint64_t chain_bytes;       // multiple of 16
     uint64_t last_len;          // bytes in the last chain of this launch (1..chain_bytes)
@@ -49,11 +59,10 @@ struct GcmLaunch {
     uint4 *partials;
     uint4 *masks;
     uint32_t split;
-    uint32_t do_ghash;          // 0: keystream only (the sequential-GHASH variant tags separately)
 };
 
 hipError_t launch_key_setup(const uint32_t key_words[8], KeyCtx *ctx, hipStream_t s);
-hipError_t launch_gcm(const GcmLaunch &p, bool encrypt, int num_cu, hipStream_t s);
+hipError_t launch_gcm(const GcmLaunch &p, bool encrypt, GcmMode mode, int num_cu, hipStream_t s);
 hipError_t launch_seq_ghash(const GcmLaunch &p, bool encrypt, hipStream_t s);
 
 }  // namespace fastrack

@@ -121,3 +121,48 @@ def test_binding_fails_loudly_without_the_library(monkeypatch):
     monkeypatch.setattr(F, "_lib", None)
     with pytest.raises(RuntimeError):
         F.lib()
+
+
+def eager(L, chain=4096, ct=A, length=65536, tags=B + 0x100000, pt=B, ok=B + 0x200000):
+    return L.fastrack_gcm_decrypt_eager(KEY, IV, chain, ct, length, tags, None, 0, pt, ok, None, None)
+
+
+@pytest.mark.parametrize("kw", [dict(pt=A), dict(tags=None), dict(ok=None), dict(ct=A + 4), dict(chain=24),
+                                dict(pt=A + 16)])
+def test_eager_rejects_bad_arguments(L, kw):
+    assert eager(L, **kw) == -1
+
+
+def keystream(L, chain=4096, base=0, length=65536, ks=A):
+    return L.fastrack_gcm_keystream(KEY, IV, chain, base, length, ks, None)
+
+
+@pytest.mark.parametrize("kw", [dict(chain=0), dict(ks=None), dict(ks=A + 8), dict(chain=(1 << 32) * 16)])
+def test_keystream_rejects_bad_arguments(L, kw):
+    assert keystream(L, **kw) == -1
+
+
+def test_keystream_zero_length_is_a_no_op(L):
+    assert keystream(L, length=0) == 0
+
+
+def apply(L, chain=4096, base=0, ct=A, length=65536, ks=B + 0x400000, tags=B + 0x100000, pt=B, ok=B + 0x200000):
+    return L.fastrack_gcm_apply_verify(KEY, IV, chain, base, ct, length, ks, tags, None, 0, pt, ok, None)
+
+
+@pytest.mark.parametrize("kw", [dict(ks=None), dict(ks=B + 0x400004), dict(ks=B + 16), dict(tags=None),
+                                dict(ok=None), dict(pt=A + 32), dict(ct=None)])
+def test_apply_verify_rejects_bad_arguments(L, kw):
+    assert apply(L, **kw) == -1
+
+
+def pipe_mode(L, mode=1, depth=2, chain=1 << 20, length=16 << 20, chunk=8 << 20):
+    stage_bytes = L.fastrack_pipeline_stage_bytes(length, chain, 0, chunk, max(depth, 2))
+    return L.fastrack_pipeline_h2d_mode(KEY, IV, chain, 0x20000, length, 0x40000, None, 0, chunk, depth, mode,
+                                        0x100000000, stage_bytes, 0x300000000, 0x400000000, None, None, None)
+
+
+@pytest.mark.parametrize("kw", [dict(mode=3), dict(mode=1, depth=0), dict(mode=2, depth=0), dict(mode=1, depth=1),
+                                dict(mode=2, depth=9)])
+def test_pipeline_mode_rejects_bad_arguments(L, kw):
+    assert pipe_mode(L, **kw) == -1

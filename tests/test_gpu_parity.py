@@ -194,18 +194,18 @@ def config5_data():
     del h_pt, h_ct
 
 
-@pytest.mark.parametrize("depth", [0, 2, 3])
-def test_config5_pipeline_4gib(F, config5_data, depth):
+@pytest.mark.parametrize("mode,depth", [(0, 0), (0, 2), (0, 3), (1, 2), (2, 2)])
+def test_config5_pipeline_4gib(F, config5_data, mode, depth):
     import torch
     w, h_pt, h_ct, tags, want = config5_data
     chain = w.chain_sizes[0]
-    say("config5 pipeline depth", depth)
-    copy_s = torch.cuda.Stream()
-    comp_s = torch.cuda.Stream()
+    say("config5 pipeline mode", mode, "depth", depth)
+    copy_s, comp_s, ver_s = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
     pt, ok = F.pipeline_h2d(w.key, w.base_iv, chain, h_ct, torch.from_numpy(tags), None,
                             chunk_bytes=w.extra["chunk_bytes"], depth=depth, copy_stream=copy_s,
-                            compute_stream=comp_s)
+                            compute_stream=comp_s, mode=mode, verify_stream=ver_s)
     comp_s.synchronize()
+    ver_s.synchronize()
     assert host(ok).all()
     idx = torch.from_numpy(w.sample_chains).cuda()
     got = pt.view(-1, chain).index_select(0, idx)
