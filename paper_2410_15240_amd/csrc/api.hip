@@ -210,7 +210,7 @@ uint32_t ceil_log2(uint64_t x)
 // chains get 16 or 32 lanes each (so one wave works on several chains and the
 // per-item lane combine is amortised over more blocks per lane); long chains
 // get 64 lanes and are cut into segments.
-void make_plan(uint64_t len, uint64_t chain_bytes, uint64_t chain_base, int num_cu, GcmLaunch &p)
+void make_plan(uint64_t len, uint64_t chain_bytes, uint64_t chain_base, uint64_t slots, GcmLaunch &p)
 {
     const uint64_t n = (len + chain_bytes - 1) / chain_bytes;
     const uint64_t qc = chain_bytes / 16;
@@ -220,7 +220,6 @@ void make_plan(uint64_t len, uint64_t chain_bytes, uint64_t chain_base, int num_
     p.qc = (uint32_t)qc;
     p.last_len = len - (n - 1) * chain_bytes;
     p.q_last = (uint32_t)((p.last_len + 15) / 16);
-    const uint64_t slots = (uint64_t)num_cu * kGcmWavesPerWg;   // resident waves
     uint32_t lg = ceil_log2(qc);
     if (lg > 31)
         lg = 31;
@@ -294,7 +293,7 @@ int run_gcm(bool encrypt, GcmMode mode, const KeyCtx *ctx, const uint8_t *base_i
 {
     GcmLaunch p;
     std::memset(&p, 0, sizeof p);
-    make_plan(len, chain_bytes, chain_base, num_cu, p);
+    make_plan(len, chain_bytes, chain_base, (uint64_t)num_cu * kGcmWavesPerWg * gcm_wgs_per_cu(mode), p);
     p.ctx = ctx;
     p.in = in;
     p.ks = ks;

@@ -262,6 +262,9 @@ constexpr int kThreads = kGcmThreads;
 constexpr int kWavesPerWg = kGcmWavesPerWg;
 constexpr uint32_t kLdsBytes = 160 * 1024;
 constexpr uint32_t kG8Base = 8192;           // uint4 index of the GHASH table in LDS
+constexpr uint32_t kLdsGhashOnly = 33 * 1024;  // modes without data AES: the GHASH table and T0
+
+
 
 #define FT_SEL(k) (0x0C020400u + ((uint32_t)(k) << 8))
 
@@ -417,7 +420,7 @@ __device__ inline u4 aes_block_lds(const char *lds, const uint32_t *rk, const u4
 
 // acc . H^L xor g with the 8-bit table of H^L in LDS: byte positions 0..7
 // directly, 8..15 through x^64.
-__device__ __forceinline__ u4 ghash_step(const uint4 *lds4, const u4 &acc, const u4 &g)
+__device__ __forceinline__ u4 ghash_step(const uint4 *g8, const u4 &acc, const u4 &g)
 {
     u4 lo = g, hi = zero4();
 #pragma unroll
@@ -426,10 +429,10 @@ __device__ __forceinline__ u4 ghash_step(const uint4 *lds4, const u4 &acc, const
         const uint32_t a1 = (acc.w[kb >> 2] >> (8 * ((kb + 1) & 3))) & 0xFFu;
         const uint32_t b0 = (acc.w[2 + (kb >> 2)] >> (8 * (kb & 3))) & 0xFFu;
         const uint32_t b1 = (acc.w[2 + (kb >> 2)] >> (8 * ((kb + 1) & 3))) & 0xFFu;
-        const uint4 ea = lds4[kG8Base + ((kb << 8) | a0)];
-        const uint4 eb = lds4[kG8Base + (((kb + 1) << 8) | a1)];
-        const uint4 fa = lds4[kG8Base + ((kb << 8) | b0)];
-        const uint4 fb = lds4[kG8Base + (((kb + 1) << 8) | b1)];
+        const uint4 ea = g8[(kb << 8) | a0];
+        const uint4 eb = g8[((kb + 1) << 8) | a1];
+        const uint4 fa = g8[(kb << 8) | b0];
+        const uint4 fb = g8[((kb + 1) << 8) | b1];
         lo.w[0] = xor3(lo.w[0], ea.x, eb.x);
         lo.w[1] = xor3(lo.w[1], ea.y, eb.y);
         lo.w[2] = xor3(lo.w[2], ea.z, eb.z);
@@ -449,7 +452,7 @@ __device__ __forceinline__ u4 ghash_step(const uint4 *lds4, const u4 &acc, const
 // chains are cut into segments whose partials a second kernel sums. MODE is a
 // GcmMode: which of keystream, data XOR and GHASH + tag the launch computes.
 template <bool ENC, int LL, bool SPLIT, int MODE>
-__global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
+__global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) void gcm_kernel(GcmLaunch p)
 {
     constexpr bool kGhash = MODE == kFused || MODE == kVerify || MODE == kApplyKs;   // GHASH + tag
     constexpr bool kAes = MODE == kFused || MODE == kCtr || MODE == kKeystream;      // keystream by AES
@@ -458,9 +461,14 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
     constexpr uint32_t L = 1u << LL;
     constexpr uint32_t G = 64u >> LL;
     // Static, so its LDS address is a compile-time constant and a v_perm result
-    // can be used as the ds_read address with no further add.
-    __shared__ uint4 lds4[kLdsBytes / 16];
+    // can be used as the ds_read address with no further add. Modes without
+    // data AES hold only the GHASH table and a plain T0 (for the J0 masks), 33
+    // KiB, so that more waves share a CU.
+    constexpr uint32_t kLdsUse = kAes ? kLdsBytes : kLdsGhashOnly;
+    __shared__ uint4 lds4[kLdsUse / 16];
     const char *lds = reinterpret_cast<const char *>(lds4);
+    const uint4 *g8 = lds4 + (kAes ? kG8Base : 0);
+    uint32_t *t0l = reinterpret_cast<uint32_t *>(lds4 + 2048);   // GHASH-only modes: T0 after the table
     const int tid = threadIdx.x;
     const uint32_t lane = tid & 63;
     const uint32_t jl = lane & (L - 1);      // lane within the item
@@ -468,16 +476,21 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
     const KeyCtx *__restrict__ c = p.ctx;
 
     {
-        uint32_t *t = reinterpret_cast<uint32_t *>(lds4);
-        for (int i = tid; i < 32768; i += kThreads) {
-            const uint32_t region = i >> 14, row = (i >> 6) & 255, tab = region * 2 + ((i >> 5) & 1);
-            const uint32_t v = c->t0[row];
-            t[i] = tab == 0 ? v : rotl32(v, 8 * tab);
+        if (kAes) {
+            uint32_t *t = reinterpret_cast<uint32_t *>(lds4);
+            for (int i = tid; i < 32768; i += kThreads) {
+                const uint32_t region = i >> 14, row = (i >> 6) & 255, tab = region * 2 + ((i >> 5) & 1);
+                const uint32_t v = c->t0[row];
+                t[i] = tab == 0 ? v : rotl32(v, 8 * tab);
+            }
+        } else {
+            for (int i = tid; i < 256; i += kThreads)
+                t0l[i] = c->t0[i];
         }
         if (kGhash) {
             const uint4 *g = reinterpret_cast<const uint4 *>(c->g8[LL - 4]);
             for (int i = tid; i < 2048; i += kThreads)
-                lds4[kG8Base + i] = g[i];
+                lds4[(kAes ? kG8Base : 0) + i] = g[i];
         }
     }
     __syncthreads();
@@ -488,10 +501,8 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
     // taken by the launch parameters and per-item state.
     uint32_t rk[60];
 #pragma unroll
-    for (int i = 0; i < 60; ++i) {
-        const uint32_t w = __builtin_amdgcn_readfirstlane(c->rk[i]);
-        rk[i] = in_vgpr(w);
-    }
+    for (int i = 0; i < 60; ++i)
+        rk[i] = kAes ? in_vgpr(__builtin_amdgcn_readfirstlane(c->rk[i])) : 0u;
 
     const uint64_t nwaves = (uint64_t)gridDim.x * kWavesPerWg;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerWg + (tid >> 6));
@@ -512,8 +523,12 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
             chain_iv(p, p.chain_base + bp.chain, biv);
             const u4 j0 = {{biv[0], biv[1], biv[2], bswap32(1u)}};   // J0 = IV_i || 0^31 || 1
             const LenTerms lt = len_terms(p, lane);
-            jmask = xor4(aes_block_lds(lds, rk, j0, lc0, lc1, lc2, lc3),
-                         bp.chain == p.n_chains - 1 ? lt.last : lt.full);
+            u4 e;
+            if constexpr (kAes)
+                e = aes_block_lds(lds, rk, j0, lc0, lc1, lc2, lc3);
+            else
+                e = aes256_encrypt_tt(j0, c->rk, [&](uint32_t x) { return t0l[x]; });
+            jmask = xor4(e, bp.chain == p.n_chains - 1 ? lt.last : lt.full);
         }
         const uint64_t item = wi * G + gs;
         const bool valid = item < p.n_items;
@@ -523,15 +538,14 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
         chain_iv(p, gchain, iv);
         // Counter mode: columns 0..2 of the state after AddRoundKey are the IV and
         // fixed for the whole chain, so 12 of round 1's 16 lookups are too.
-        const uint32_t c0 = iv[0] ^ rk[0], c1 = iv[1] ^ rk[1], c2 = iv[2] ^ rk[2];
-        const uint32_t p0 = xor3(tlk(lds, c0, lc0, FT_SEL(0)), tlk(lds, c1, lc1, FT_SEL(1)),
-                                 xor3(tlk(lds, c2, lc2, FT_SEL(2)), rk[4], 0u));
-        const uint32_t p1 = xor3(tlk(lds, c1, lc0, FT_SEL(0)), tlk(lds, c2, lc1, FT_SEL(1)),
-                                 xor3(tlk(lds, c0, lc3, FT_SEL(3)), rk[5], 0u));
-        const uint32_t p2 = xor3(tlk(lds, c2, lc0, FT_SEL(0)), tlk(lds, c0, lc2, FT_SEL(2)),
-                                 xor3(tlk(lds, c1, lc3, FT_SEL(3)), rk[6], 0u));
-        const uint32_t p3 = xor3(tlk(lds, c0, lc1, FT_SEL(1)), tlk(lds, c1, lc2, FT_SEL(2)),
-                                 xor3(tlk(lds, c2, lc3, FT_SEL(3)), rk[7], 0u));
+        uint32_t p0 = 0, p1 = 0, p2 = 0, p3 = 0;
+        if constexpr (kAes) {
+            const uint32_t c0 = iv[0] ^ rk[0], c1 = iv[1] ^ rk[1], c2 = iv[2] ^ rk[2];
+            p0 = xor3(tlk(lds, c0, lc0, FT_SEL(0)), tlk(lds, c1, lc1, FT_SEL(1)), xor3(tlk(lds, c2, lc2, FT_SEL(2)), rk[4], 0u));
+            p1 = xor3(tlk(lds, c1, lc0, FT_SEL(0)), tlk(lds, c2, lc1, FT_SEL(1)), xor3(tlk(lds, c0, lc3, FT_SEL(3)), rk[5], 0u));
+            p2 = xor3(tlk(lds, c2, lc0, FT_SEL(0)), tlk(lds, c0, lc2, FT_SEL(2)), xor3(tlk(lds, c1, lc3, FT_SEL(3)), rk[6], 0u));
+            p3 = xor3(tlk(lds, c0, lc1, FT_SEL(1)), tlk(lds, c1, lc2, FT_SEL(2)), xor3(tlk(lds, c2, lc3, FT_SEL(3)), rk[7], 0u));
+        }
         const uint8_t *src = kRead ? p.in + (uint64_t)ip.chain * p.chain_bytes : nullptr;
         uint8_t *dst = kWrite ? p.out + (uint64_t)ip.chain * p.chain_bytes : nullptr;
         const uint8_t *ksrc = MODE == kApplyKs ? p.ks + (uint64_t)ip.chain * p.chain_bytes : nullptr;
@@ -572,23 +586,39 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
             for (int k = kmin; k < 0; ++k) {
                 const int v = k * (int)L + (int)jl - pad;
                 const u4 g = v >= -na ? aad_block(aad_c, (uint32_t)(v + na), p.aad_bytes) : zero4();
-                acc = k == kmin ? g : ghash_step(lds4, acc, g);
+                acc = k == kmin ? g : ghash_step(g8, acc, g);
             }
         }
-        for (uint32_t k = 0; k < Ku; ++k) {
-            const int v = (int)(k << LL) + (int)jl - pad;
-            const bool active = valid && v >= 0;
-            const uint32_t t = ip.b + (uint32_t)v;                 // block index inside the chain
-            const bool partial = active && tail != 0 && t == ip.q - 1;
-            u4 d = zero4();
-            if (kRead && active) {
-                if (!partial) {
-                    const uint4 x = reinterpret_cast<const uint4 *>(src)[t];
-                    d.w[0] = x.x; d.w[1] = x.y; d.w[2] = x.z; d.w[3] = x.w;
+        // The lane's slot in iteration k: v = k L + jl - pad (below 0: a padding slot),
+        // block t of the chain; a final partial block holds `tail` bytes.
+        struct Slot {
+            int v;
+            bool active, partial;
+            uint32_t t;
+        };
+        auto slot_of = [&](uint32_t k) {
+            Slot q;
+            q.v = (int)(k << LL) + (int)jl - pad;
+            q.active = valid && q.v >= 0;
+            q.t = ip.b + (uint32_t)q.v;
+            q.partial = q.active && tail != 0 && q.t == ip.q - 1;
+            return q;
+        };
+        auto load_block = [&](const uint8_t *base, const Slot &q) {
+            u4 x = zero4();
+            if (q.active) {
+                if (!q.partial) {
+                    const uint4 y = reinterpret_cast<const uint4 *>(base)[q.t];
+                    x.w[0] = y.x; x.w[1] = y.y; x.w[2] = y.z; x.w[3] = y.w;
                 } else {
-                    d = load_bytes(src + 16ull * t, tail);
+                    x = load_bytes(base + 16ull * q.t, tail);
                 }
             }
+            return x;
+        };
+        // Iteration k on the loaded data block d (and keystream block kv for kApplyKs).
+        auto process = [&](uint32_t k, const Slot &q, const u4 &d, const u4 &kv) {
+            const uint32_t t = q.t;
             u4 o;
             if constexpr (kAes) {
                 // Counter block IV_i || [t + 2]_32 (data blocks start at inc32(J0)).
@@ -625,21 +655,12 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
                     }
                 }
             } else if constexpr (MODE == kApplyKs) {
-                u4 k4 = zero4();
-                if (active) {
-                    if (!partial) {
-                        const uint4 x = reinterpret_cast<const uint4 *>(ksrc)[t];
-                        k4.w[0] = x.x; k4.w[1] = x.y; k4.w[2] = x.z; k4.w[3] = x.w;
-                    } else {
-                        k4 = load_bytes(ksrc + 16ull * t, tail);
-                    }
-                }
-                o = xor4(d, k4);
+                o = xor4(d, kv);
             } else {
                 o = d;
             }
-            if (kWrite && active) {
-                if (!partial) {
+            if (kWrite && q.active) {
+                if (!q.partial) {
                     reinterpret_cast<uint4 *>(dst)[t] = make_uint4(o.w[0], o.w[1], o.w[2], o.w[3]);
                 } else {
                     store_bytes(dst + 16ull * t, o, tail);
@@ -648,9 +669,9 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
             if constexpr (kGhash) {
                 u4 g = ENC ? o : d;
                 if (ENC) {
-                    if (!active) {
+                    if (!q.active) {
                         g = zero4();
-                    } else if (partial) {                     // GHASH sees the ciphertext zero-padded
+                    } else if (q.partial) {                   // GHASH sees the ciphertext zero-padded
                         for (int j = 0; j < 4; ++j) {
                             const int nb = (int)tail - 4 * j;
                             const uint32_t m = nb >= 4 ? 0xFFFFFFFFu : (nb <= 0 ? 0u : ((1u << (8 * nb)) - 1u));
@@ -658,10 +679,15 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
                         }
                     }
                 }
-                if ((int)k <= kmax && v < 0 && v >= -na)        // an AAD block in a padding slot
-                    g = aad_block(aad_c, (uint32_t)(v + na), p.aad_bytes);
-                acc = (k == 0 && kmin == 0) ? g : ghash_step(lds4, acc, g);
+                if ((int)k <= kmax && q.v < 0 && q.v >= -na)    // an AAD block in a padding slot
+                    g = aad_block(aad_c, (uint32_t)(q.v + na), p.aad_bytes);
+                acc = (k == 0 && kmin == 0) ? g : ghash_step(g8, acc, g);
             }
+        };
+        for (uint32_t k = 0; k < Ku; ++k) {
+            const Slot q = slot_of(k);
+            process(k, q, kRead ? load_block(src, q) : zero4(),
+                    MODE == kApplyKs ? load_block(ksrc, q) : zero4());
         }
         if constexpr (kGhash) {
             // Lane j's chain carries weight H^(L-j) in its segment; one more H for the tag.
@@ -703,29 +729,32 @@ __global__ __launch_bounds__(kThreads, 1) void gcm_kernel(GcmLaunch p)
 }
 
 // Chains cut into segments: T = mask xor the XOR of the chain's weighted
-// partials, one thread per chain.
+// partials. One wave per chain: the lanes load the partials side by side and
+// the wave XOR-sums them.
+constexpr int kTagThreads = 256;
+
 template <bool ENC>
-__global__ __launch_bounds__(256) void chain_tag_kernel(GcmLaunch p)
+__global__ __launch_bounds__(kTagThreads) void chain_tag_kernel(GcmLaunch p)
 {
-    const uint32_t chain = blockIdx.x * blockDim.x + threadIdx.x;
+    const uint32_t chain = __builtin_amdgcn_readfirstlane(blockIdx.x * (kTagThreads / 64) + (threadIdx.x >> 6));
+    const uint32_t lane = threadIdx.x & 63;
     if (chain >= p.n_chains)
         return;
     const uint64_t gchain = p.chain_base + chain;
     const uint32_t S = chain == p.n_chains - 1 ? p.segs_last : p.segs_full;
-    const u4 got = ENC ? zero4() : load16(p.tags_in + 16 * gchain);
-    const uint4 m = p.masks[chain];
-    u4 tag = {{m.x, m.y, m.z, m.w}};
     const uint4 *part = p.partials + (uint64_t)chain * p.segs_full;
-    for (uint32_t s = 0; s < S; ++s) {
+    u4 t = zero4();
+    for (uint32_t s = lane; s < S; s += 64) {
         const uint4 g = part[s];
-        tag.w[0] ^= g.x; tag.w[1] ^= g.y; tag.w[2] ^= g.z; tag.w[3] ^= g.w;
+        t.w[0] ^= g.x; t.w[1] ^= g.y; t.w[2] ^= g.z; t.w[3] ^= g.w;
     }
-    emit_tag<ENC>(p, gchain, tag, got);
+    t = wave_xor(t);
+    if (lane == 0) {
+        const uint4 m = p.masks[chain];
+        t.w[0] ^= m.x; t.w[1] ^= m.y; t.w[2] ^= m.z; t.w[3] ^= m.w;
+        emit_tag<ENC>(p, gchain, t, ENC ? zero4() : load16(p.tags_in + 16 * gchain));
+    }
 }
-
-// ===========================================================================
-// Baseline: sequential GHASH
-// ===========================================================================
 
 template <class LK>
 __device__ inline u4 j0_mask(const GcmLaunch &p, uint64_t gchain, LK T)
@@ -784,8 +813,8 @@ static hipError_t launch_mode(const GcmLaunch &p, int num_cu, hipStream_t s)
     const uint64_t per_wave = 64u >> p.lanes_log2;
     const uint64_t waves = (p.n_items + per_wave - 1) / per_wave;
     uint64_t wgs = (waves + kWavesPerWg - 1) / kWavesPerWg;
-    if (wgs > (uint64_t)num_cu)
-        wgs = (uint64_t)num_cu;
+    if (wgs > (uint64_t)num_cu * gcm_wgs_per_cu(MODE))
+        wgs = (uint64_t)num_cu * gcm_wgs_per_cu(MODE);
     if (p.lanes_log2 == 4)
         hipLaunchKernelGGL((gcm_kernel<ENC, 4, false, MODE>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
     else if (p.lanes_log2 == 5)
@@ -797,7 +826,9 @@ static hipError_t launch_mode(const GcmLaunch &p, int num_cu, hipStream_t s)
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !ghash || !p.split)
         return e;
-    hipLaunchKernelGGL(chain_tag_kernel<ENC>, dim3((p.n_chains + 255) / 256), dim3(256), 0, s, p);
+    constexpr uint32_t per_block = kTagThreads / 64;
+    hipLaunchKernelGGL(chain_tag_kernel<ENC>, dim3((p.n_chains + per_block - 1) / per_block), dim3(kTagThreads), 0, s,
+                       p);
     return hipGetLastError();
 }
 

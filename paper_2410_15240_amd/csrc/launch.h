@@ -25,6 +25,10 @@ enum GcmMode : int {
     kApplyKs = 4,     // out = in XOR a precomputed keystream `ks`, GHASH over `in`, tag check
 };
 
+// Workgroups of the streaming kernel per CU: the modes with data AES take a
+// CU's whole LDS; the GHASH-only modes need 33 KiB, and two fit the registers.
+constexpr int gcm_wgs_per_cu(int mode) { return mode == kVerify || mode == kApplyKs ? 2 : 1; }
+
 // One launch of the streaming kernel over `n_chains` consecutive chains.
 // The work is split into items (chain, segment); a segment is a run of
 // 2^seg_log2 blocks aligned to the END of its chain (segment 0 may be short).
