@@ -348,6 +348,33 @@ def pipeline(F, W, torch, np, dev):
         assert bool(ok.all()) and torch.equal(out, d_pt), "pipeline produced wrong output"
         res["%s_gbps" % name] = round(length / dt / 1e9, 2)
         log("pipeline %s: %.2f GB/s" % (name, length / dt / 1e9))
+    # D2H: encrypt + tag of the same 4 GiB on the device, copied out chunk by chunk
+    h_out = torch.empty(length, dtype=torch.uint8, pin_memory=True)
+    h_tg = torch.empty((n, 16), dtype=torch.uint8, pin_memory=True)
+    d_ctb = torch.empty_like(d_pt)
+    d_tg = torch.empty((n, 16), dtype=torch.uint8, device=dev)
+    for rep in range(2):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        F.pipeline_d2h(key, iv, chain, d_pt, chunk_bytes=chunk, out=d_ctb, tags=d_tg, h_ct=h_out, h_tags=h_tg,
+                       copy_stream=cs, compute_stream=ks)
+        cs.synchronize()
+        dt = time.perf_counter() - t0
+    assert torch.equal(h_out, h_ct) and torch.equal(h_tg, h_tags), "D2H pipeline produced wrong ciphertext"
+    res["d2h_gbps"] = round(length / dt / 1e9, 2)
+    log("pipeline d2h: %.2f GB/s" % res["d2h_gbps"])
+    with torch.cuda.stream(cs):
+        for rep in range(2):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for off in range(0, length, chunk):
+                h_out[off:off + chunk].copy_(d_ctb[off:off + chunk], non_blocking=True)
+            cs.synchronize()
+            dt = time.perf_counter() - t0
+    res["pinned_copy_d2h_gbps"] = round(length / dt / 1e9, 2)
+    res["d2h_ratio_vs_copy"] = round(res["d2h_gbps"] / res["pinned_copy_d2h_gbps"], 3)
+    log("pinned d2h copy %.2f GB/s" % res["pinned_copy_d2h_gbps"])
+    del h_out, d_ctb, d_tg
     # plain pinned copy of the same bytes in the same chunks on one stream
     with torch.cuda.stream(cs):
         for rep in range(2):

@@ -183,6 +183,28 @@ int fastrack_pipeline_h2d_mode(const uint8_t *key, const uint8_t *base_iv, uint6
                                uint8_t *d_stage, uint64_t stage_bytes, uint8_t *d_pt, uint8_t *d_ok,
                                void *copy_stream, void *compute_stream, void *verify_stream);
 
+/*
+ * Pipelined encrypt + device-to-host copy (the reverse direction of the
+ * paper's section 5.3 pipeline, for results and gradients leaving the GPU):
+ * each chunk of chunk_bytes of d_pt is encrypted and tagged on compute_stream
+ * into d_ct (+ the same offset; d_ct may equal d_pt), and copied to the pinned
+ * host buffer h_ct on copy_stream while later chunks are encrypted. The tags
+ * (d_tags, n x 16 on the device) follow to h_tags[n][16] at the end. The
+ * copies are paced from the host: the call enqueues every encryption, then
+ * waits on the host for each group of chunks (at least 32 MiB) to be encrypted
+ * before enqueueing its copies, and returns once all copies are enqueued (the
+ * encryptions are then done; the copies may still be running).
+ *   d_aad        [n][aad_bytes] device AAD, or NULL with aad_bytes = 0
+ *   h_ct         [len] PINNED host memory (ENOTPINNED otherwise)
+ * h_ct and h_tags are valid once copy_stream has completed.
+ * EINVAL covers the checks of fastrack_gcm_encrypt_tag, chunk_bytes (a nonzero
+ * multiple of chain_bytes) and NULL h_ct, h_tags or d_tags.
+ */
+int fastrack_pipeline_d2h(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes, const uint8_t *d_pt,
+                          uint64_t len, const uint8_t *d_aad, uint32_t aad_bytes, uint64_t chunk_bytes,
+                          uint8_t *d_ct, uint8_t *d_tags, uint8_t *h_ct, uint8_t *h_tags, void *copy_stream,
+                          void *compute_stream);
+
 /* Message of the last failure on this thread ("" if none). */
 const char *fastrack_last_error(void);
 

@@ -15,7 +15,7 @@ import torch as _torch  # loads the HIP runtime that the library then shares
 from . import build as _build
 
 __all__ = ["FastrackError", "decrypt_verify", "encrypt_tag", "decrypt_eager", "Eager", "keystream", "apply_verify",
-           "pipeline_h2d", "num_chains", "stage_bytes", "shutdown", "library_path", "F_SEQ_GHASH", "PIPE_FUSED",
+           "pipeline_h2d", "pipeline_d2h", "num_chains", "stage_bytes", "shutdown", "library_path", "F_SEQ_GHASH", "PIPE_FUSED",
            "PIPE_EAGER", "PIPE_OTP"]
 
 F_SEQ_GHASH = 1
@@ -61,6 +61,8 @@ def lib():
         L.fastrack_pipeline_h2d_mode.argtypes = [u8p, u8p, u64, u8p, u64, u8p, u8p, u32, u64, _ct.c_int, u32, u8p,
                                                  u64, u8p, u8p, vp, vp, vp]
         L.fastrack_pipeline_h2d_mode.restype = _ct.c_int
+        L.fastrack_pipeline_d2h.argtypes = [u8p, u8p, u64, u8p, u64, u8p, u32, u64, u8p, u8p, u8p, u8p, vp, vp]
+        L.fastrack_pipeline_d2h.restype = _ct.c_int
         L.fastrack_gcm_decrypt_eager.argtypes = [u8p, u8p, u64, u8p, u64, u8p, u8p, u32, u8p, u8p, vp, vp]
         L.fastrack_gcm_decrypt_eager.restype = _ct.c_int
         L.fastrack_gcm_keystream.argtypes = [u8p, u8p, u64, u64, u64, u8p, vp]
@@ -265,6 +267,34 @@ def pipeline_h2d(key, base_iv, chain_bytes, h_ct, h_tags, h_aad=None, chunk_byte
                                             aad_bytes, chunk_bytes, depth, mode, _dptr(stage), stage.numel(),
                                             _dptr(out), _dptr(ok), cs, ks, vs))
     return out, ok
+
+
+def pipeline_d2h(key, base_iv, chain_bytes, pt, aad=None, chunk_bytes=8 << 20, out=None, tags=None, h_ct=None,
+                 h_tags=None, copy_stream=None, compute_stream=None):
+    """Encrypt + tag pt (uint8 CUDA tensor) chunk by chunk into `out` (device; may be pt) and copy each
+    chunk to the pinned host tensor h_ct while later chunks are encrypted. Returns (h_ct, h_tags)."""
+    _u8_dev(pt, "pt")
+    n = num_chains(pt.numel(), chain_bytes)
+    aad_bytes = 0 if aad is None else aad.numel() // max(n, 1)
+    if aad is not None:
+        _u8_dev(aad, "aad")
+    if out is None:
+        out = _torch.empty_like(pt)
+    if tags is None:
+        tags = _torch.empty((n, 16), dtype=_torch.uint8, device=pt.device)
+    if h_ct is None:
+        h_ct = _torch.empty(pt.numel(), dtype=_torch.uint8, pin_memory=True)
+    if h_tags is None:
+        h_tags = _torch.empty((n, 16), dtype=_torch.uint8, pin_memory=True)
+    if not (isinstance(h_ct, _torch.Tensor) and h_ct.device.type == "cpu" and h_ct.numel() >= pt.numel()):
+        raise ValueError("h_ct must be a pinned uint8 CPU tensor of at least len bytes")
+    if h_tags.device.type != "cpu" or h_tags.numel() < 16 * n:
+        raise ValueError("h_tags must be a uint8 CPU tensor of n x 16 bytes")
+    _check(lib().fastrack_pipeline_d2h(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"), chain_bytes,
+                                       _dptr(pt), pt.numel(), _dptr(aad), aad_bytes, chunk_bytes, _dptr(out),
+                                       _dptr(tags), h_ct.data_ptr(), h_tags.data_ptr(), _stream(copy_stream),
+                                       _stream(compute_stream)))
+    return h_ct, h_tags
 
 
 def shutdown():

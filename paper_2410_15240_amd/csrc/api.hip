@@ -42,6 +42,7 @@ constexpr uint64_t kMaxChainBlocks = 0xFFFFFFFEull;   // GCM: at most 2^32 - 2 b
 constexpr size_t kMaxKeys = 8;
 constexpr int kMinSegLog2 = 8;                          // segments of >= 256 blocks (4 per lane)
 constexpr int kMaxPipelineDepth = 8;                    // staging-ring slots
+constexpr uint64_t kD2hGroupBytes = 32ull << 20;        // D2H: encrypted bytes per copy-stream wait
 
 struct KeyEntry {
     int dev;
@@ -706,6 +707,101 @@ FT_EXPORT int fastrack_pipeline_h2d_mode(const uint8_t *key, const uint8_t *base
 {
     return pipeline_impl(key, base_iv, chain_bytes, h_ct, len, h_tags, h_aad, aad_bytes, chunk_bytes, depth, mode,
                          d_stage, stage_bytes, d_pt, d_ok, copy_stream, compute_stream, verify_stream);
+}
+
+FT_EXPORT int fastrack_pipeline_d2h(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                                    const uint8_t *d_pt, uint64_t len, const uint8_t *d_aad, uint32_t aad_bytes,
+                                    uint64_t chunk_bytes, uint8_t *d_ct, uint8_t *d_tags, uint8_t *h_ct,
+                                    uint8_t *h_tags, void *copy_stream, void *compute_stream)
+{
+    g_err.clear();
+    int rc = check_common(key, base_iv, chain_bytes, len, d_pt, d_ct, d_aad, aad_bytes, 0);
+    if (rc || len == 0)
+        return rc;
+    if (!d_tags || !h_ct || !h_tags)
+        return fail(FASTRACK_EINVAL, "d_tags, h_ct and h_tags must be non-NULL");
+    if (chunk_bytes == 0 || chunk_bytes % chain_bytes != 0)
+        return fail(FASTRACK_EINVAL, "chunk_bytes must be a nonzero multiple of chain_bytes");
+    hipPointerAttribute_t attr;
+    hipError_t he = hipPointerGetAttributes(&attr, h_ct);
+    if (he != hipSuccess || attr.type != hipMemoryTypeHost) {
+        (void)hipGetLastError();
+        return fail(FASTRACK_ENOTPINNED, "h_ct is not pinned host memory");
+    }
+    hipStream_t cs = reinterpret_cast<hipStream_t>(copy_stream);
+    hipStream_t ks = reinterpret_cast<hipStream_t>(compute_stream);
+    const uint64_t n = (len + chain_bytes - 1) / chain_bytes;
+    const uint64_t nchunks = (len + chunk_bytes - 1) / chunk_bytes;
+    const uint64_t cpc = chunk_bytes / chain_bytes;
+    const uint64_t group = (kD2hGroupBytes + chunk_bytes - 1) / chunk_bytes;
+    const uint64_t ngroups = (nchunks + group - 1) / group;
+    auto chunk_len = [&](uint64_t k) { return len - k * chunk_bytes < chunk_bytes ? len - k * chunk_bytes : chunk_bytes; };
+
+    // A copy that waits on the compute stream's events on the GPU stalls the copy
+    // engine far longer than the encryption takes, so the copies are paced from
+    // the host: every encryption is enqueued first, with an event per group of
+    // chunks, and the copies of a group are enqueued once its event has completed.
+    // Encrypting is several times faster than copying, so the copy engine stays busy.
+    std::vector<hipEvent_t> ev;
+    auto cleanup = [&]() {
+        for (auto e : ev)
+            (void)hipEventDestroy(e);
+    };
+    for (uint64_t g = 0; g < ngroups; ++g) {
+        hipEvent_t e;
+        he = hipEventCreateWithFlags(&e, hipEventDisableTiming);
+        if (he != hipSuccess) {
+            cleanup();
+            return hip_fail(he, "hipEventCreate");
+        }
+        ev.push_back(e);
+    }
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        int dev, ncu;
+        if ((rc = current_device(&dev, &ncu))) {
+            cleanup();
+            return rc;
+        }
+        const KeyCtx *ctx;
+        if ((rc = key_ctx(key, ks, dev, &ctx))) {
+            cleanup();
+            return rc;
+        }
+        for (uint64_t g = 0; g < ngroups; ++g) {
+            for (uint64_t k = g * group; k < (g + 1) * group && k < nchunks; ++k) {
+                const uint64_t off = k * chunk_bytes;
+                rc = run_gcm(true, kFused, ctx, base_iv, chain_bytes, k * cpc, d_pt + off, nullptr, chunk_len(k),
+                             d_ct + off, aad_bytes ? d_aad : nullptr, aad_bytes, nullptr, d_tags, nullptr, 0, dev, ncu,
+                             ks);
+                if (rc) {
+                    cleanup();
+                    return rc;
+                }
+            }
+            he = hipEventRecord(ev[g], ks);
+            if (he != hipSuccess) {
+                cleanup();
+                return hip_fail(he, "hipEventRecord");
+            }
+        }
+    }
+    for (uint64_t g = 0; g < ngroups; ++g) {
+        he = hipEventSynchronize(ev[g]);
+        for (uint64_t k = g * group; k < (g + 1) * group && k < nchunks && he == hipSuccess; ++k) {
+            const uint64_t off = k * chunk_bytes;
+            he = hipMemcpyAsync(h_ct + off, d_ct + off, chunk_len(k), hipMemcpyDeviceToHost, cs);
+        }
+        if (he != hipSuccess) {
+            cleanup();
+            return hip_fail(he, "pipeline copy");
+        }
+    }
+    he = hipMemcpyAsync(h_tags, d_tags, 16 * n, hipMemcpyDeviceToHost, cs);
+    cleanup();
+    if (he != hipSuccess)
+        return hip_fail(he, "tag copy");
+    return FASTRACK_OK;
 }
 
 FT_EXPORT void fastrack_shutdown(void)

@@ -166,3 +166,13 @@ def pipe_mode(L, mode=1, depth=2, chain=1 << 20, length=16 << 20, chunk=8 << 20)
                                 dict(mode=2, depth=9)])
 def test_pipeline_mode_rejects_bad_arguments(L, kw):
     assert pipe_mode(L, **kw) == -1
+
+
+def d2h(L, chain=4096, pt=A, length=65536, chunk=16384, ct=B, tags=B + 0x100000, h_ct=0x20000, h_tags=0x40000):
+    return L.fastrack_pipeline_d2h(KEY, IV, chain, pt, length, None, 0, chunk, ct, tags, h_ct, h_tags, None, None)
+
+
+@pytest.mark.parametrize("kw", [dict(chunk=0), dict(chunk=4096 + 16), dict(tags=None), dict(h_ct=None),
+                                dict(h_tags=None), dict(ct=A + 16), dict(pt=A + 4), dict(chain=0)])
+def test_pipeline_d2h_rejects_bad_arguments(L, kw):
+    assert d2h(L, **kw) == -1

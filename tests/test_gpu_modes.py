@@ -143,3 +143,40 @@ def test_pipeline_modes_small(F, mode, depth):
     vs.synchronize()
     assert np.array_equal(host(pt), want_pt)
     assert np.array_equal(host(ok), want_ok)
+
+
+@pytest.mark.parametrize("length,chain,chunk,abytes,inplace", [
+    (24 * MiB + 3 * 64 * KiB + 100, 64 * KiB, 1 * MiB, 32, False),
+    (5 * MiB + 16, 256 * KiB, 2 * MiB, 0, True),
+    (40 * 4096 + 5, 4096, 4 * 4096, 13, False),
+])
+def test_pipeline_d2h_matches_oracle(F, length, chain, chunk, abytes, inplace):
+    import torch
+    say("d2h", length, chain, chunk, abytes, inplace)
+    w = W.random_case(length % 977 + abytes, length, chain, abytes)
+    aad = W.case_aad(w, chain)
+    want_ct, want_tags = oracle.chains_encrypt(w.key, w.base_iv, chain, w.payload, aad, abytes)
+    cs, ks = torch.cuda.Stream(), torch.cuda.Stream()
+    d_pt = dev(w.payload)
+    h_ct, h_tags = F.pipeline_d2h(w.key, w.base_iv, chain, d_pt, dev(aad) if abytes else None, chunk_bytes=chunk,
+                                  out=d_pt if inplace else None, copy_stream=cs, compute_stream=ks)
+    cs.synchronize()
+    assert np.array_equal(h_tags.numpy(), want_tags)
+    assert np.array_equal(h_ct.numpy()[:length], want_ct)
+
+
+def test_pipeline_d2h_gradients_256mib(F):
+    """The fp32-gradients workload (256 MiB, 256 KiB chains) leaving the GPU in 8 MiB chunks."""
+    import torch
+    say("d2h gradients generate")
+    w = W.config4()
+    chain = w.chain_sizes[0]
+    say("d2h gradients oracle encrypt")
+    want_ct, want_tags = oracle.chains_encrypt(w.key, w.base_iv, chain, w.payload)
+    cs, ks = torch.cuda.Stream(), torch.cuda.Stream()
+    say("d2h gradients GPU")
+    h_ct, h_tags = F.pipeline_d2h(w.key, w.base_iv, chain, dev(w.payload), chunk_bytes=8 * MiB, copy_stream=cs,
+                                  compute_stream=ks)
+    cs.synchronize()
+    assert np.array_equal(h_tags.numpy(), want_tags)
+    assert np.array_equal(h_ct.numpy(), want_ct)
