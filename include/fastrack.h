@@ -205,6 +205,47 @@ int fastrack_pipeline_d2h(const uint8_t *key, const uint8_t *base_iv, uint64_t c
                           uint8_t *d_ct, uint8_t *d_tags, uint8_t *h_ct, uint8_t *h_tags, void *copy_stream,
                           void *compute_stream);
 
+/*
+ * Ragged chains: the paper's per-sample layout (section 5.2: every input sample
+ * of a batch is cut into several chains, each with its own tag and a one-byte
+ * serial number as AAD; section 5.4: the serial number exposes reordering).
+ * Chain i is bytes [h_chain_off[i], h_chain_off[i] + h_chain_len[i]) of the
+ * device buffers, an independent GCM message under IV_i (the chain index i as
+ * above), with AAD i at d_aad + i * aad_bytes, tag i at d_tags + 16 i and
+ * ok[i]. Lengths are free (0 allowed: the tag then covers the AAD alone).
+ *   h_chain_off  [n_chains] HOST array: byte offsets, each a multiple of 16,
+ *                increasing, chains not overlapping (gaps are left untouched)
+ *   h_chain_len  [n_chains] HOST array: byte lengths, each at most (2^32-2)*16
+ * d_ct and d_pt (or d_pt and d_ct) may be NULL when every chain is empty.
+ * The host arrays are read during the call only. The chain table goes to the
+ * device through a per-stream pinned staging buffer that the library owns; a
+ * later call on the same stream reuses it once the device has read it.
+ * EINVAL: as for fastrack_gcm_decrypt_verify / fastrack_gcm_encrypt_tag, plus
+ * NULL h_chain_off/h_chain_len with n_chains > 0, a misaligned, decreasing or
+ * overlapping offset, an oversized chain, more than 2^32-1 chains or work items.
+ * n_chains == 0 is a successful no-op.
+ */
+int fastrack_gcm_decrypt_verify_ragged(const uint8_t *key, const uint8_t *base_iv, const uint64_t *h_chain_off,
+                                       const uint64_t *h_chain_len, uint64_t n_chains, const uint8_t *d_ct,
+                                       const uint8_t *d_tags, const uint8_t *d_aad, uint32_t aad_bytes,
+                                       uint8_t *d_pt, uint8_t *d_ok, void *stream);
+
+int fastrack_gcm_encrypt_tag_ragged(const uint8_t *key, const uint8_t *base_iv, const uint64_t *h_chain_off,
+                                    const uint64_t *h_chain_len, uint64_t n_chains, const uint8_t *d_pt,
+                                    const uint8_t *d_aad, uint32_t aad_bytes, uint8_t *d_ct, uint8_t *d_tags,
+                                    void *stream);
+
+/*
+ * Host helper for the per-sample layout: samples of h_sample_len[s] bytes are
+ * packed back to back, each starting 16-byte aligned, and each is cut into
+ * chains_per_sample chains of equal whole-block parts (the last part shorter,
+ * parts past the end of a short sample empty). Writes n_samples *
+ * chains_per_sample entries to h_chain_off / h_chain_len and returns the
+ * packed buffer size in bytes (0 on NULL arrays or chains_per_sample == 0).
+ */
+uint64_t fastrack_sample_chains(const uint64_t *h_sample_len, uint64_t n_samples, uint32_t chains_per_sample,
+                                uint64_t *h_chain_off, uint64_t *h_chain_len);
+
 /* Message of the last failure on this thread ("" if none). */
 const char *fastrack_last_error(void);
 

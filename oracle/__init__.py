@@ -201,6 +201,45 @@ def chains_decrypt_subset(key, base_iv, chain_bytes, ct, tags, idx, aad=None, aa
     return pt, ok
 
 
+def ragged_encrypt(key, base_iv, chain_off, chain_len, pt, aad=None, aad_bytes=0, out=None):
+    """Chains of their own offsets and lengths (the paper's per-sample chaining, section 5.2): chain i is
+    bytes [off_i, off_i + len_i) of pt, encrypted as its own GCM message under chain_iv(base_iv, i) with
+    AAD aad[i]. Bytes outside every chain keep the value they have in ``out`` (zeros if out is None).
+    Returns (ct uint8[len(pt)], tags uint8[n, 16])."""
+    p = _u8(pt)
+    off = _np.asarray(chain_off, dtype=_np.uint64).reshape(-1)
+    ln = _np.asarray(chain_len, dtype=_np.uint64).reshape(-1)
+    n = off.size
+    a = _u8(aad, n * aad_bytes).reshape(n, aad_bytes) if aad_bytes else None
+    ct = out if out is not None else _np.zeros(p.size, _np.uint8)
+    tags = _np.zeros((n, 16), _np.uint8)
+    for i in range(n):
+        o, l = int(off[i]), int(ln[i])
+        c, t = gcm_encrypt(key, chain_iv(base_iv, i), p[o:o + l], a[i] if aad_bytes else b"")
+        ct[o:o + l] = c
+        tags[i] = t
+    return ct, tags
+
+
+def ragged_decrypt(key, base_iv, chain_off, chain_len, ct, tags, aad=None, aad_bytes=0, out=None):
+    """Inverse of ragged_encrypt: returns (pt uint8[len(ct)], ok uint8[n]); every chain's plaintext is
+    written whether or not its tag verifies."""
+    c = _u8(ct)
+    off = _np.asarray(chain_off, dtype=_np.uint64).reshape(-1)
+    ln = _np.asarray(chain_len, dtype=_np.uint64).reshape(-1)
+    n = off.size
+    t = _u8(tags, 16 * n).reshape(n, 16)
+    a = _u8(aad, n * aad_bytes).reshape(n, aad_bytes) if aad_bytes else None
+    pt = out if out is not None else _np.zeros(c.size, _np.uint8)
+    ok = _np.zeros(n, _np.uint8)
+    for i in range(n):
+        o, l = int(off[i]), int(ln[i])
+        p, good = gcm_decrypt(key, chain_iv(base_iv, i), c[o:o + l], t[i], a[i] if aad_bytes else b"")
+        pt[o:o + l] = p
+        ok[i] = int(good)
+    return pt, ok
+
+
 def max_threads():
     return int(lib().orc_max_threads())
 

@@ -15,7 +15,7 @@ import torch as _torch  # loads the HIP runtime that the library then shares
 from . import build as _build
 
 __all__ = ["FastrackError", "decrypt_verify", "encrypt_tag", "decrypt_eager", "Eager", "keystream", "apply_verify",
-           "pipeline_h2d", "pipeline_d2h", "num_chains", "stage_bytes", "shutdown", "library_path", "F_SEQ_GHASH", "PIPE_FUSED",
+           "pipeline_h2d", "pipeline_d2h", "decrypt_verify_ragged", "encrypt_tag_ragged", "sample_chains", "num_chains", "stage_bytes", "shutdown", "library_path", "F_SEQ_GHASH", "PIPE_FUSED",
            "PIPE_EAGER", "PIPE_OTP"]
 
 F_SEQ_GHASH = 1
@@ -69,6 +69,12 @@ def lib():
         L.fastrack_gcm_keystream.restype = _ct.c_int
         L.fastrack_gcm_apply_verify.argtypes = [u8p, u8p, u64, u64, u8p, u64, u8p, u8p, u8p, u32, u8p, u8p, vp]
         L.fastrack_gcm_apply_verify.restype = _ct.c_int
+        L.fastrack_gcm_decrypt_verify_ragged.argtypes = [u8p, u8p, vp, vp, u64, u8p, u8p, u8p, u32, u8p, u8p, vp]
+        L.fastrack_gcm_decrypt_verify_ragged.restype = _ct.c_int
+        L.fastrack_gcm_encrypt_tag_ragged.argtypes = [u8p, u8p, vp, vp, u64, u8p, u8p, u32, u8p, u8p, vp]
+        L.fastrack_gcm_encrypt_tag_ragged.restype = _ct.c_int
+        L.fastrack_sample_chains.argtypes = [vp, u64, u32, vp, vp]
+        L.fastrack_sample_chains.restype = u64
         L.fastrack_last_error.restype = _ct.c_char_p
         L.fastrack_shutdown.restype = None
         _lib = L
@@ -295,6 +301,74 @@ def pipeline_d2h(key, base_iv, chain_bytes, pt, aad=None, chunk_bytes=8 << 20, o
                                        _dptr(tags), h_ct.data_ptr(), h_tags.data_ptr(), _stream(copy_stream),
                                        _stream(compute_stream)))
     return h_ct, h_tags
+
+
+def _u64_host(x, what):
+    import numpy as np
+    a = np.ascontiguousarray(np.asarray(x, dtype=np.uint64))
+    if a.ndim != 1:
+        raise ValueError("%s must be one-dimensional" % what)
+    return a
+
+
+def sample_chains(sample_lens, chains_per_sample):
+    """Per-sample chain layout: samples packed 16-byte aligned, each cut into chains_per_sample chains.
+    Returns (chain_off, chain_len, total_bytes) with numpy uint64 arrays."""
+    import numpy as np
+    if int(chains_per_sample) <= 0:
+        raise ValueError("chains_per_sample must be positive")
+    s = _u64_host(sample_lens, "sample_lens")
+    n = s.size * int(chains_per_sample)
+    off = np.zeros(max(n, 1), dtype=np.uint64)
+    ln = np.zeros(max(n, 1), dtype=np.uint64)
+    total = lib().fastrack_sample_chains(s.ctypes.data, s.size, chains_per_sample, off.ctypes.data, ln.ctypes.data)
+    return off[:n], ln[:n], int(total)
+
+
+def decrypt_verify_ragged(key, base_iv, chain_off, chain_len, ct, tags, aad=None, out=None, ok=None, stream=None):
+    """Decrypt + verify chains of their own offsets and lengths in ct (uint8 CUDA tensor). Returns (pt, ok);
+    bytes of pt outside every chain are left as they were."""
+    _u8_dev(ct, "ct")
+    off, ln = _u64_host(chain_off, "chain_off"), _u64_host(chain_len, "chain_len")
+    if off.size != ln.size:
+        raise ValueError("chain_off and chain_len differ in length")
+    n = off.size
+    if n and int((off + ln).max()) > ct.numel():
+        raise ValueError("a chain ends past the end of ct")
+    _u8_dev(tags, "tags")
+    aad_bytes = 0 if aad is None else aad.numel() // max(n, 1)
+    if aad is not None:
+        _u8_dev(aad, "aad")
+    if out is None:
+        out = _torch.empty_like(ct)
+    if ok is None:
+        ok = _torch.empty(n, dtype=_torch.uint8, device=ct.device)
+    _check(lib().fastrack_gcm_decrypt_verify_ragged(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
+                                                    off.ctypes.data, ln.ctypes.data, n, _dptr(ct), _dptr(tags),
+                                                    _dptr(aad), aad_bytes, _dptr(out), _dptr(ok), _stream(stream)))
+    return out, ok
+
+
+def encrypt_tag_ragged(key, base_iv, chain_off, chain_len, pt, aad=None, out=None, tags=None, stream=None):
+    """Encrypt + tag chains of their own offsets and lengths in pt (uint8 CUDA tensor). Returns (ct, tags)."""
+    _u8_dev(pt, "pt")
+    off, ln = _u64_host(chain_off, "chain_off"), _u64_host(chain_len, "chain_len")
+    if off.size != ln.size:
+        raise ValueError("chain_off and chain_len differ in length")
+    n = off.size
+    if n and int((off + ln).max()) > pt.numel():
+        raise ValueError("a chain ends past the end of pt")
+    aad_bytes = 0 if aad is None else aad.numel() // max(n, 1)
+    if aad is not None:
+        _u8_dev(aad, "aad")
+    if out is None:
+        out = _torch.empty_like(pt)
+    if tags is None:
+        tags = _torch.empty((n, 16), dtype=_torch.uint8, device=pt.device)
+    _check(lib().fastrack_gcm_encrypt_tag_ragged(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
+                                                 off.ctypes.data, ln.ctypes.data, n, _dptr(pt), _dptr(aad), aad_bytes,
+                                                 _dptr(out), _dptr(tags), _stream(stream)))
+    return out, tags
 
 
 def shutdown():

@@ -58,6 +58,11 @@ struct ScratchEntry {
     hipStream_t stream;
     void *ptr;
     size_t bytes;
+    // pinned host staging for the tables of ragged launches, and the event after
+    // the copy that last read it
+    void *host = nullptr;
+    size_t host_bytes = 0;
+    hipEvent_t host_read = nullptr;
 };
 
 struct DevInfo {
@@ -198,6 +203,51 @@ int scratch_for(int dev, hipStream_t s, size_t bytes, void **out)
     return FASTRACK_OK;
 }
 
+// Pinned host staging of at least `bytes` for (device, stream), free to overwrite:
+// the copy that last read it has completed.
+int staging_for(int dev, hipStream_t s, size_t bytes, uint8_t **out)
+{
+    ScratchEntry *e = nullptr;
+    for (auto &x : g_scratch)
+        if (x.dev == dev && x.stream == s)
+            e = &x;
+    if (!e) {
+        g_scratch.push_back(ScratchEntry{dev, s, nullptr, 0});
+        e = &g_scratch.back();
+    }
+    hipError_t he;
+    if (e->host_read && (he = hipEventSynchronize(e->host_read)) != hipSuccess)
+        return hip_fail(he, "hipEventSynchronize");
+    if (!e->host_read && (he = hipEventCreateWithFlags(&e->host_read, hipEventDisableTiming)) != hipSuccess) {
+        e->host_read = nullptr;
+        return hip_fail(he, "hipEventCreate");
+    }
+    if (e->host_bytes < bytes) {
+        if (e->host)
+            (void)hipHostFree(e->host);
+        e->host = nullptr;
+        e->host_bytes = 0;
+        if ((he = hipHostMalloc(&e->host, bytes, 0)) != hipSuccess) {
+            e->host = nullptr;
+            return fail(FASTRACK_ENOMEM, "hipHostMalloc(%zu) for staging: %s", bytes, hipGetErrorString(he));
+        }
+        e->host_bytes = bytes;
+    }
+    *out = static_cast<uint8_t *>(e->host);
+    return FASTRACK_OK;
+}
+
+// Record on `s` that the staging of (dev, s) has been read by the work queued so far.
+int staging_read(int dev, hipStream_t s)
+{
+    for (auto &x : g_scratch)
+        if (x.dev == dev && x.stream == s) {
+            hipError_t he = hipEventRecord(x.host_read, s);
+            return he == hipSuccess ? FASTRACK_OK : hip_fail(he, "hipEventRecord");
+        }
+    return fail(FASTRACK_EHIP, "no staging for this stream");
+}
+
 uint32_t ceil_log2(uint64_t x)
 {
     uint32_t r = 0;
@@ -232,11 +282,19 @@ void make_plan(uint64_t len, uint64_t chain_bytes, uint64_t chain_base, uint64_t
         }
     if (ll == 0)   // short chains keep few lanes each; otherwise 64 lanes
         ll = qc >= 256 ? 6 : (qc >= 128 ? 5 : 4);
-    // Only items of 64 lanes may be segments of a longer chain (the streaming
-    // kernel weights segments with a wave-cooperative multiply).
-    if (ll == 6)   // too few whole chains to fill the GPU: cut them into segments
-        while (lg > (uint32_t)kMinSegLog2 && n * ((qc + (1ull << lg) - 1) >> lg) < slots)
+    auto items_at = [&](uint32_t g) { return n * ((qc + (1ull << g) - 1) >> g); };
+    if (ll == 6) {   // too few whole chains to fill the GPU: cut them into segments
+        while (lg > (uint32_t)kMinSegLog2 && items_at(lg) < slots)
             --lg;
+    } else {
+        // A few wave-items per wave that do not divide evenly leave some waves with
+        // one more than others: cut the chains until each wave has about 8 (segments
+        // of at least 4 iterations).
+        const uint64_t g = 64u >> ll;
+        auto wave_items = [&](uint32_t lgv) { return (items_at(lgv) + g - 1) / g; };
+        while (lg > ll + 2 && wave_items(lg) < 8 * slots && wave_items(lg) % slots != 0)
+            --lg;
+    }
     p.lanes_log2 = ll;
     p.seg_log2 = lg;
     p.segs_full = (uint32_t)((qc + (1ull << lg) - 1) >> lg);
@@ -804,6 +862,193 @@ FT_EXPORT int fastrack_pipeline_d2h(const uint8_t *key, const uint8_t *base_iv, 
     return FASTRACK_OK;
 }
 
+namespace {
+
+// Ragged chains: chain i = bytes [off[i], off[i] + len[i]) of in/out, IV_i, tag i,
+// AAD i, ok[i]. The chains are planned on the host (lanes per item from the mean
+// chain length, segments of one size for all chains) and the chain and item
+// tables go to the device through the stream's pinned staging.
+int run_ragged(bool encrypt, const uint8_t *key, const uint8_t *base_iv, const uint64_t *h_off, const uint64_t *h_len,
+               uint64_t n, const uint8_t *in, uint8_t *out, const uint8_t *aad, uint32_t aad_bytes,
+               const uint8_t *tags_in, uint8_t *tags_out, uint8_t *ok, void *stream)
+{
+    g_err.clear();
+    if (!key || !base_iv)
+        return fail(FASTRACK_EINVAL, "key and base_iv must be non-NULL host pointers");
+    if (n == 0)
+        return FASTRACK_OK;
+    if (!h_off || !h_len)
+        return fail(FASTRACK_EINVAL, "h_chain_off and h_chain_len must be non-NULL host arrays");
+    if (n > 0xFFFFFFFFull)
+        return fail(FASTRACK_EINVAL, "more than 2^32-1 chains");
+    uint64_t end = 0, blocks = 0, qmax = 0;
+    for (uint64_t i = 0; i < n; ++i) {
+        if (h_off[i] & 15)
+            return fail(FASTRACK_EINVAL, "chain %llu starts at offset %llu, not a multiple of 16", (unsigned long long)i,
+                        (unsigned long long)h_off[i]);
+        if (h_off[i] < end)
+            return fail(FASTRACK_EINVAL, "chain %llu overlaps the chain before it (chains must be in increasing order)",
+                        (unsigned long long)i);
+        if ((h_len[i] + 15) / 16 > kMaxChainBlocks)
+            return fail(FASTRACK_EINVAL, "chain %llu is longer than (2^32-2)*16 bytes", (unsigned long long)i);
+        end = h_off[i] + h_len[i];
+        const uint64_t q = (h_len[i] + 15) / 16;
+        blocks += q;
+        qmax = q > qmax ? q : qmax;
+    }
+    if (aad_bytes && !aad)
+        return fail(FASTRACK_EINVAL, "aad is NULL but aad_bytes = %u", aad_bytes);
+    if (blocks && (!in || !out))   // NULL buffers are fine when every chain is empty
+        return fail(FASTRACK_EINVAL, "input and output buffers must be non-NULL");
+    if (((uintptr_t)in & 15) || ((uintptr_t)out & 15))
+        return fail(FASTRACK_EINVAL, "input and output must be 16-byte aligned");
+    if (blocks && overlap_bad(in, out, end))
+        return fail(FASTRACK_EINVAL, "input and output overlap partially (in place means the same pointer)");
+    if (encrypt ? !tags_out : (!tags_in || !ok))
+        return fail(FASTRACK_EINVAL, encrypt ? "d_tags must be non-NULL" : "d_tags and d_ok must be non-NULL");
+
+    std::lock_guard<std::mutex> lk(g_mu);
+    int dev, ncu;
+    int rc;
+    if ((rc = current_device(&dev, &ncu)))
+        return rc;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const KeyCtx *ctx;
+    if ((rc = key_ctx(key, s, dev, &ctx)))
+        return rc;
+
+    // Plan: lanes per item from the mean chain length, as for uniform chains. Chains
+    // of their own lengths leave the waves unevenly loaded when a wave takes few
+    // items, so chains are cut into segments of one size (2^lg blocks, at least
+    // 4 iterations of the item's lanes) until every wave has about 8 wave-items.
+    const uint64_t slots = (uint64_t)ncu * kGcmWavesPerWg;
+    const uint64_t qmean = (blocks + n - 1) / n;
+    uint32_t ll = 0;
+    for (uint32_t cand = 4; cand <= 6; ++cand)
+        if (qmean >= (4ull << cand) && ((n << cand) + 63) / 64 >= slots) {
+            ll = cand;
+            break;
+        }
+    if (ll == 0)
+        ll = qmean >= 256 ? 6 : (qmean >= 128 ? 5 : 4);
+    uint32_t lg = ceil_log2(qmax > 0 ? qmax : 1);
+    if (lg > 31)
+        lg = 31;
+    auto segs_of = [&](uint64_t q, uint32_t g) { const uint64_t sg = (q + (1ull << g) - 1) >> g; return sg ? sg : 1ull; };
+    auto items_at = [&](uint32_t g) {
+        uint64_t t = 0;
+        for (uint64_t i = 0; i < n; ++i)
+            t += segs_of((h_len[i] + 15) / 16, g);
+        return t;
+    };
+    const uint32_t lg_min = ll + 2;
+    const uint64_t want_items = (8 * slots) << (6 - ll);   // 8 wave-items of 64 / 2^ll items per wave
+    while (lg > lg_min && items_at(lg) < want_items)
+        --lg;
+    const uint64_t n_items = items_at(lg);
+    if (n_items > 0xFFFFFFFFull)
+        return fail(FASTRACK_EINVAL, "more than 2^32-1 work items");
+
+    // Device: chain table | item table | (split) partials | masks. Host: the two tables.
+    const size_t tab_bytes = round256(n * sizeof(RaggedChain)) + round256(n_items * 4);
+    const bool split = n_items > n;
+    const size_t dev_bytes = tab_bytes + (split ? (n_items + n) * 16 : 0);
+    void *sc = nullptr;
+    if ((rc = scratch_for(dev, s, dev_bytes, &sc)))
+        return rc;
+    uint8_t *host = nullptr;
+    if ((rc = staging_for(dev, s, tab_bytes, &host)))
+        return rc;
+    RaggedChain *hc = reinterpret_cast<RaggedChain *>(host);
+    uint32_t *hi = reinterpret_cast<uint32_t *>(host + round256(n * sizeof(RaggedChain)));
+    uint64_t item = 0;
+    for (uint64_t i = 0; i < n; ++i) {
+        const uint64_t sg = segs_of((h_len[i] + 15) / 16, lg);
+        hc[i].off = h_off[i];
+        hc[i].len = h_len[i];
+        hc[i].item_base = item;
+        hc[i].segs = (uint32_t)sg;
+        hc[i].reserved = 0;
+        for (uint64_t k = 0; k < sg; ++k)
+            hi[item++] = (uint32_t)i;
+    }
+    hipError_t he = hipMemcpyAsync(sc, host, tab_bytes, hipMemcpyHostToDevice, s);
+    if (he != hipSuccess)
+        return hip_fail(he, "chain table upload");
+    if ((rc = staging_read(dev, s)))
+        return rc;
+
+    GcmLaunch p;
+    std::memset(&p, 0, sizeof p);
+    p.ctx = ctx;
+    p.in = in;
+    p.out = out;
+    iv_words(base_iv, p.iv);
+    p.aad = aad_bytes ? aad : nullptr;
+    p.aad_bytes = aad_bytes;
+    p.tags_in = tags_in;
+    p.tags_out = tags_out;
+    p.ok = ok;
+    p.n_chains = (uint32_t)n;
+    p.n_items = n_items;
+    p.lanes_log2 = ll;
+    p.seg_log2 = lg;
+    p.qc = (uint32_t)qmax;
+    p.rchains = reinterpret_cast<const RaggedChain *>(sc);
+    p.ritem_chain = reinterpret_cast<const uint32_t *>(static_cast<uint8_t *>(sc) + round256(n * sizeof(RaggedChain)));
+    p.split = split ? 1u : 0u;
+    if (split) {
+        p.partials = reinterpret_cast<uint4 *>(static_cast<uint8_t *>(sc) + tab_bytes);
+        p.masks = p.partials + n_items;
+    }
+    he = launch_gcm(p, encrypt, kFused, ncu, s);
+    if (he != hipSuccess)
+        return hip_fail(he, "GCM launch");
+    return FASTRACK_OK;
+}
+
+}  // namespace
+
+FT_EXPORT int fastrack_gcm_decrypt_verify_ragged(const uint8_t *key, const uint8_t *base_iv, const uint64_t *h_chain_off,
+                                                 const uint64_t *h_chain_len, uint64_t n_chains, const uint8_t *d_ct,
+                                                 const uint8_t *d_tags, const uint8_t *d_aad, uint32_t aad_bytes,
+                                                 uint8_t *d_pt, uint8_t *d_ok, void *stream)
+{
+    return run_ragged(false, key, base_iv, h_chain_off, h_chain_len, n_chains, d_ct, d_pt, d_aad, aad_bytes, d_tags,
+                      nullptr, d_ok, stream);
+}
+
+FT_EXPORT int fastrack_gcm_encrypt_tag_ragged(const uint8_t *key, const uint8_t *base_iv, const uint64_t *h_chain_off,
+                                              const uint64_t *h_chain_len, uint64_t n_chains, const uint8_t *d_pt,
+                                              const uint8_t *d_aad, uint32_t aad_bytes, uint8_t *d_ct, uint8_t *d_tags,
+                                              void *stream)
+{
+    return run_ragged(true, key, base_iv, h_chain_off, h_chain_len, n_chains, d_pt, d_ct, d_aad, aad_bytes, nullptr,
+                      d_tags, nullptr, stream);
+}
+
+FT_EXPORT uint64_t fastrack_sample_chains(const uint64_t *h_sample_len, uint64_t n_samples, uint32_t chains_per_sample,
+                                          uint64_t *h_chain_off, uint64_t *h_chain_len)
+{
+    if (!h_sample_len || !h_chain_off || !h_chain_len || chains_per_sample == 0)
+        return 0;
+    uint64_t off = 0, c = 0;
+    for (uint64_t s = 0; s < n_samples; ++s) {
+        const uint64_t len = h_sample_len[s];
+        // equal parts rounded up to whole blocks, so every chain but the last starts aligned
+        const uint64_t part = ((len + chains_per_sample - 1) / chains_per_sample + 15) & ~15ull;
+        for (uint32_t j = 0; j < chains_per_sample; ++j) {
+            const uint64_t b = (uint64_t)j * part;
+            const uint64_t l = b >= len ? 0 : (len - b < part ? len - b : part);
+            h_chain_off[c] = off + (b < len ? b : len);
+            h_chain_len[c] = l;
+            ++c;
+        }
+        off = (off + len + 15) & ~15ull;   // the next sample starts 16-byte aligned
+    }
+    return off;
+}
+
 FT_EXPORT void fastrack_shutdown(void)
 {
     std::lock_guard<std::mutex> lk(g_mu);
@@ -813,7 +1058,12 @@ FT_EXPORT void fastrack_shutdown(void)
     for (auto &k : g_keys)
         free_key_entry(k);
     g_keys.clear();
-    for (auto &s : g_scratch)
+    for (auto &s : g_scratch) {
         (void)hipFree(s.ptr);
+        if (s.host)
+            (void)hipHostFree(s.host);
+        if (s.host_read)
+            (void)hipEventDestroy(s.host_read);
+    }
     g_scratch.clear();
 }

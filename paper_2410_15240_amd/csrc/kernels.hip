@@ -223,19 +223,37 @@ __device__ inline void store_bytes(uint8_t *dst, const u4 &v, uint32_t n)
                 dst[4 * j + b] = (uint8_t)(v.w[j] >> (8 * b));
 }
 
-// Position of an item: chain, and the block range [b, e) of its segment.
+// Position of an item: chain, segment s of S, the block range [b, e) of the
+// segment in the chain's q blocks, and the chain's byte offset, length and
+// final partial-block bytes.
 struct ItemPos {
-    uint32_t chain, s, S, q, b, e;
+    uint32_t chain, s, S, q, b, e, tail;
+    uint64_t off, len;
 };
 
+template <bool RAG>
 __device__ __forceinline__ ItemPos item_pos(const GcmLaunch &p, uint64_t item)
 {
     ItemPos r;
-    r.chain = (uint32_t)(item / p.segs_full);
-    r.s = (uint32_t)(item - (uint64_t)r.chain * p.segs_full);
-    const bool last = r.chain == p.n_chains - 1;
-    r.q = last ? p.q_last : p.qc;
-    r.S = last ? p.segs_last : p.segs_full;
+    if constexpr (RAG) {
+        r.chain = p.ritem_chain[item];
+        const RaggedChain rc = p.rchains[r.chain];
+        r.s = (uint32_t)(item - rc.item_base);
+        r.S = rc.segs;
+        r.q = (uint32_t)((rc.len + 15) >> 4);
+        r.off = rc.off;
+        r.len = rc.len;
+        r.tail = (uint32_t)(rc.len & 15);
+    } else {
+        r.chain = (uint32_t)(item / p.segs_full);
+        r.s = (uint32_t)(item - (uint64_t)r.chain * p.segs_full);
+        const bool last = r.chain == p.n_chains - 1;
+        r.q = last ? p.q_last : p.qc;
+        r.S = last ? p.segs_last : p.segs_full;
+        r.off = (uint64_t)r.chain * p.chain_bytes;
+        r.len = last ? p.last_len : p.chain_bytes;
+        r.tail = last ? (uint32_t)(p.last_len & 15) : 0u;
+    }
     r.e = r.q - ((r.S - 1 - r.s) << p.seg_log2);
     r.b = r.s == 0 ? 0u : r.e - (1u << p.seg_log2);
     return r;
@@ -300,20 +318,33 @@ __device__ __forceinline__ u4 mul_x64(const u4 &y)
     return r;
 }
 
-// X . Y for a wave-uniform X: lanes 0..31 each look up one nibble position of
-// Y's 4-bit table and the wave XOR sums the 32 entries. Every lane receives the
-// product.
-__device__ inline u4 coop_mul_tab4(const u4 &x, const Tab4 *__restrict__ t, uint32_t lane)
+// X . Y where the L = 2^LL lanes of each aligned lane group hold one X (the
+// groups may differ) and t points to Y's 4-bit table (it may differ per group
+// as well): lane j of a group looks up the nibble positions j, j + L, ... < 32
+// of X and the group XOR-sums the entries. Every lane of a group receives its
+// group's product.
+template <int LL>
+__device__ inline u4 group_mul_tab4(const u4 &x, const Tab4 *__restrict__ t, uint32_t jl)
 {
+    constexpr uint32_t L = 1u << LL;
     u4 r = zero4();
-    if (lane < 32) {
-        const uint32_t w = lane < 8 ? x.w[0] : (lane < 16 ? x.w[1] : (lane < 24 ? x.w[2] : x.w[3]));
-        const uint32_t byte = (w >> (8 * ((lane >> 1) & 3))) & 0xFFu;
-        const uint32_t nib = (lane & 1) ? (byte & 0xFu) : (byte >> 4);
-        const uint4 e = *reinterpret_cast<const uint4 *>(t->e[lane][nib]);
-        r.w[0] = e.x; r.w[1] = e.y; r.w[2] = e.z; r.w[3] = e.w;
+#pragma unroll
+    for (uint32_t rep = 0; rep < (L < 32 ? 32 / L : 1); ++rep) {
+        const uint32_t pos = jl + rep * L;   // nibble position: word pos/8, byte (pos/2)%4, high nibble first
+        if (pos < 32) {
+            const uint32_t lo = (pos & 8) ? x.w[1] : x.w[0], hi = (pos & 8) ? x.w[3] : x.w[2];
+            const uint32_t w = (pos & 16) ? hi : lo;
+            const uint32_t byte = (w >> (8 * ((pos >> 1) & 3))) & 0xFFu;
+            const uint32_t nib = (pos & 1) ? (byte & 0xFu) : (byte >> 4);
+            const uint4 e = *reinterpret_cast<const uint4 *>(t->e[pos][nib]);
+            r.w[0] ^= e.x; r.w[1] ^= e.y; r.w[2] ^= e.z; r.w[3] ^= e.w;
+        }
     }
-    return wave_xor(r);
+#pragma unroll
+    for (uint32_t off = L / 2; off >= 1; off >>= 1)
+        for (int w = 0; w < 4; ++w)
+            r.w[w] ^= __shfl_xor(r.w[w], off, 64);
+    return r;
 }
 
 // AAD block u of a chain's AAD (zero-padded); one vector load when it is whole and aligned.
@@ -448,10 +479,11 @@ __device__ __forceinline__ u4 ghash_step(const uint4 *g8, const u4 &acc, const u
 // Lanes per item L = 2^LL. Item slot g of a wave (lanes g*L .. g*L+L-1) takes
 // L consecutive blocks of its segment per iteration; each lane keeps a Horner
 // accumulator with multiplier H^L, and lane j's accumulator carries the weight
-// H^(L-j) in its segment (times one more H for the tag). SPLIT (64 lanes only):
-// chains are cut into segments whose partials a second kernel sums. MODE is a
+// H^(L-j) in its segment (times one more H for the tag). SPLIT: chains are cut
+// into segments whose weighted partials a second kernel sums. MODE is a
 // GcmMode: which of keystream, data XOR and GHASH + tag the launch computes.
-template <bool ENC, int LL, bool SPLIT, int MODE>
+// RAG: chains of their own offsets and lengths from the launch's chain table.
+template <bool ENC, int LL, bool SPLIT, int MODE, bool RAG>
 __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) void gcm_kernel(GcmLaunch p)
 {
     constexpr bool kGhash = MODE == kFused || MODE == kVerify || MODE == kApplyKs;   // GHASH + tag
@@ -508,7 +540,7 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
     const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerWg + (tid >> 6));
     const uint64_t n_wave_items = (p.n_items + G - 1) / G;
     const uint32_t seg = 1u << p.seg_log2;
-    const uint32_t Ku = ((seg < p.qc ? seg : p.qc) + L - 1) >> LL;   // iterations per item, uniform
+    const uint32_t Ku_uniform = ((seg < p.qc ? seg : p.qc) + L - 1) >> LL;   // iterations per item
     // The tag mask AES_K(J0) xor L . H of the chains of this wave's next L
     // wave-items, one per lane: lane b*G + g holds the mask of slot g of the b-th
     // of them. One lane-parallel AES pass serves L wave-items.
@@ -518,22 +550,41 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
         const uint32_t bi = it & (L - 1);
         if (kGhash && bi == 0) {
             const uint64_t bitem = (wi + (uint64_t)(lane >> (6 - LL)) * nwaves) * G + (lane & (G - 1));
-            const ItemPos bp = item_pos(p, bitem < p.n_items ? bitem : p.n_items - 1);
+            const ItemPos bp = item_pos<RAG>(p, bitem < p.n_items ? bitem : p.n_items - 1);
             uint32_t biv[3];
             chain_iv(p, p.chain_base + bp.chain, biv);
             const u4 j0 = {{biv[0], biv[1], biv[2], bswap32(1u)}};   // J0 = IV_i || 0^31 || 1
-            const LenTerms lt = len_terms(p, lane);
+            u4 lenh;
+            if constexpr (RAG) {   // every chain has its own length: each lane multiplies its own
+                const uint64_t abits = (uint64_t)p.aad_bytes * 8, cbits = bp.len * 8;
+                const u4 lens = {{bswap32((uint32_t)(abits >> 32)), bswap32((uint32_t)abits),
+                                  bswap32((uint32_t)(cbits >> 32)), bswap32((uint32_t)cbits)}};
+                lenh = mul_tab4(lens, &c->h1_tab);
+            } else {
+                const LenTerms lt = len_terms(p, lane);
+                lenh = bp.chain == p.n_chains - 1 ? lt.last : lt.full;
+            }
             u4 e;
             if constexpr (kAes)
                 e = aes_block_lds(lds, rk, j0, lc0, lc1, lc2, lc3);
             else
                 e = aes256_encrypt_tt(j0, c->rk, [&](uint32_t x) { return t0l[x]; });
-            jmask = xor4(e, bp.chain == p.n_chains - 1 ? lt.last : lt.full);
+            jmask = xor4(e, lenh);
         }
         const uint64_t item = wi * G + gs;
         const bool valid = item < p.n_items;
-        const ItemPos ip = item_pos(p, valid ? item : p.n_items - 1);
+        const ItemPos ip = item_pos<RAG>(p, valid ? item : p.n_items - 1);
         const uint64_t gchain = p.chain_base + ip.chain;
+        // Iterations of this wave-item: uniform for uniform chains; for ragged chains
+        // the longest of the wave's segments (shorter ones are padded in front).
+        uint32_t Ku = Ku_uniform;
+        if constexpr (RAG) {
+            uint32_t ku = valid ? (ip.e - ip.b + L - 1) >> LL : 0u;
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1)
+                ku = max(ku, (uint32_t)__shfl_xor((int)ku, off, 64));
+            Ku = __builtin_amdgcn_readfirstlane(ku);
+        }
         uint32_t iv[3];
         chain_iv(p, gchain, iv);
         // Counter mode: columns 0..2 of the state after AddRoundKey are the IV and
@@ -546,11 +597,10 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
             p2 = xor3(tlk(lds, c2, lc0, FT_SEL(0)), tlk(lds, c0, lc2, FT_SEL(2)), xor3(tlk(lds, c1, lc3, FT_SEL(3)), rk[6], 0u));
             p3 = xor3(tlk(lds, c0, lc1, FT_SEL(1)), tlk(lds, c1, lc2, FT_SEL(2)), xor3(tlk(lds, c2, lc3, FT_SEL(3)), rk[7], 0u));
         }
-        const uint8_t *src = kRead ? p.in + (uint64_t)ip.chain * p.chain_bytes : nullptr;
-        uint8_t *dst = kWrite ? p.out + (uint64_t)ip.chain * p.chain_bytes : nullptr;
-        const uint8_t *ksrc = MODE == kApplyKs ? p.ks + (uint64_t)ip.chain * p.chain_bytes : nullptr;
-        const bool last_chain = ip.chain == p.n_chains - 1;
-        const uint32_t tail = last_chain ? (uint32_t)(p.last_len & 15) : 0u;   // bytes of a final partial block
+        const uint8_t *src = kRead ? p.in + ip.off : nullptr;
+        uint8_t *dst = kWrite ? p.out + ip.off : nullptr;
+        const uint8_t *ksrc = MODE == kApplyKs ? p.ks + ip.off : nullptr;
+        const uint32_t tail = ip.tail;   // bytes of a final partial block
         const int pad = (int)((Ku << LL) - (ip.e - ip.b));                   // zero blocks in front
         // The AAD blocks precede ciphertext block 0 of the chain in GHASH order: in
         // segment 0, AAD block u takes the slot v = u - na just before it. Lane jl
@@ -697,20 +747,30 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                 for (int w = 0; w < 4; ++w)
                     acc.w[w] ^= __shfl_xor(acc.w[w], off, 64);
             if (SPLIT) {
-                // A chain cut into S segments (only with 64 lanes per item): segment s
-                // carries the weight H^((S-1-s) . 2^seg_log2) inside its chain. The
-                // partials and segment 0's mask go to memory; the chain kernel sums them.
-                uint32_t m = ip.S - 1 - ip.s;
-                while (m) {
-                    const uint32_t b = __builtin_ctz(m);
-                    acc = coop_mul_tab4(acc, &c->sq_tab[p.seg_log2 + b], lane);
-                    m &= m - 1;
+                // A chain cut into S segments: segment s carries the weight
+                // H^((S-1-s) . 2^seg_log2) inside its chain, one multiply by a
+                // square H^(2^(seg_log2+b)) per set bit b of S-1-s, shared by the
+                // item's lanes. The partials and segment 0's mask go to memory; the
+                // chain kernel sums them.
+                uint32_t m = valid ? ip.S - 1 - ip.s : 0u;
+                uint32_t rounds = __popc(m);
+#pragma unroll
+                for (int off = 32; off >= 1; off >>= 1)
+                    rounds = max(rounds, (uint32_t)__shfl_xor((int)rounds, off, 64));
+                rounds = __builtin_amdgcn_readfirstlane(rounds);
+                for (uint32_t r = 0; r < rounds; ++r) {
+                    const uint32_t b = m ? (uint32_t)__builtin_ctz(m) : 0u;
+                    const u4 prod = group_mul_tab4<LL>(acc, &c->sq_tab[p.seg_log2 + b], jl);
+                    if (m) {
+                        acc = prod;
+                        m &= m - 1;
+                    }
                 }
                 const uint32_t src_lane = bi * G + gs;
                 u4 e;
                 for (int w = 0; w < 4; ++w)
                     e.w[w] = __shfl(jmask.w[w], (int)src_lane, 64);
-                if (lane == 0) {
+                if (valid && jl == 0) {
                     p.partials[item] = make_uint4(acc.w[0], acc.w[1], acc.w[2], acc.w[3]);
                     if (ip.s == 0)
                         p.masks[ip.chain] = make_uint4(e.w[0], e.w[1], e.w[2], e.w[3]);
@@ -733,7 +793,7 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
 // the wave XOR-sums them.
 constexpr int kTagThreads = 256;
 
-template <bool ENC>
+template <bool ENC, bool RAG>
 __global__ __launch_bounds__(kTagThreads) void chain_tag_kernel(GcmLaunch p)
 {
     const uint32_t chain = __builtin_amdgcn_readfirstlane(blockIdx.x * (kTagThreads / 64) + (threadIdx.x >> 6));
@@ -741,8 +801,16 @@ __global__ __launch_bounds__(kTagThreads) void chain_tag_kernel(GcmLaunch p)
     if (chain >= p.n_chains)
         return;
     const uint64_t gchain = p.chain_base + chain;
-    const uint32_t S = chain == p.n_chains - 1 ? p.segs_last : p.segs_full;
-    const uint4 *part = p.partials + (uint64_t)chain * p.segs_full;
+    uint32_t S;
+    const uint4 *part;
+    if constexpr (RAG) {
+        const RaggedChain rc = p.rchains[chain];
+        S = rc.segs;
+        part = p.partials + rc.item_base;
+    } else {
+        S = chain == p.n_chains - 1 ? p.segs_last : p.segs_full;
+        part = p.partials + (uint64_t)chain * p.segs_full;
+    }
     u4 t = zero4();
     for (uint32_t s = lane; s < S; s += 64) {
         const uint4 g = part[s];
@@ -804,7 +872,7 @@ __global__ __launch_bounds__(256) void seq_ghash_kernel(GcmLaunch p)
     emit_tag<ENC>(p, gchain, tag, ENC ? zero4() : load16(p.tags_in + 16 * gchain));
 }
 
-template <bool ENC, int MODE>
+template <bool ENC, int MODE, bool RAG>
 static hipError_t launch_mode(const GcmLaunch &p, int num_cu, hipStream_t s)
 {
     constexpr bool ghash = MODE == kFused || MODE == kVerify || MODE == kApplyKs;
@@ -815,36 +883,46 @@ static hipError_t launch_mode(const GcmLaunch &p, int num_cu, hipStream_t s)
     uint64_t wgs = (waves + kWavesPerWg - 1) / kWavesPerWg;
     if (wgs > (uint64_t)num_cu * gcm_wgs_per_cu(MODE))
         wgs = (uint64_t)num_cu * gcm_wgs_per_cu(MODE);
-    if (p.lanes_log2 == 4)
-        hipLaunchKernelGGL((gcm_kernel<ENC, 4, false, MODE>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+    const bool split = ghash && p.split;
+    if (p.lanes_log2 == 4 && !split)
+        hipLaunchKernelGGL((gcm_kernel<ENC, 4, false, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+    else if (p.lanes_log2 == 4)
+        hipLaunchKernelGGL((gcm_kernel<ENC, 4, ghash, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+    else if (p.lanes_log2 == 5 && !split)
+        hipLaunchKernelGGL((gcm_kernel<ENC, 5, false, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
     else if (p.lanes_log2 == 5)
-        hipLaunchKernelGGL((gcm_kernel<ENC, 5, false, MODE>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
-    else if (!ghash || !p.split)
-        hipLaunchKernelGGL((gcm_kernel<ENC, 6, false, MODE>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+        hipLaunchKernelGGL((gcm_kernel<ENC, 5, ghash, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+    else if (!split)
+        hipLaunchKernelGGL((gcm_kernel<ENC, 6, false, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
     else
-        hipLaunchKernelGGL((gcm_kernel<ENC, 6, ghash, MODE>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+        hipLaunchKernelGGL((gcm_kernel<ENC, 6, ghash, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !ghash || !p.split)
         return e;
     constexpr uint32_t per_block = kTagThreads / 64;
-    hipLaunchKernelGGL(chain_tag_kernel<ENC>, dim3((p.n_chains + per_block - 1) / per_block), dim3(kTagThreads), 0, s,
-                       p);
+    hipLaunchKernelGGL((chain_tag_kernel<ENC, RAG>), dim3((p.n_chains + per_block - 1) / per_block), dim3(kTagThreads),
+                       0, s, p);
     return hipGetLastError();
 }
 
 hipError_t launch_gcm(const GcmLaunch &p, bool encrypt, GcmMode mode, int num_cu, hipStream_t s)
 {
+    if (p.rchains) {   // ragged chains: the fused path only
+        if (mode != kFused)
+            return hipErrorInvalidValue;
+        return encrypt ? launch_mode<true, kFused, true>(p, num_cu, s) : launch_mode<false, kFused, true>(p, num_cu, s);
+    }
     switch (mode) {
     case kFused:
-        return encrypt ? launch_mode<true, kFused>(p, num_cu, s) : launch_mode<false, kFused>(p, num_cu, s);
+        return encrypt ? launch_mode<true, kFused, false>(p, num_cu, s) : launch_mode<false, kFused, false>(p, num_cu, s);
     case kCtr:
-        return launch_mode<false, kCtr>(p, num_cu, s);   // CTR is its own inverse
+        return launch_mode<false, kCtr, false>(p, num_cu, s);   // CTR is its own inverse
     case kVerify:
-        return launch_mode<false, kVerify>(p, num_cu, s);
+        return launch_mode<false, kVerify, false>(p, num_cu, s);
     case kKeystream:
-        return launch_mode<false, kKeystream>(p, num_cu, s);
+        return launch_mode<false, kKeystream, false>(p, num_cu, s);
     case kApplyKs:
-        return launch_mode<false, kApplyKs>(p, num_cu, s);
+        return launch_mode<false, kApplyKs, false>(p, num_cu, s);
     }
     return hipErrorInvalidValue;
 }

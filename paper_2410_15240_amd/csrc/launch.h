@@ -29,6 +29,16 @@ enum GcmMode : int {
 // CU's whole LDS; the GHASH-only modes need 33 KiB, and two fit the registers.
 constexpr int gcm_wgs_per_cu(int mode) { return mode == kVerify || mode == kApplyKs ? 2 : 1; }
 
+// One chain of a ragged launch: bytes [off, off + len) of the buffers (off a
+// multiple of 16); its segments are the items item_base .. item_base + segs - 1.
+struct RaggedChain {
+    uint64_t off;
+    uint64_t len;
+    uint64_t item_base;
+    uint32_t segs;
+    uint32_t reserved;
+};
+
 // One launch of the streaming kernel over `n_chains` consecutive chains.
 // The work is split into items (chain, segment); a segment is a run of
 // 2^seg_log2 blocks aligned to the END of its chain (segment 0 may be short).
@@ -63,6 +73,11 @@ struct GcmLaunch {
     uint4 *partials;
     uint4 *masks;
     uint32_t split;
+    // Ragged launches (chains of their own lengths and offsets): the chain table
+    // and each item's chain; chain_bytes, qc, last_len and the segs_* fields
+    // are then unused. NULL for uniform chains.
+    const RaggedChain *rchains;
+    const uint32_t *ritem_chain;
 };
 
 hipError_t launch_key_setup(const uint32_t key_words[8], KeyCtx *ctx, hipStream_t s);

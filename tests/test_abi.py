@@ -27,7 +27,8 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for want in ("fastrack_gcm_decrypt_verify", "fastrack_gcm_encrypt_tag", "fastrack_pipeline_h2d",
-                 "fastrack_num_chains", "fastrack_last_error", "fastrack_shutdown", "fastrack_pipeline_stage_bytes"):
+                 "fastrack_num_chains", "fastrack_last_error", "fastrack_shutdown", "fastrack_pipeline_stage_bytes",
+                 "fastrack_gcm_decrypt_verify_ragged", "fastrack_gcm_encrypt_tag_ragged", "fastrack_sample_chains"):
         assert want in names
 
 
@@ -176,3 +177,67 @@ def d2h(L, chain=4096, pt=A, length=65536, chunk=16384, ct=B, tags=B + 0x100000,
                                 dict(h_tags=None), dict(ct=A + 16), dict(pt=A + 4), dict(chain=0)])
 def test_pipeline_d2h_rejects_bad_arguments(L, kw):
     assert d2h(L, **kw) == -1
+
+
+def u64s(*v):
+    return (ctypes.c_uint64 * max(len(v), 1))(*v)
+
+
+def rag_dec(L, off=(0, 4096, 8192), ln=(4096, 100, 0), n=None, ct=A, tags=B + 0x100000, pt=B, ok=B + 0x200000,
+            aad=None, abytes=0, key=KEY):
+    n = (3 if off is None else len(off)) if n is None else n
+    o = None if off is None else u64s(*off)
+    l = None if ln is None else u64s(*ln)
+    return L.fastrack_gcm_decrypt_verify_ragged(key, IV, o, l, n, ct, tags, aad, abytes, pt, ok, None)
+
+
+def rag_enc(L, off=(0, 4096), ln=(4096, 100), pt=A, ct=B, tags=B + 0x100000):
+    return L.fastrack_gcm_encrypt_tag_ragged(KEY, IV, u64s(*off), u64s(*ln), len(off), pt, None, 0, ct, tags, None)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(off=(0, 4100, 8192)),               # misaligned chain offset
+    dict(off=(0, 4096, 4096 + 64)),          # chain 2 starts inside chain 1 (100 bytes, 7 blocks)
+    dict(off=(4096, 0, 8192)),               # decreasing
+    dict(off=None), dict(ln=None), dict(key=None),
+    dict(ln=(4096, (1 << 32) * 16, 0)),       # oversized chain
+    dict(ct=None), dict(ct=A + 8), dict(pt=A + 16), dict(tags=None), dict(ok=None),
+    dict(abytes=1, aad=None),
+])
+def test_ragged_decrypt_rejects_bad_arguments(L, kw):
+    assert rag_dec(L, **kw) == -1
+    assert L.fastrack_last_error()
+
+
+@pytest.mark.parametrize("kw", [dict(tags=None), dict(off=(16, 0)), dict(pt=A + 4)])
+def test_ragged_encrypt_rejects_bad_arguments(L, kw):
+    assert rag_enc(L, **kw) == -1
+
+
+def test_ragged_no_chains_is_a_no_op(L):
+    assert rag_dec(L, off=(), ln=(), n=0) == 0
+
+
+def test_ragged_empty_chains_need_no_data_buffers(L):
+    assert rag_dec(L, off=(0, 16), ln=(0, 0), ct=None, pt=None, key=None) == -1   # still checks the rest
+    assert rag_dec(L, off=(0, 16), ln=(0, 1), ct=None, pt=None) == -1
+
+
+def test_sample_chains_layout(L):
+    """Samples packed back to back, each 16-byte aligned, each cut into equal whole-block parts."""
+    lens = [100, 0, 33, 4096, 5]
+    k = 4
+    n = len(lens) * k
+    off, ln = (ctypes.c_uint64 * n)(), (ctypes.c_uint64 * n)()
+    total = L.fastrack_sample_chains(u64s(*lens), len(lens), k, off, ln)
+    want_off, want_len, pos = [], [], 0
+    for s in lens:
+        part = -(-(-(-s // k)) // 16) * 16          # ceil(ceil(s / k) / 16) * 16
+        for j in range(k):
+            b = min(j * part, s)
+            want_off.append(pos + b)
+            want_len.append(min(part, s - b))
+        pos += -(-s // 16) * 16
+    assert list(off) == want_off and list(ln) == want_len and total == pos
+    assert sum(want_len) == sum(lens)
+    assert L.fastrack_sample_chains(u64s(*lens), len(lens), 0, off, ln) == 0

@@ -417,3 +417,63 @@ def test_multichain_costs_match_the_paper():
         assert costs[n][0] - costs[1][0] == n - 1            # n-1 more tags
         assert costs[n][1] == n * facts["serial_aad_bytes"]["value"]   # n AAD bytes
         assert costs[n][2] - costs[1][2] == n - 1            # n-1 more AES blocks (one J0 per chain)
+
+
+# --------------------------------------------------------------------------
+# Per-sample (ragged) chains (paper sections 5.2 and 5.4)
+# --------------------------------------------------------------------------
+
+@needs_libcrypto
+def test_ragged_chains_are_standard_gcm_at_their_offsets():
+    w = W.ragged_case(1, [0, 1, 17, 4096, 15, 33, 1000, 16], gaps=[0, 2, 0, 1, 0, 3, 0, 0], aad_bytes=3)
+    off, ln, aad = w.extra["chain_off"], w.extra["chain_len"], w.extra["aad"]
+    fill = np.full(w.payload.size, 0xA5, np.uint8)
+    ct, tags = oracle.ragged_encrypt(w.key, w.base_iv, off, ln, w.payload, aad, 3, out=fill.copy())
+    covered = np.zeros(w.payload.size, bool)
+    for i in range(off.size):
+        o, l = int(off[i]), int(ln[i])
+        covered[o:o + l] = True
+        c, t = LC.gcm_encrypt(w.key, bytes(oracle.chain_iv(w.base_iv, i)), w.payload[o:o + l], aad[i])
+        assert bytes(ct[o:o + l]) == c and bytes(tags[i]) == t, i
+    assert (ct[~covered] == 0xA5).all()       # bytes outside every chain are left alone
+    pt, ok = oracle.ragged_decrypt(w.key, w.base_iv, off, ln, ct, tags, aad, 3)
+    assert ok.all() and np.array_equal(pt[covered], w.payload[covered])
+
+
+def test_ragged_with_uniform_offsets_is_the_uniform_layout():
+    r = rng(67)
+    key, base_iv = rbytes(r, 32), rbytes(r, 12)
+    chain, length = 1024, 9 * 1024 + 300
+    pt = rbytes(r, length)
+    n = W.n_chains(length, chain)
+    off = np.arange(n, dtype=np.uint64) * chain
+    ln = np.minimum(chain, length - off.astype(np.int64)).astype(np.uint64)
+    aad = rbytes(r, n * 32).reshape(n, 32)
+    want = oracle.chains_encrypt(key, base_iv, chain, pt, aad, 32)
+    got = oracle.ragged_encrypt(key, base_iv, off, ln, pt, aad, 32)
+    assert np.array_equal(got[0], want[0]) and np.array_equal(got[1], want[1])
+
+
+def test_ragged_sample_reorder_and_tamper_are_caught_per_chain():
+    """Section 5.4: the serial-number AAD exposes chains moved within a sample."""
+    w = W.sample_batch(n_samples=3, chains_per_sample=4, median=3000, sigma=0.3, lo=100, hi=5000)
+    lens = w.extra["sample_lens"]
+    offs, cl = [], []
+    for o, l in zip(w.extra["sample_off"].tolist(), lens.tolist()):
+        part = ((l + 3) // 4 + 15) // 16 * 16
+        for j in range(4):
+            b = min(j * part, l)
+            offs.append(o + b)
+            cl.append(min(part, l - b))
+    off, ln = np.array(offs, np.uint64), np.array(cl, np.uint64)
+    aad = w.extra["aad"]
+    ct, tags = oracle.ragged_encrypt(w.key, w.base_iv, off, ln, w.payload, aad, 1)
+    # the same ciphertext and tag under another serial number (chain 1 presented as chain 2)
+    a2 = aad.copy()
+    a2[[1, 2]] = aad[[2, 1]]
+    _, ok = oracle.ragged_decrypt(w.key, w.base_iv, off, ln, ct, tags, a2, 1)
+    assert ok.tolist() == [1, 0, 0] + [1] * 9
+    c2 = ct.copy()
+    W.flip_bit(c2[int(off[6]):int(off[6] + ln[6])], 5)
+    _, ok = oracle.ragged_decrypt(w.key, w.base_iv, off, ln, c2, tags, aad, 1)
+    assert ok.tolist() == [1] * 6 + [0] + [1] * 5

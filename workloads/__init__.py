@@ -176,3 +176,54 @@ def case_aad(w: Workload, chain_bytes: int) -> Optional[np.ndarray]:
     if "aad" in w.extra:
         return w.extra["aad"]
     return w.aad(chain_bytes)
+
+
+def sample_batch(n_samples: int = 256, chains_per_sample: int = 16, seed: int = 6, median: int = 110 * KiB,
+                 sigma: float = 0.6, lo: int = 4 * KiB, hi: int = MiB) -> Workload:
+    """A batch of variable-size samples in the paper's per-sample chain layout (sections 5.2 and 5.4).
+
+    Sample sizes are log-normal (median ``median`` bytes, shape ``sigma``) clipped to [lo, hi] and not
+    multiples of 16 in general: compressed-image-like files standing in for a batch of ImageNet JPEGs
+    (the paper's ResNet-50 workload, section 6.1). Samples are packed back to back, each starting
+    16-byte aligned, with zero bytes in the gaps; the payload bytes are uniform (compressed data is
+    high-entropy). Each sample is cut into ``chains_per_sample`` chains (16 tags per sample as in the
+    paper's evaluation, section 6.3), and each chain carries its 1-byte serial number within the sample as
+    AAD. ``extra`` holds sample_lens, sample_off, chains_per_sample and the AAD array (uint8[n, 1]).
+    """
+    rng = rng_for(seed)
+    key, iv = draw_key_iv(rng)
+    lens = np.clip(np.round(median * np.exp(sigma * rng.standard_normal(n_samples))), lo, hi).astype(np.uint64)
+    padded = (lens + np.uint64(15)) & ~np.uint64(15)
+    offs = np.zeros(n_samples, np.uint64)
+    if n_samples > 1:
+        offs[1:] = np.cumsum(padded)[:-1]
+    total = int(padded.sum())
+    payload = np.zeros(total, np.uint8)
+    for o, l in zip(offs.tolist(), lens.tolist()):
+        payload[o:o + l] = np.frombuffer(rng.bytes(l), np.uint8)
+    serial = np.tile(np.arange(chains_per_sample, dtype=np.uint8), n_samples).reshape(-1, 1)
+    return Workload("sample-batch-%d" % n_samples, key, iv, payload, [], aad_bytes=1,
+                    extra={"sample_lens": lens, "sample_off": offs, "chains_per_sample": chains_per_sample,
+                           "aad": serial})
+
+
+def ragged_case(seed: int, chain_lens, gaps=None, aad_bytes: int = 0) -> Workload:
+    """Small seeded ragged case: chains of the given lengths laid out in order, chain i starting at the
+    16-byte-aligned end of chain i-1 plus gaps[i] blocks; uniform bytes, arbitrary AAD bytes.
+    ``extra`` holds chain_off and chain_len (uint64)."""
+    rng = np.random.Generator(np.random.PCG64(SEED_BASE + 2000 + seed))
+    key, iv = draw_key_iv(rng)
+    ln = np.asarray(chain_lens, dtype=np.uint64)
+    g = np.zeros(ln.size, np.uint64) if gaps is None else np.asarray(gaps, dtype=np.uint64)
+    off = np.zeros(ln.size, np.uint64)
+    pos = 0
+    for i in range(ln.size):
+        pos += 16 * int(g[i])
+        off[i] = pos
+        pos += (int(ln[i]) + 15) // 16 * 16
+    payload = np.frombuffer(rng.bytes(pos), np.uint8).copy() if pos else np.zeros(0, np.uint8)
+    w = Workload("ragged-%d" % seed, key, iv, payload, [], aad_bytes=aad_bytes,
+                 extra={"chain_off": off, "chain_len": ln})
+    if aad_bytes:
+        w.extra["aad"] = np.frombuffer(rng.bytes(ln.size * aad_bytes), np.uint8).reshape(-1, aad_bytes).copy()
+    return w
