@@ -264,7 +264,7 @@ __device__ __forceinline__ ItemPos item_pos(const GcmLaunch &p, uint64_t item)
 // The streaming kernel
 // ===========================================================================
 //
-// LDS layout (160 KiB, one workgroup per CU):
+// LDS layout (160 KiB, one 1024-thread workgroup per CU):
 //   [0, 64 KiB)        region 0: row x (256 B) = T0[x] for lanes 0..31 | T1[x] for lanes 0..31
 //   [64, 128 KiB)      region 1: row x        = T2[x] ...              | T3[x] ...
 //   [128, 160 KiB)     positions 0..7 of the 8-bit table of H^L: entry (k, v) at 128 KiB + (k*256 + v)*16
@@ -289,16 +289,6 @@ constexpr uint32_t kLdsGhashOnly = 33 * 1024;  // modes without data AES: the GH
 __device__ __forceinline__ uint32_t tlk(const char *lds, uint32_t word, uint32_t lanec, uint32_t sel)
 {
     return *reinterpret_cast<const uint32_t *>(lds + __builtin_amdgcn_perm(word, lanec, sel));
-}
-
-// A uniform value held in a VGPR: the 60 round-key words stay resident in
-// vector registers (the kernel has room for them) instead of overflowing the
-// scalar register file.
-__device__ __forceinline__ uint32_t in_vgpr(uint32_t x)
-{
-    uint32_t r;
-    asm("v_mov_b32 %0, %1" : "=v"(r) : "s"(x));
-    return r;
 }
 
 // Y . x^64 in little-endian-word form: bytes 0..7 move to bytes 8..15 and the
@@ -509,32 +499,51 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
 
     {
         if (kAes) {
+            // Pass k of a wave writes the 64 words (w + k W) * 64 + [0, 64) of region
+            // (w + k W) / 256, all from one T0 row: lane k fetches that row up front
+            // and each pass broadcasts it, so no pass waits on memory.
             uint32_t *t = reinterpret_cast<uint32_t *>(lds4);
-            for (int i = tid; i < 32768; i += kThreads) {
-                const uint32_t region = i >> 14, row = (i >> 6) & 255, tab = region * 2 + ((i >> 5) & 1);
-                const uint32_t v = c->t0[row];
-                t[i] = tab == 0 ? v : rotl32(v, 8 * tab);
+            constexpr uint32_t kPasses = (32768 + kThreads - 1) / kThreads;
+            static_assert(kPasses <= 64, "one T0 row per lane and pass");
+            const uint32_t w = (uint32_t)tid >> 6;
+            const uint32_t mine = c->t0[(w + kWavesPerWg * lane) & 255];
+#pragma unroll 8
+            for (uint32_t k = 0; k < kPasses; ++k) {
+                const uint32_t ib = (w << 6) + k * kThreads;   // wave-uniform
+                if (ib < 32768) {
+                    const uint32_t v = __builtin_amdgcn_readlane(mine, k);
+                    const uint32_t tab = ((ib >> 13) & 2) | ((lane >> 5) & 1);
+                    t[ib + lane] = tab == 0 ? v : rotl32(v, 8 * tab);
+                }
             }
         } else {
             for (int i = tid; i < 256; i += kThreads)
                 t0l[i] = c->t0[i];
         }
-        if (kGhash) {
+        if (kGhash) {   // all loads of the 32 KiB table first, then the stores
             const uint4 *g = reinterpret_cast<const uint4 *>(c->g8[LL - 4]);
-            for (int i = tid; i < 2048; i += kThreads)
-                lds4[(kAes ? kG8Base : 0) + i] = g[i];
+            constexpr int kPer = (2048 + kThreads - 1) / kThreads;
+            uint4 gv[kPer];
+#pragma unroll
+            for (int r = 0; r < kPer; ++r)
+                gv[r] = g[min(tid + r * kThreads, 2047)];
+#pragma unroll
+            for (int r = 0; r < kPer; ++r)
+                if (tid + r * kThreads < 2048)
+                    lds4[(kAes ? kG8Base : 0) + tid + r * kThreads] = gv[r];
         }
     }
     __syncthreads();
 
     const uint32_t lb = (lane & 31) << 2;
     const uint32_t lc0 = lb, lc1 = lb | 0x80u, lc2 = lb | 0x10000u, lc3 = lb | 0x10080u;
-    // The 60 round-key words live in vector registers: the scalar file is
-    // taken by the launch parameters and per-item state.
+    // The 60 round-key words are uniform: they stay in scalar registers (the XORs
+    // take them as scalar operands), which keeps the kernel within the 128 VGPRs
+    // that four waves per SIMD allow.
     uint32_t rk[60];
 #pragma unroll
     for (int i = 0; i < 60; ++i)
-        rk[i] = kAes ? in_vgpr(__builtin_amdgcn_readfirstlane(c->rk[i])) : 0u;
+        rk[i] = kAes ? __builtin_amdgcn_readfirstlane(c->rk[i]) : 0u;
 
     const uint64_t nwaves = (uint64_t)gridDim.x * kWavesPerWg;
     const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerWg + (tid >> 6));

@@ -9,9 +9,11 @@
 namespace fastrack {
 
 // Threads per workgroup of the streaming kernel. Its 160 KiB of LDS allow one
-// workgroup per CU, so this is also the number of resident threads per CU.
+// workgroup per CU, so this is also the number of resident threads per CU:
+// 16 waves, four per SIMD, which the kernel's register use (at most 128 VGPRs)
+// allows. More waves per SIMD hide more of the LDS latency of the table lookups.
 #ifndef FT_GCM_THREADS
-#define FT_GCM_THREADS 512
+#define FT_GCM_THREADS 1024
 #endif
 constexpr int kGcmThreads = FT_GCM_THREADS;
 constexpr int kGcmWavesPerWg = kGcmThreads / 64;
@@ -26,8 +28,12 @@ enum GcmMode : int {
 };
 
 // Workgroups of the streaming kernel per CU: the modes with data AES take a
-// CU's whole LDS; the GHASH-only modes need 33 KiB, and two fit the registers.
-constexpr int gcm_wgs_per_cu(int mode) { return mode == kVerify || mode == kApplyKs ? 2 : 1; }
+// CU's whole LDS; the GHASH-only modes need 33 KiB and run 16 waves per CU too
+// (more would squeeze their registers).
+constexpr int gcm_wgs_per_cu(int mode)
+{
+    return (mode == kVerify || mode == kApplyKs) && kGcmWavesPerWg < 16 ? 16 / kGcmWavesPerWg : 1;
+}
 
 // One chain of a ragged launch: bytes [off, off + len) of the buffers (off a
 // multiple of 16); its segments are the items item_base .. item_base + segs - 1.

@@ -76,8 +76,8 @@ SMALL = [
     (3 * 4096 + 5, 4096, 1000), (3 * 65536 + 16, 65536, 2000), (2 * MiB + 100, 256 * KiB, 5003),
     (40, 16, 100),
     # many chains with 16 and 32 lanes each whose wave-items do not divide evenly over
-    # the waves of a 256-CU GPU: the chains are cut into segments
-    (8200 * 2048 + 100, 2048, 1), (5000 * 4096 - 7, 4096, 32),
+    # the 4096 resident waves of a 256-CU GPU: the chains are cut into segments
+    (16400 * 2048 + 100, 2048, 1), (9000 * 4096 - 7, 4096, 32),
 ]
 
 
