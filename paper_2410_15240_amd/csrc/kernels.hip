@@ -675,20 +675,44 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
             }
             return x;
         };
+        // Counter blocks of one 256-block group (the counter's upper 24 bits fixed):
+        // after round 1 only column 0 of the state varies (it takes the counter's low
+        // byte), so in round 2 the three lookups of each output column that read
+        // columns 1..3 are fixed too. q0..q3 cache those partial sums for the group
+        // gq of the lane's current counter.
+        uint32_t q0 = 0, q1 = 0, q2 = 0, q3 = 0, gq = 0xFFFFFFFFu;
+        auto group_setup = [&](uint32_t ctr) {
+            const uint32_t s3i = bswap32(ctr) ^ rk[3];
+            const uint32_t s1 = p1 ^ tlk(lds, s3i, lc2, FT_SEL(2));
+            const uint32_t s2 = p2 ^ tlk(lds, s3i, lc1, FT_SEL(1));
+            const uint32_t s3 = p3 ^ tlk(lds, s3i, lc0, FT_SEL(0));
+            q0 = xor3(tlk(lds, s1, lc1, FT_SEL(1)), tlk(lds, s2, lc2, FT_SEL(2)), xor3(tlk(lds, s3, lc3, FT_SEL(3)), rk[8], 0u));
+            q1 = xor3(tlk(lds, s1, lc0, FT_SEL(0)), tlk(lds, s2, lc1, FT_SEL(1)), xor3(tlk(lds, s3, lc2, FT_SEL(2)), rk[9], 0u));
+            q2 = xor3(tlk(lds, s2, lc0, FT_SEL(0)), tlk(lds, s3, lc1, FT_SEL(1)), xor3(tlk(lds, s1, lc3, FT_SEL(3)), rk[10], 0u));
+            q3 = xor3(tlk(lds, s3, lc0, FT_SEL(0)), tlk(lds, s1, lc2, FT_SEL(2)), xor3(tlk(lds, s2, lc3, FT_SEL(3)), rk[11], 0u));
+            gq = ctr >> 8;
+        };
+        const uint32_t k3 = rk[3] >> 24;   // key byte that meets the counter's low byte
         // Iteration k on the loaded data block d (and keystream block kv for kApplyKs).
         auto process = [&](uint32_t k, const Slot &q, const u4 &d, const u4 &kv) {
             const uint32_t t = q.t;
             u4 o;
             if constexpr (kAes) {
                 // Counter block IV_i || [t + 2]_32 (data blocks start at inc32(J0)).
-                const uint32_t s3i = bswap32(t + 2u) ^ rk[3];
-                // Round 1: only the counter column varies; it feeds row 3-j of output column j.
-                uint32_t s0 = p0 ^ tlk(lds, s3i, lc3, FT_SEL(3));
-                uint32_t s1 = p1 ^ tlk(lds, s3i, lc2, FT_SEL(2));
-                uint32_t s2 = p2 ^ tlk(lds, s3i, lc1, FT_SEL(1));
-                uint32_t s3 = p3 ^ tlk(lds, s3i, lc0, FT_SEL(0));
+                const uint32_t ctr = t + 2u;
+                const bool stale = q.active && (ctr >> 8) != gq;
+                if (__ballot(stale))
+                    if (stale)
+                        group_setup(ctr);
+                // Round 1, column 0 (T3 of the counter's low byte), then round 2 on the
+                // cached sums: each output column adds its one lookup of column 0.
+                const uint32_t c0 = p0 ^ tlk(lds, ctr ^ k3, lc3, FT_SEL(0));
+                uint32_t s0 = q0 ^ tlk(lds, c0, lc0, FT_SEL(0));
+                uint32_t s1 = q1 ^ tlk(lds, c0, lc3, FT_SEL(3));
+                uint32_t s2 = q2 ^ tlk(lds, c0, lc2, FT_SEL(2));
+                uint32_t s3 = q3 ^ tlk(lds, c0, lc1, FT_SEL(1));
 #pragma unroll
-                for (int r = 2; r < 14; ++r) {
+                for (int r = 3; r < 14; ++r) {
                     const uint32_t n0 = xor3(tlk(lds, s0, lc0, FT_SEL(0)), tlk(lds, s1, lc1, FT_SEL(1)),
                                              xor3(tlk(lds, s2, lc2, FT_SEL(2)), tlk(lds, s3, lc3, FT_SEL(3)), rk[4 * r + 0]));
                     const uint32_t n1 = xor3(tlk(lds, s1, lc0, FT_SEL(0)), tlk(lds, s2, lc1, FT_SEL(1)),
