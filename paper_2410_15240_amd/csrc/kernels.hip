@@ -546,7 +546,12 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
         rk[i] = kAes ? __builtin_amdgcn_readfirstlane(c->rk[i]) : 0u;
 
     const uint64_t nwaves = (uint64_t)gridDim.x * kWavesPerWg;
-    const uint32_t wave = __builtin_amdgcn_readfirstlane(blockIdx.x * kWavesPerWg + (tid >> 6));
+    // A launch with fewer wave-items than resident waves numbers its waves across
+    // the workgroups first, which spreads the wave-items over all CUs; a full
+    // launch keeps each workgroup's waves on consecutive wave-items.
+    const bool spread = ((p.n_items + G - 1) / G) < nwaves;
+    const uint32_t wave = __builtin_amdgcn_readfirstlane(spread ? (tid >> 6) * gridDim.x + blockIdx.x
+                                                                : blockIdx.x * kWavesPerWg + (tid >> 6));
     const uint64_t n_wave_items = (p.n_items + G - 1) / G;
     const uint32_t seg = 1u << p.seg_log2;
     const uint32_t Ku_uniform = ((seg < p.qc ? seg : p.qc) + L - 1) >> LL;   // iterations per item
@@ -913,7 +918,9 @@ static hipError_t launch_mode(const GcmLaunch &p, int num_cu, hipStream_t s)
         return hipSuccess;
     const uint64_t per_wave = 64u >> p.lanes_log2;
     const uint64_t waves = (p.n_items + per_wave - 1) / per_wave;
-    uint64_t wgs = (waves + kWavesPerWg - 1) / kWavesPerWg;
+    // One workgroup per CU (or per wave when there are fewer waves than CUs):
+    // the kernel numbers waves across workgroups, so small launches use every CU.
+    uint64_t wgs = waves;
     if (wgs > (uint64_t)num_cu * gcm_wgs_per_cu(MODE))
         wgs = (uint64_t)num_cu * gcm_wgs_per_cu(MODE);
     const bool split = ghash && p.split;
