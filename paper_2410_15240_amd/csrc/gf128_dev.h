@@ -112,6 +112,34 @@ __device__ inline u4 mul_tab4(const u4 &x, const Tab4 *__restrict__ t)
     return z;
 }
 
+// The same product with the eight lookups of each word in flight together
+// (the scheduling barrier keeps the batches apart, so at most 32 VGPRs hold
+// table entries): for latency-bound callers that run few multiplies in sequence.
+__device__ inline u4 mul_tab4_b8(const u4 &x, const Tab4 *__restrict__ t)
+{
+    u4 z = {{0u, 0u, 0u, 0u}};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const uint32_t w = x.w[j];
+        uint4 e[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const uint32_t byte = (w >> (8 * (q >> 1))) & 0xFFu;
+            const uint32_t nib = (q & 1) ? (byte & 0xFu) : (byte >> 4);
+            e[q] = *reinterpret_cast<const uint4 *>(t->e[8 * j + q][nib]);
+        }
+#pragma unroll
+        for (int q = 0; q < 8; q += 2) {
+            z.w[0] = xor3(z.w[0], e[q].x, e[q + 1].x);
+            z.w[1] = xor3(z.w[1], e[q].y, e[q + 1].y);
+            z.w[2] = xor3(z.w[2], e[q].z, e[q + 1].z);
+            z.w[3] = xor3(z.w[3], e[q].w, e[q + 1].w);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    return z;
+}
+
 __device__ __forceinline__ u4 xor4(const u4 &a, const u4 &b)
 {
     u4 r;

@@ -144,15 +144,13 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
         for (int j = 0; j < 4; ++j)
             ctx->hsq[i][j] = s_hsq[i].w[j];
 
-    // 4-bit tables: H, the lane weights H^(65-l) and every H^(2^t).
-    for (int task = tid; task < (1 + kMaxPow + kSquares) * kTab4Pos; task += blockDim.x) {
+    // 4-bit tables: H and every H^(2^t).
+    for (int task = tid; task < (1 + kSquares) * kTab4Pos; task += blockDim.x) {
         const int tbl = task / kTab4Pos, p = task % kTab4Pos;
         if (tbl == 0)
             build_tab4_row(s_hp[1], p, &ctx->h1_tab);
-        else if (tbl <= kMaxPow)
-            build_tab4_row(s_hp[kMaxPow + 1 - (tbl - 1)], p, &ctx->lane_tab[tbl - 1]);
         else
-            build_tab4_row(s_hsq[tbl - 1 - kMaxPow], p, &ctx->sq_tab[tbl - 1 - kMaxPow]);
+            build_tab4_row(s_hsq[tbl - 1], p, &ctx->sq_tab[tbl - 1]);
     }
 
     // 8-bit positional tables of H^16, H^32, H^64:
@@ -265,13 +263,17 @@ __device__ __forceinline__ ItemPos item_pos(const GcmLaunch &p, uint64_t item)
 // ===========================================================================
 //
 // LDS layout (160 KiB, one 1024-thread workgroup per CU):
-//   [0, 64 KiB)        region 0: row x (256 B) = T0[x] for lanes 0..31 | T1[x] for lanes 0..31
-//   [64, 128 KiB)      region 1: row x        = T2[x] ...              | T3[x] ...
+//   [0, 64 KiB)        row x (256 B) = T0[x] for lanes 0..31 | T1[x] for lanes 0..31
+//   [64, 112 KiB)      4-bit tables of H^(2^t), t = 0..5 (8 KiB each): the lane-combine tree
+//   [112 KiB, +64 B)   per-wave progress counters (see the priority steps in the kernel)
 //   [128, 160 KiB)     positions 0..7 of the 8-bit table of H^L: entry (k, v) at 128 KiB + (k*256 + v)*16
-// T_r[x] = rotl(T0[x], 8r). Lanes l and l+32 share a copy: the LDS serves a wave's
-// 32-bit reads 32 lanes at a time, so the 32 copies make every lookup
-// conflict-free. A T_r address is one v_perm_b32: byte 0 = (lane%32)*4 + 128*(r&1),
-// byte 1 = the state byte, byte 2 = r>>1 (the region), byte 3 = 0.
+// T_r[x] = rotl(T0[x], 8r), so T2[x] = rotl16(T0[x]) and T3[x] = rotl16(T1[x]): a
+// round column T0[a] ^ T1[b] ^ T2[c] ^ T3[d] ^ k is T0[a] ^ T1[b] ^ rotl16(T0[c] ^
+// T1[d] ^ rotl16(k)), one rotate more than with four tables, and the 64 KiB saved
+// hold the tables the lane combine needs. Lanes l and l+32 share a copy: the LDS
+// serves a wave's 32-bit reads 32 lanes at a time, so the 32 copies make every
+// lookup conflict-free. A T0/T1 address is one v_perm_b32: byte 0 = (lane%32)*4 +
+// 128*table, byte 1 = the state byte, bytes 2..3 = 0.
 // GHASH multiplies by H^L with the byte positions 8..15 folded onto 0..7: the
 // entry for byte position k+8 is the entry for position k times x^64, so
 //   X . H^L = sum_{k<8} E_k[x_k]  xor  (sum_{k<8} E_k[x_(k+8)]) . x^64.
@@ -280,7 +282,14 @@ constexpr int kThreads = kGcmThreads;
 constexpr int kWavesPerWg = kGcmWavesPerWg;
 constexpr uint32_t kLdsBytes = 160 * 1024;
 constexpr uint32_t kG8Base = 8192;           // uint4 index of the GHASH table in LDS
-constexpr uint32_t kLdsGhashOnly = 33 * 1024;  // modes without data AES: the GHASH table and T0
+constexpr int kTreeTabs = 6;                 // H^(2^t), t = 0..5: lanes per item up to 64
+constexpr uint32_t kTreeBase = 4096;         // uint4 index of the tree tables (64 KiB)
+// Modes without data AES: the GHASH table, T0 (for the J0 masks) and the tree tables.
+constexpr uint32_t kTreeBaseGhashOnly = 2112;   // 33 KiB
+constexpr uint32_t kLdsGhashOnly = (33 + 8 * kTreeTabs) * 1024 + 64;
+// Per-wave progress counters (16 words): at 112 KiB, or the last 64 B of the GHASH-only layout.
+constexpr uint32_t kProgBase = 112 * 1024 / 4;
+constexpr uint32_t kProgBaseGhashOnly = kLdsGhashOnly / 4 - 16;
 
 
 
@@ -289,6 +298,29 @@ constexpr uint32_t kLdsGhashOnly = 33 * 1024;  // modes without data AES: the GH
 __device__ __forceinline__ uint32_t tlk(const char *lds, uint32_t word, uint32_t lanec, uint32_t sel)
 {
     return *reinterpret_cast<const uint32_t *>(lds + __builtin_amdgcn_perm(word, lanec, sel));
+}
+
+__device__ __forceinline__ uint32_t rotl16(uint32_t x) { return __builtin_amdgcn_alignbit(x, x, 16); }
+
+// One output column of an AES round, T0[a.b0] ^ T1[b.b1] ^ T2[c.b2] ^ T3[d.b3] ^ k,
+// with kr = rotl16(k): only T0 and T1 are in LDS.
+__device__ __forceinline__ uint32_t tcol(const char *lds, uint32_t a, uint32_t b, uint32_t c, uint32_t d,
+                                         uint32_t kr, uint32_t lc0, uint32_t lc1)
+{
+    const uint32_t u = xor3(tlk(lds, c, lc0, FT_SEL(2)), tlk(lds, d, lc1, FT_SEL(3)), kr);
+    return xor3(tlk(lds, a, lc0, FT_SEL(0)), tlk(lds, b, lc1, FT_SEL(1)), rotl16(u));
+}
+
+// Final round column, S(a.b0) | S(b.b1) << 8 | S(c.b2) << 16 | S(d.b3) << 24, XOR k:
+// S(x) is byte 1 of T0[x] and byte 2 of T1[x].
+__device__ __forceinline__ uint32_t tlast(const char *lds, uint32_t a, uint32_t b, uint32_t c, uint32_t d,
+                                          uint32_t k, uint32_t lc0, uint32_t lc1)
+{
+    const uint32_t a0 = tlk(lds, a, lc0, FT_SEL(0));
+    const uint32_t a1 = tlk(lds, b, lc1, FT_SEL(1));
+    const uint32_t a2 = tlk(lds, c, lc0, FT_SEL(2));
+    const uint32_t a3 = tlk(lds, d, lc1, FT_SEL(3));
+    return xor3(__builtin_amdgcn_perm(a1, a0, 0x0C0C0601u), __builtin_amdgcn_perm(a3, a2, 0x06010C0Cu), k);
 }
 
 // Y . x^64 in little-endian-word form: bytes 0..7 move to bytes 8..15 and the
@@ -353,11 +385,11 @@ __device__ __forceinline__ u4 aad_block(const uint8_t *aad, uint32_t u, uint32_t
 // L . H for the two length blocks of a launch, L = [len A]_64 || [len C]_64 in
 // bits, with len C the full chain length (lanes 0..31) or the last chain's
 // (lanes 32..63). Each lane looks up one nibble position of its L in the 4-bit
-// table of H, and each half of the wave XOR-sums its 32 entries.
+// table of H (h1), and each half of the wave XOR-sums its 32 entries.
 struct LenTerms {
     u4 full, last;
 };
-__device__ inline LenTerms len_terms(const GcmLaunch &p, uint32_t lane)
+__device__ inline LenTerms len_terms(const GcmLaunch &p, const Tab4 *h1, uint32_t lane)
 {
     const uint64_t abits = (uint64_t)p.aad_bytes * 8;
     const uint64_t cbits = (lane < 32 ? p.chain_bytes : p.last_len) * 8;
@@ -365,7 +397,7 @@ __device__ inline LenTerms len_terms(const GcmLaunch &p, uint32_t lane)
     const uint64_t half = pos < 16 ? abits : cbits;         // bytes 0..7 hold len A, 8..15 len C (big-endian)
     const uint32_t byte = (uint32_t)(half >> (8 * (7 - ((pos >> 1) & 7)))) & 0xFFu;
     const uint32_t nib = (pos & 1) ? (byte & 0xFu) : (byte >> 4);
-    const uint4 e = *reinterpret_cast<const uint4 *>(p.ctx->h1_tab.e[pos][nib]);
+    const uint4 e = *reinterpret_cast<const uint4 *>(h1->e[pos][nib]);
     u4 r = {{e.x, e.y, e.z, e.w}};
 #pragma unroll
     for (int off = 16; off >= 1; off >>= 1)
@@ -408,34 +440,24 @@ __device__ inline void emit_tag(const GcmLaunch &p, uint64_t gchain, const u4 &t
 }
 
 // AES-256 of one block x (before the first AddRoundKey) with the streaming
-// kernel's LDS T-tables: every lane encrypts its own block.
-__device__ inline u4 aes_block_lds(const char *lds, const uint32_t *rk, const u4 &x, uint32_t lc0, uint32_t lc1,
-                                   uint32_t lc2, uint32_t lc3)
+// kernel's LDS T-tables: every lane encrypts its own block. rk holds the round
+// keys of rounds 1..13 rotated by 16 bits (rk[4..55]), the others as they are.
+__device__ inline u4 aes_block_lds(const char *lds, const uint32_t *rk, const u4 &x, uint32_t lc0, uint32_t lc1)
 {
     uint32_t s0 = x.w[0] ^ rk[0], s1 = x.w[1] ^ rk[1], s2 = x.w[2] ^ rk[2], s3 = x.w[3] ^ rk[3];
 #pragma unroll
     for (int r = 1; r < 14; ++r) {
-        const uint32_t n0 = xor3(tlk(lds, s0, lc0, FT_SEL(0)), tlk(lds, s1, lc1, FT_SEL(1)),
-                                 xor3(tlk(lds, s2, lc2, FT_SEL(2)), tlk(lds, s3, lc3, FT_SEL(3)), rk[4 * r + 0]));
-        const uint32_t n1 = xor3(tlk(lds, s1, lc0, FT_SEL(0)), tlk(lds, s2, lc1, FT_SEL(1)),
-                                 xor3(tlk(lds, s3, lc2, FT_SEL(2)), tlk(lds, s0, lc3, FT_SEL(3)), rk[4 * r + 1]));
-        const uint32_t n2 = xor3(tlk(lds, s2, lc0, FT_SEL(0)), tlk(lds, s3, lc1, FT_SEL(1)),
-                                 xor3(tlk(lds, s0, lc2, FT_SEL(2)), tlk(lds, s1, lc3, FT_SEL(3)), rk[4 * r + 2]));
-        const uint32_t n3 = xor3(tlk(lds, s3, lc0, FT_SEL(0)), tlk(lds, s0, lc1, FT_SEL(1)),
-                                 xor3(tlk(lds, s1, lc2, FT_SEL(2)), tlk(lds, s2, lc3, FT_SEL(3)), rk[4 * r + 3]));
+        const uint32_t n0 = tcol(lds, s0, s1, s2, s3, rk[4 * r + 0], lc0, lc1);
+        const uint32_t n1 = tcol(lds, s1, s2, s3, s0, rk[4 * r + 1], lc0, lc1);
+        const uint32_t n2 = tcol(lds, s2, s3, s0, s1, rk[4 * r + 2], lc0, lc1);
+        const uint32_t n3 = tcol(lds, s3, s0, s1, s2, rk[4 * r + 3], lc0, lc1);
         s0 = n0; s1 = n1; s2 = n2; s3 = n3;
     }
-    const uint32_t st[4] = {s0, s1, s2, s3};
     u4 o;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const uint32_t a0 = tlk(lds, st[j], lc0, FT_SEL(0));
-        const uint32_t a1 = tlk(lds, st[(j + 1) & 3], lc1, FT_SEL(1));
-        const uint32_t a2 = tlk(lds, st[(j + 2) & 3], lc2, FT_SEL(2));
-        const uint32_t a3 = tlk(lds, st[(j + 3) & 3], lc3, FT_SEL(3));
-        o.w[j] = xor3(__builtin_amdgcn_perm(a1, a0, 0x0C0C0601u), __builtin_amdgcn_perm(a3, a2, 0x04030C0Cu),
-                      rk[56 + j]);
-    }
+    o.w[0] = tlast(lds, s0, s1, s2, s3, rk[56], lc0, lc1);
+    o.w[1] = tlast(lds, s1, s2, s3, s0, rk[57], lc0, lc1);
+    o.w[2] = tlast(lds, s2, s3, s0, s1, rk[58], lc0, lc1);
+    o.w[3] = tlast(lds, s3, s0, s1, s2, rk[59], lc0, lc1);
     return o;
 }
 
@@ -491,6 +513,9 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
     const char *lds = reinterpret_cast<const char *>(lds4);
     const uint4 *g8 = lds4 + (kAes ? kG8Base : 0);
     uint32_t *t0l = reinterpret_cast<uint32_t *>(lds4 + 2048);   // GHASH-only modes: T0 after the table
+    constexpr uint32_t kTree = kAes ? kTreeBase : kTreeBaseGhashOnly;
+    const Tab4 *tree = reinterpret_cast<const Tab4 *>(lds4 + kTree);   // tree[t]: 4-bit table of H^(2^t)
+    constexpr uint32_t kProg = kAes ? kProgBase : kProgBaseGhashOnly;
     const int tid = threadIdx.x;
     const uint32_t lane = tid & 63;
     const uint32_t jl = lane & (L - 1);      // lane within the item
@@ -503,47 +528,59 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
             // (w + k W) / 256, all from one T0 row: lane k fetches that row up front
             // and each pass broadcasts it, so no pass waits on memory.
             uint32_t *t = reinterpret_cast<uint32_t *>(lds4);
-            constexpr uint32_t kPasses = (32768 + kThreads - 1) / kThreads;
+            constexpr uint32_t kPasses = (16384 + kThreads - 1) / kThreads;
             static_assert(kPasses <= 64, "one T0 row per lane and pass");
             const uint32_t w = (uint32_t)tid >> 6;
             const uint32_t mine = c->t0[(w + kWavesPerWg * lane) & 255];
 #pragma unroll 8
             for (uint32_t k = 0; k < kPasses; ++k) {
                 const uint32_t ib = (w << 6) + k * kThreads;   // wave-uniform
-                if (ib < 32768) {
+                if (ib < 16384) {
                     const uint32_t v = __builtin_amdgcn_readlane(mine, k);
-                    const uint32_t tab = ((ib >> 13) & 2) | ((lane >> 5) & 1);
-                    t[ib + lane] = tab == 0 ? v : rotl32(v, 8 * tab);
+                    t[ib + lane] = lane < 32 ? v : rotl32(v, 8);
                 }
             }
         } else {
             for (int i = tid; i < 256; i += kThreads)
                 t0l[i] = c->t0[i];
         }
-        if (kGhash) {   // all loads of the 32 KiB table first, then the stores
+        if (tid < 16)
+            reinterpret_cast<uint32_t *>(lds4)[kProg + tid] = 0u;
+        if (kGhash) {   // all loads of the 32 KiB GHASH table and the tree tables first, then the stores
             const uint4 *g = reinterpret_cast<const uint4 *>(c->g8[LL - 4]);
+            const uint4 *sq = reinterpret_cast<const uint4 *>(c->sq_tab);
+            constexpr int kTreeU4 = kTreeTabs * (int)(sizeof(Tab4) / 16);
             constexpr int kPer = (2048 + kThreads - 1) / kThreads;
-            uint4 gv[kPer];
+            constexpr int kPerT = (kTreeU4 + kThreads - 1) / kThreads;
+            uint4 gv[kPer], tv[kPerT];
 #pragma unroll
             for (int r = 0; r < kPer; ++r)
                 gv[r] = g[min(tid + r * kThreads, 2047)];
 #pragma unroll
+            for (int r = 0; r < kPerT; ++r)
+                tv[r] = sq[min(tid + r * kThreads, kTreeU4 - 1)];
+#pragma unroll
             for (int r = 0; r < kPer; ++r)
                 if (tid + r * kThreads < 2048)
                     lds4[(kAes ? kG8Base : 0) + tid + r * kThreads] = gv[r];
+#pragma unroll
+            for (int r = 0; r < kPerT; ++r)
+                if (tid + r * kThreads < kTreeU4)
+                    lds4[kTree + tid + r * kThreads] = tv[r];
         }
     }
     __syncthreads();
 
     const uint32_t lb = (lane & 31) << 2;
-    const uint32_t lc0 = lb, lc1 = lb | 0x80u, lc2 = lb | 0x10000u, lc3 = lb | 0x10080u;
+    const uint32_t lc0 = lb, lc1 = lb | 0x80u;
     // The 60 round-key words are uniform: they stay in scalar registers (the XORs
     // take them as scalar operands), which keeps the kernel within the 128 VGPRs
-    // that four waves per SIMD allow.
+    // that four waves per SIMD allow. Rounds 1..13 keep them rotated by 16 bits
+    // (the form tcol takes).
     uint32_t rk[60];
 #pragma unroll
     for (int i = 0; i < 60; ++i)
-        rk[i] = kAes ? __builtin_amdgcn_readfirstlane(c->rk[i]) : 0u;
+        rk[i] = kAes ? __builtin_amdgcn_readfirstlane(i >= 4 && i < 56 ? rotl16(c->rk[i]) : c->rk[i]) : 0u;
 
     const uint64_t nwaves = (uint64_t)gridDim.x * kWavesPerWg;
     // A launch with fewer wave-items than resident waves numbers its waves across
@@ -560,6 +597,17 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
     // of them. One lane-parallel AES pass serves L wave-items.
     u4 jmask = zero4();
     uint32_t it = 0;   // wave-items done by this wave
+    // The SIMD's instruction arbiter favours its oldest wave, so the waves of a SIMD
+    // would finish their equal shares one after another, the last ones with the SIMD
+    // to themselves. Wave w of the workgroup runs on SIMD w % 4; every wave publishes
+    // its iteration count in LDS and, each iteration, takes issue priority 3 while it
+    // is the slowest wave of its SIMD, 2 or 1 while it leads the slowest by one or two
+    // iterations, and 0 beyond that, so the four keep pace with each other.
+    volatile uint32_t *prog = reinterpret_cast<volatile uint32_t *>(lds4) + kProg;
+    const uint32_t wslot = (uint32_t)tid >> 6;
+    const uint32_t pidx = (wslot & 3) * 4 + (wslot >> 2);
+    uint32_t iters_done = 0;
+    __builtin_amdgcn_s_setprio(3);
     for (uint64_t wi = wave; wi < n_wave_items; wi += nwaves, ++it) {
         const uint32_t bi = it & (L - 1);
         if (kGhash && bi == 0) {
@@ -568,27 +616,38 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
             uint32_t biv[3];
             chain_iv(p, p.chain_base + bp.chain, biv);
             const u4 j0 = {{biv[0], biv[1], biv[2], bswap32(1u)}};   // J0 = IV_i || 0^31 || 1
-            u4 lenh;
-            if constexpr (RAG) {   // every chain has its own length: each lane multiplies its own
-                const uint64_t abits = (uint64_t)p.aad_bytes * 8, cbits = bp.len * 8;
-                const u4 lens = {{bswap32((uint32_t)(abits >> 32)), bswap32((uint32_t)abits),
-                                  bswap32((uint32_t)(cbits >> 32)), bswap32((uint32_t)cbits)}};
-                lenh = mul_tab4(lens, &c->h1_tab);
-            } else {
-                const LenTerms lt = len_terms(p, lane);
+            // Only lanes whose item exists and starts its chain (segment 0) need a mask;
+            // the others stay inactive, so the pass costs LDS lookups for those lanes only.
+            const bool need = bitem < p.n_items && bp.s == 0;
+            u4 lenh = zero4();
+            if constexpr (!RAG) {
+                const LenTerms lt = len_terms(p, &tree[0], lane);
                 lenh = bp.chain == p.n_chains - 1 ? lt.last : lt.full;
             }
-            u4 e;
-            if constexpr (kAes)
-                e = aes_block_lds(lds, rk, j0, lc0, lc1, lc2, lc3);
-            else
-                e = aes256_encrypt_tt(j0, c->rk, [&](uint32_t x) { return t0l[x]; });
-            jmask = xor4(e, lenh);
+            if (need) {
+                if constexpr (RAG) {   // every chain has its own length: each lane multiplies its own
+                    const uint64_t abits = (uint64_t)p.aad_bytes * 8, cbits = bp.len * 8;
+                    const u4 lens = {{bswap32((uint32_t)(abits >> 32)), bswap32((uint32_t)abits),
+                                      bswap32((uint32_t)(cbits >> 32)), bswap32((uint32_t)cbits)}};
+                    lenh = mul_tab4(lens, &tree[0]);
+                }
+                u4 e;
+                if constexpr (kAes)
+                    e = aes_block_lds(lds, rk, j0, lc0, lc1);
+                else
+                    e = aes256_encrypt_tt(j0, c->rk, [&](uint32_t x) { return t0l[x]; });
+                jmask = xor4(e, lenh);
+            }
         }
         const uint64_t item = wi * G + gs;
         const bool valid = item < p.n_items;
         const ItemPos ip = item_pos<RAG>(p, valid ? item : p.n_items - 1);
         const uint64_t gchain = p.chain_base + ip.chain;
+        // A whole-chain item checks its tag at the end: fetch the received tag now.
+        u4 got = zero4();
+        if constexpr (!ENC && !SPLIT && kGhash)
+            if (valid && jl == 0)
+                got = load16(p.tags_in + 16 * gchain);
         // Iterations of this wave-item: uniform for uniform chains; for ragged chains
         // the longest of the wave's segments (shorter ones are padded in front).
         uint32_t Ku = Ku_uniform;
@@ -605,11 +664,14 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
         // fixed for the whole chain, so 12 of round 1's 16 lookups are too.
         uint32_t p0 = 0, p1 = 0, p2 = 0, p3 = 0;
         if constexpr (kAes) {
+            // (rk[4..7] are rotated by 16 bits; T2 = rotl16(T0), T3 = rotl16(T1).)
             const uint32_t c0 = iv[0] ^ rk[0], c1 = iv[1] ^ rk[1], c2 = iv[2] ^ rk[2];
-            p0 = xor3(tlk(lds, c0, lc0, FT_SEL(0)), tlk(lds, c1, lc1, FT_SEL(1)), xor3(tlk(lds, c2, lc2, FT_SEL(2)), rk[4], 0u));
-            p1 = xor3(tlk(lds, c1, lc0, FT_SEL(0)), tlk(lds, c2, lc1, FT_SEL(1)), xor3(tlk(lds, c0, lc3, FT_SEL(3)), rk[5], 0u));
-            p2 = xor3(tlk(lds, c2, lc0, FT_SEL(0)), tlk(lds, c0, lc2, FT_SEL(2)), xor3(tlk(lds, c1, lc3, FT_SEL(3)), rk[6], 0u));
-            p3 = xor3(tlk(lds, c0, lc1, FT_SEL(1)), tlk(lds, c1, lc2, FT_SEL(2)), xor3(tlk(lds, c2, lc3, FT_SEL(3)), rk[7], 0u));
+            p0 = xor3(tlk(lds, c0, lc0, FT_SEL(0)), tlk(lds, c1, lc1, FT_SEL(1)),
+                      rotl16(tlk(lds, c2, lc0, FT_SEL(2)) ^ rk[4]));
+            p1 = xor3(tlk(lds, c1, lc0, FT_SEL(0)), tlk(lds, c2, lc1, FT_SEL(1)),
+                      rotl16(tlk(lds, c0, lc1, FT_SEL(3)) ^ rk[5]));
+            p2 = tlk(lds, c2, lc0, FT_SEL(0)) ^ rotl16(xor3(tlk(lds, c0, lc0, FT_SEL(2)), tlk(lds, c1, lc1, FT_SEL(3)), rk[6]));
+            p3 = tlk(lds, c0, lc1, FT_SEL(1)) ^ rotl16(xor3(tlk(lds, c1, lc0, FT_SEL(2)), tlk(lds, c2, lc1, FT_SEL(3)), rk[7]));
         }
         const uint8_t *src = kRead ? p.in + ip.off : nullptr;
         uint8_t *dst = kWrite ? p.out + ip.off : nullptr;
@@ -688,13 +750,13 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
         uint32_t q0 = 0, q1 = 0, q2 = 0, q3 = 0, gq = 0xFFFFFFFFu;
         auto group_setup = [&](uint32_t ctr) {
             const uint32_t s3i = bswap32(ctr) ^ rk[3];
-            const uint32_t s1 = p1 ^ tlk(lds, s3i, lc2, FT_SEL(2));
+            const uint32_t s1 = p1 ^ rotl16(tlk(lds, s3i, lc0, FT_SEL(2)));
             const uint32_t s2 = p2 ^ tlk(lds, s3i, lc1, FT_SEL(1));
             const uint32_t s3 = p3 ^ tlk(lds, s3i, lc0, FT_SEL(0));
-            q0 = xor3(tlk(lds, s1, lc1, FT_SEL(1)), tlk(lds, s2, lc2, FT_SEL(2)), xor3(tlk(lds, s3, lc3, FT_SEL(3)), rk[8], 0u));
-            q1 = xor3(tlk(lds, s1, lc0, FT_SEL(0)), tlk(lds, s2, lc1, FT_SEL(1)), xor3(tlk(lds, s3, lc2, FT_SEL(2)), rk[9], 0u));
-            q2 = xor3(tlk(lds, s2, lc0, FT_SEL(0)), tlk(lds, s3, lc1, FT_SEL(1)), xor3(tlk(lds, s1, lc3, FT_SEL(3)), rk[10], 0u));
-            q3 = xor3(tlk(lds, s3, lc0, FT_SEL(0)), tlk(lds, s1, lc2, FT_SEL(2)), xor3(tlk(lds, s2, lc3, FT_SEL(3)), rk[11], 0u));
+            q0 = tlk(lds, s1, lc1, FT_SEL(1)) ^ rotl16(xor3(tlk(lds, s2, lc0, FT_SEL(2)), tlk(lds, s3, lc1, FT_SEL(3)), rk[8]));
+            q1 = xor3(tlk(lds, s1, lc0, FT_SEL(0)), tlk(lds, s2, lc1, FT_SEL(1)), rotl16(tlk(lds, s3, lc0, FT_SEL(2)) ^ rk[9]));
+            q2 = xor3(tlk(lds, s2, lc0, FT_SEL(0)), tlk(lds, s3, lc1, FT_SEL(1)), rotl16(tlk(lds, s1, lc1, FT_SEL(3)) ^ rk[10]));
+            q3 = tlk(lds, s3, lc0, FT_SEL(0)) ^ rotl16(xor3(tlk(lds, s1, lc0, FT_SEL(2)), tlk(lds, s2, lc1, FT_SEL(3)), rk[11]));
             gq = ctr >> 8;
         };
         const uint32_t k3 = rk[3] >> 24;   // key byte that meets the counter's low byte
@@ -711,37 +773,24 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                         group_setup(ctr);
                 // Round 1, column 0 (T3 of the counter's low byte), then round 2 on the
                 // cached sums: each output column adds its one lookup of column 0.
-                const uint32_t c0 = p0 ^ tlk(lds, ctr ^ k3, lc3, FT_SEL(0));
+                const uint32_t c0 = p0 ^ rotl16(tlk(lds, ctr ^ k3, lc1, FT_SEL(0)));
                 uint32_t s0 = q0 ^ tlk(lds, c0, lc0, FT_SEL(0));
-                uint32_t s1 = q1 ^ tlk(lds, c0, lc3, FT_SEL(3));
-                uint32_t s2 = q2 ^ tlk(lds, c0, lc2, FT_SEL(2));
+                uint32_t s1 = q1 ^ rotl16(tlk(lds, c0, lc1, FT_SEL(3)));
+                uint32_t s2 = q2 ^ rotl16(tlk(lds, c0, lc0, FT_SEL(2)));
                 uint32_t s3 = q3 ^ tlk(lds, c0, lc1, FT_SEL(1));
 #pragma unroll
                 for (int r = 3; r < 14; ++r) {
-                    const uint32_t n0 = xor3(tlk(lds, s0, lc0, FT_SEL(0)), tlk(lds, s1, lc1, FT_SEL(1)),
-                                             xor3(tlk(lds, s2, lc2, FT_SEL(2)), tlk(lds, s3, lc3, FT_SEL(3)), rk[4 * r + 0]));
-                    const uint32_t n1 = xor3(tlk(lds, s1, lc0, FT_SEL(0)), tlk(lds, s2, lc1, FT_SEL(1)),
-                                             xor3(tlk(lds, s3, lc2, FT_SEL(2)), tlk(lds, s0, lc3, FT_SEL(3)), rk[4 * r + 1]));
-                    const uint32_t n2 = xor3(tlk(lds, s2, lc0, FT_SEL(0)), tlk(lds, s3, lc1, FT_SEL(1)),
-                                             xor3(tlk(lds, s0, lc2, FT_SEL(2)), tlk(lds, s1, lc3, FT_SEL(3)), rk[4 * r + 2]));
-                    const uint32_t n3 = xor3(tlk(lds, s3, lc0, FT_SEL(0)), tlk(lds, s0, lc1, FT_SEL(1)),
-                                             xor3(tlk(lds, s1, lc2, FT_SEL(2)), tlk(lds, s2, lc3, FT_SEL(3)), rk[4 * r + 3]));
+                    const uint32_t n0 = tcol(lds, s0, s1, s2, s3, rk[4 * r + 0], lc0, lc1);
+                    const uint32_t n1 = tcol(lds, s1, s2, s3, s0, rk[4 * r + 1], lc0, lc1);
+                    const uint32_t n2 = tcol(lds, s2, s3, s0, s1, rk[4 * r + 2], lc0, lc1);
+                    const uint32_t n3 = tcol(lds, s3, s0, s1, s2, rk[4 * r + 3], lc0, lc1);
                     s0 = n0; s1 = n1; s2 = n2; s3 = n3;
                 }
-                // Final round: S(x) is byte (1+r)&3 of T_r[x]; assemble four of them with v_perm.
-                {
-                    const uint32_t st[4] = {s0, s1, s2, s3};
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        const uint32_t a0 = tlk(lds, st[j], lc0, FT_SEL(0));
-                        const uint32_t a1 = tlk(lds, st[(j + 1) & 3], lc1, FT_SEL(1));
-                        const uint32_t a2 = tlk(lds, st[(j + 2) & 3], lc2, FT_SEL(2));
-                        const uint32_t a3 = tlk(lds, st[(j + 3) & 3], lc3, FT_SEL(3));
-                        const uint32_t lo = __builtin_amdgcn_perm(a1, a0, 0x0C0C0601u);
-                        const uint32_t hi = __builtin_amdgcn_perm(a3, a2, 0x04030C0Cu);
-                        o.w[j] = xor3(lo, hi, rk[56 + j] ^ d.w[j]);
-                    }
-                }
+                // Final round, XOR the data.
+                o.w[0] = tlast(lds, s0, s1, s2, s3, rk[56] ^ d.w[0], lc0, lc1);
+                o.w[1] = tlast(lds, s1, s2, s3, s0, rk[57] ^ d.w[1], lc0, lc1);
+                o.w[2] = tlast(lds, s2, s3, s0, s1, rk[58] ^ d.w[2], lc0, lc1);
+                o.w[3] = tlast(lds, s3, s0, s1, s2, rk[59] ^ d.w[3], lc0, lc1);
             } else if constexpr (MODE == kApplyKs) {
                 o = xor4(d, kv);
             } else {
@@ -773,17 +822,47 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
             }
         };
         for (uint32_t k = 0; k < Ku; ++k) {
+            {
+                const uint32_t mine = iters_done + k;
+                if (lane == 0)
+                    prog[pidx] = mine;
+                const uint4 g = reinterpret_cast<const uint4 *>(lds4)[(kProg + (pidx & ~3u)) / 4];
+                const uint32_t mn = __builtin_amdgcn_readfirstlane(min(min(g.x, g.y), min(g.z, g.w)));
+                const uint32_t lead = mine - (mn < mine ? mn : mine);
+                if (lead == 0u)
+                    __builtin_amdgcn_s_setprio(3);
+                else if (lead == 1u)
+                    __builtin_amdgcn_s_setprio(2);
+                else if (lead == 2u)
+                    __builtin_amdgcn_s_setprio(1);
+                else
+                    __builtin_amdgcn_s_setprio(0);
+            }
             const Slot q = slot_of(k);
             process(k, q, kRead ? load_block(src, q) : zero4(),
                     MODE == kApplyKs ? load_block(ksrc, q) : zero4());
         }
+        iters_done += Ku;
         if constexpr (kGhash) {
-            // Lane j's chain carries weight H^(L-j) in its segment; one more H for the tag.
-            acc = mul_tab4(acc, &c->lane_tab[64 - L + jl]);
-#pragma unroll
-            for (uint32_t off = L / 2; off >= 1; off >>= 1)
+            __builtin_amdgcn_s_setprio(3);   // the tail is a short latency-bound chain
+            // Lane j's stream carries the weight H^(L+1-j) in its segment (one H of it
+            // for the tag). sum_j acc_j H^(L-1-j) is a tree over the lanes: level t folds
+            // lane j + 2^t into lane j with the factor H^(2^t), every lane active at a
+            // level reading the same LDS table; then one multiply by H^2 in lane 0.
+#pragma unroll 1
+            for (uint32_t lv = 0; lv < (uint32_t)LL; ++lv) {
+                const uint32_t dl = 1u << lv;
+                u4 right;
                 for (int w = 0; w < 4; ++w)
-                    acc.w[w] ^= __shfl_xor(acc.w[w], off, 64);
+                    right.w[w] = __shfl_down(acc.w[w], dl, 64);
+                if ((jl & (2 * dl - 1)) == 0)
+                    acc = xor4(mul_tab4_b8(acc, &tree[lv]), right);
+            }
+            if (jl == 0)
+                acc = mul_tab4_b8(acc, &tree[1]);
+            if (SPLIT)   // the segment weights below take the sum in every lane of the group
+                for (int w = 0; w < 4; ++w)
+                    acc.w[w] = __shfl(acc.w[w], (int)(lane - jl), 64);
             if (SPLIT) {
                 // A chain cut into S segments: segment s carries the weight
                 // H^((S-1-s) . 2^seg_log2) inside its chain, one multiply by a
@@ -820,10 +899,12 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                 for (int w = 0; w < 4; ++w)
                     e.w[w] = __shfl(jmask.w[w], (int)(bi * G + gs), 64);
                 if (valid && jl == 0)
-                    emit_tag<ENC>(p, gchain, xor4(acc, e), ENC ? zero4() : load16(p.tags_in + 16 * gchain));
+                    emit_tag<ENC>(p, gchain, xor4(acc, e), got);
             }
         }
     }
+    if (lane == 0)   // a finished wave no longer holds the others of its SIMD back
+        prog[pidx] = 0xFFFFFFFFu;
 }
 
 // Chains cut into segments: T = mask xor the XOR of the chain's weighted

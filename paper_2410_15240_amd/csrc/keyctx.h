@@ -19,7 +19,7 @@ namespace fastrack {
 
 constexpr int kTab4Pos = 32;    // nibble positions of a 128-bit operand
 constexpr int kTab4Ent = 16;    // values of a nibble
-constexpr int kMaxPow = 64;     // lane-combine powers H^1 .. H^64 (one wave of 64 lanes)
+constexpr int kMaxPow = 64;     // powers H^1 .. H^64 (Horner multipliers up to one wave of 64 lanes)
 constexpr int kSquares = 32;    // H^(2^t), t = 0..31 (chains are < 2^32 blocks)
 
 struct Tab4 {                   // 4-bit positional multiplication table of a fixed Y:
@@ -34,8 +34,7 @@ struct KeyCtx {
     uint32_t hp[kMaxPow + 2][4];      // hp[e] = H^e, e = 0..65 (hp[0] = 1)
     uint32_t hsq[kSquares][4];        // hsq[t] = H^(2^t)
     Tab4 h1_tab;                // table of H
-    Tab4 lane_tab[kMaxPow];     // lane_tab[l]: table of H^(65-l), the lane-combine weight of lane l
-    Tab4 sq_tab[kSquares];      // sq_tab[t]: table of H^(2^t)
+    Tab4 sq_tab[kSquares];      // sq_tab[t]: table of H^(2^t) (t = 0..5 also combine the lanes of an item)
     // 8-bit positional tables of the Horner multipliers H^16, H^32 and H^64 (lanes per
     // chain 16, 32, 64): g8[i][k][v] = (byte v at byte k) . H^(16 << i)
     uint32_t g8[3][16][256][4];
