@@ -323,6 +323,22 @@ __device__ __forceinline__ uint32_t tlast(const char *lds, uint32_t a, uint32_t 
     return xor3(__builtin_amdgcn_perm(a1, a0, 0x0C0C0601u), __builtin_amdgcn_perm(a3, a2, 0x06010C0Cu), k);
 }
 
+// Lane i receives x from lane i + D (for lanes where that stays inside the
+// aligned group the tree folds): DPP row shifts for D < 16, the gfx950 half-row
+// and half-wave swaps for 16 and 32. VALU moves, no LDS round trip.
+template <uint32_t D>
+__device__ __forceinline__ uint32_t lane_down(uint32_t x)
+{
+    if constexpr (D < 16) {
+        return __builtin_amdgcn_update_dpp(0u, x, 0x100 + D, 0xF, 0xF, false);   // row_shl:D
+    } else if constexpr (D == 16) {
+        return __builtin_amdgcn_permlane16_swap(x, x, false, false)[1];
+    } else {
+        static_assert(D == 32, "shift of 1..8, 16 or 32 lanes");
+        return __builtin_amdgcn_permlane32_swap(x, x, false, false)[1];
+    }
+}
+
 // Y . x^64 in little-endian-word form: bytes 0..7 move to bytes 8..15 and the
 // bytes that pass degree 127, F, come back as F . (1 + x + x^2 + x^7).
 __device__ __forceinline__ u4 mul_x64(const u4 &y)
@@ -851,11 +867,19 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
             // level reading the same LDS table; then one multiply by H^2 in lane 0.
 #pragma unroll 1
             for (uint32_t lv = 0; lv < (uint32_t)LL; ++lv) {
-                const uint32_t dl = 1u << lv;
                 u4 right;
-                for (int w = 0; w < 4; ++w)
-                    right.w[w] = __shfl_down(acc.w[w], dl, 64);
-                if ((jl & (2 * dl - 1)) == 0)
+                for (int w = 0; w < 4; ++w) {
+                    const uint32_t x = acc.w[w];
+                    switch (lv) {   // uniform: the VALU cross-lane move for this distance
+                    case 0: right.w[w] = lane_down<1>(x); break;
+                    case 1: right.w[w] = lane_down<2>(x); break;
+                    case 2: right.w[w] = lane_down<4>(x); break;
+                    case 3: right.w[w] = lane_down<8>(x); break;
+                    case 4: right.w[w] = lane_down<16>(x); break;
+                    default: right.w[w] = lane_down<32>(x); break;
+                    }
+                }
+                if ((jl & ((2u << lv) - 1)) == 0)
                     acc = xor4(mul_tab4_b8(acc, &tree[lv]), right);
             }
             if (jl == 0)
