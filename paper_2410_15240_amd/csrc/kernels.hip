@@ -94,6 +94,7 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
         for (int i = 0; i < 60; ++i) {
             s_rk[i] = rk[i];
             ctx->rk[i] = rk[i];
+            ctx->rk16[i] = i >= 4 && i < 56 ? rotl32(rk[i], 16) : rk[i];
         }
     }
     __syncthreads();
@@ -591,12 +592,14 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
     const uint32_t lc0 = lb, lc1 = lb | 0x80u;
     // The 60 round-key words are uniform: they stay in scalar registers (the XORs
     // take them as scalar operands), which keeps the kernel within the 128 VGPRs
-    // that four waves per SIMD allow. Rounds 1..13 keep them rotated by 16 bits
-    // (the form tcol takes).
+    // that four waves per SIMD allow. Rounds 1..13 use them rotated by 16 bits (the
+    // form tcol takes), precomputed per key. (Loaded after the table fill: scalar
+    // loads and LDS accesses share one wait counter, so loading them earlier would
+    // hold up the fill.)
     uint32_t rk[60];
 #pragma unroll
     for (int i = 0; i < 60; ++i)
-        rk[i] = kAes ? __builtin_amdgcn_readfirstlane(i >= 4 && i < 56 ? rotl16(c->rk[i]) : c->rk[i]) : 0u;
+        rk[i] = kAes ? c->rk16[i] : 0u;
 
     const uint64_t nwaves = (uint64_t)gridDim.x * kWavesPerWg;
     // A launch with fewer wave-items than resident waves numbers its waves across

@@ -28,6 +28,7 @@ struct Tab4 {                   // 4-bit positional multiplication table of a fi
 
 struct KeyCtx {
     uint32_t rk[60];            // AES-256 round keys (FIPS-197 key expansion)
+    uint32_t rk16[60];          // the same with the words of rounds 1..13 (rk[4..55]) rotated by 16 bits
     uint32_t t0[256];           // T0[x] = {02}S(x) | S(x)<<8 | S(x)<<16 | {03}S(x)<<24
     uint8_t sbox[256];
     uint32_t h[4];              // H = AES_K(0^128)
