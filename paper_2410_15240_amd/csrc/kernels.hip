@@ -19,7 +19,8 @@
 //     acc_l <- acc_l . H^64  xor  X_(64k+l)
 // and at the end of its segment the lanes are combined with one extra factor H:
 //     G'_s = sum_l acc_l . H^(65-l)
-// (lane l's last block has 63-l blocks after it). A segment shorter than a
+// (lane l's last block has 63-l blocks after it), computed as a tree over the
+// lanes whose level t multiplies by H^(2^t). A segment shorter than a
 // multiple of 64 is padded with zero blocks at its START, which leaves GHASH
 // unchanged. Segments are aligned to the end of the chain, so segment s of S
 // carries the weight H^((S-1-s) . 2^seg_log2) within the chain.
@@ -30,8 +31,8 @@
 // The AAD blocks ride in the same Horner streams (they are the blocks that
 // precede the first ciphertext block), so a chain's streams sum to
 // GHASH(A || C) . H = G_C . H xor GHASH(A) . H^(q+1). A chain cut into segments
-// applies each segment's weight inside the chain and gathers the segments by
-// atomic XOR; whoever holds the complete sum adds L . H and AES_K(J0).
+// applies each segment's weight inside the chain and stores it; a second kernel
+// XORs a chain's segments and adds L . H and AES_K(J0).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
