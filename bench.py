@@ -226,6 +226,20 @@ def extras(F, W, torch, np, dev, stream, args):
     log("encrypt+tag %.1f GB/s" % res["encrypt_tag"]["gbps"])
     del pt4, out4, tags4
 
+    # encrypt + tag against chain size: the decrypt sweep's image batch and chain sizes
+    w2s = W.config2()
+    p2s = torch.from_numpy(w2s.payload).to(dev)
+    o2s = torch.empty_like(p2s)
+    esweep = {}
+    for chain in w2s.chain_sizes:
+        a2s = torch.from_numpy(w2s.aad(chain)).to(dev)
+        t2s = torch.empty((F.num_chains(p2s.numel(), chain), 16), dtype=torch.uint8, device=dev)
+        ms = time_calls(torch, stream, lambda: F.encrypt_tag(w2s.key, w2s.base_iv, chain, p2s, a2s, out=o2s, tags=t2s), 20)
+        esweep["%dKiB" % (chain // KiB)] = {"gbps": round(p2s.numel() / ms / 1e6, 1), "us": round(ms * 1e3, 1)}
+    res["encrypt_sweep"] = {"workload": "image-batch-64MiB, 32-byte AAD per chain", "sweep": esweep}
+    log("encrypt sweep:", esweep)
+    del p2s, o2s
+
     # the paper's sequential GHASH vs multi-chain, 1 MiB buffer
     w1 = W.config1()
     p1 = torch.from_numpy(w1.payload).to(dev)
