@@ -162,6 +162,25 @@ int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, uint64_t c
                           void *compute_stream);
 
 /*
+ * The operations fastrack_pipeline_h2d(_mode) enqueues, in order, for these sizes
+ * (the paper's decryption pipeline, section 5.3): a pure host function with no
+ * device access, for inspecting and checking the schedule.
+ *   h_ops    host array of max_ops records of 6 int64 each, written in order:
+ *            kind, stream, event, chunk, slot, aux. May be NULL (count only).
+ *            kind: 0 upload tags + AAD, 1 record `event`, 2 wait for the last
+ *            record of `event`, 3 copy chunk `chunk` into buffer `slot`, 4 keystream
+ *            of chunk `chunk` into ring slot `slot`, 5 decrypt + verify chunk
+ *            `chunk` read from buffer `slot`, 6 XOR keystream slot `aux` into chunk
+ *            `chunk` read from buffer `slot` + tag check, 7 decrypt only, 8 tag
+ *            check only. Buffer slot -1 is the chunk's own place in d_pt, 0..depth-1
+ *            a staging slot. stream: 0 copy, 1 compute, 2 verify. event: -1 none.
+ * Returns the number of operations (>= 0; 0 for len = 0) or FASTRACK_EINVAL for
+ * the argument errors the pipeline itself rejects (chunk_bytes, depth, mode).
+ */
+int64_t fastrack_pipeline_plan(uint64_t len, uint64_t chain_bytes, uint64_t chunk_bytes, int depth, uint32_t mode,
+                               int64_t *h_ops, uint64_t max_ops);
+
+/*
  * fastrack_pipeline_h2d with a mode:
  *   FASTRACK_PIPE_FUSED  as fastrack_pipeline_h2d (verify_stream unused)
  *   FASTRACK_PIPE_EAGER  chunks land in a ring of depth >= 2 staging slots; each

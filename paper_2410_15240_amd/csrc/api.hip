@@ -563,6 +563,91 @@ FT_EXPORT uint64_t fastrack_pipeline_stage_bytes(uint64_t len, uint64_t chain_by
 
 namespace {
 
+// The H2D pipeline as a list of stream operations, built on the host before any
+// of them is enqueued (and exported for inspection). Streams: 0 copy, 1 compute,
+// 2 verify (the eager mode only; the other modes put its work on stream 1).
+enum PlanKind : uint32_t {
+    kOpMeta = 0,       // upload the tags and the AAD
+    kOpRecord = 1,     // record `event` on the stream
+    kOpWait = 2,       // the stream waits for the last record of `event`
+    kOpCopy = 3,       // copy chunk `chunk` from the host into buffer `slot` (-1: its place in d_pt)
+    kOpKeystream = 4,  // keystream of chunk `chunk` into ring slot `slot`
+    kOpFused = 5,      // decrypt + verify chunk `chunk` from buffer `slot` into d_pt
+    kOpApply = 6,      // XOR keystream slot `aux` into chunk `chunk` (read from `slot`) + tag check
+    kOpCtr = 7,        // decrypt chunk `chunk` from buffer `slot` into d_pt (no tag check)
+    kOpVerify = 8,     // tag check of chunk `chunk` read from buffer `slot`
+};
+struct PlanOp {
+    uint32_t kind;
+    uint32_t stream;
+    int32_t event;
+    uint64_t chunk;
+    int32_t slot;
+    int32_t aux;
+};
+// Events: meta (0); copied[i] (1..P), freed[i] (1+P..2P), decrypted[i] (1+2P..3P), reused modulo
+// P = 4: copied[k % P] is waited on right after it is recorded, decrypted[k % P] at once by the
+// verify stream, freed[k % P] at most two chunks later (a wait takes the event's state at the
+// time it is enqueued).
+constexpr int kPlanP = 4;
+constexpr int kPlanEvents = 3 * kPlanP + 1;
+
+std::vector<PlanOp> h2d_plan(uint64_t len, uint64_t chunk_bytes, int depth, uint32_t mode)
+{
+    std::vector<PlanOp> ops;
+    const uint32_t VS = mode == FASTRACK_PIPE_EAGER ? 2u : 1u;
+    auto op = [&](uint32_t kind, uint32_t stream, int32_t event, uint64_t chunk, int32_t slot, int32_t aux) {
+        ops.push_back(PlanOp{kind, stream, event, chunk, slot, aux});
+    };
+    const int32_t meta = 0, copied = 1, freed = 1 + kPlanP, decrypted = 1 + 2 * kPlanP;
+    op(kOpMeta, 0, -1, 0, -1, -1);
+    op(kOpRecord, 0, meta, 0, -1, -1);
+    op(kOpWait, 1, meta, 0, -1, -1);
+    if (VS != 1)
+        op(kOpWait, VS, meta, 0, -1, -1);
+    const uint64_t nchunks = (len + chunk_bytes - 1) / chunk_bytes;
+    // OTP: the keystream of chunk 0 before anything arrives; that of chunk k+1 while
+    // chunk k+1 is on the bus, in ring slot (k+1) % depth. A slot is rewritten only
+    // after the XOR that read it, earlier on the same stream.
+    if (mode == FASTRACK_PIPE_OTP)
+        op(kOpKeystream, 1, -1, 0, 0, -1);
+    // depth 0 (and OTP): each chunk is copied straight to its place in d_pt and
+    // decrypted there, so no buffer is reused and the copy stream never waits. A ring
+    // of `depth` slots must not overwrite slot k % depth before chunk k - depth has
+    // been read; the copy stream waits for the release two chunks back, which covers
+    // the next depth - 1 copies and, with decrypts faster than copies, has happened by
+    // then (a wait on the copy stream costs the copy engine time).
+    const bool ring = mode != FASTRACK_PIPE_OTP && depth > 0;
+    int64_t covered = -1;   // copies up to this chunk index have their slot's wait enqueued
+    for (uint64_t k = 0; k < nchunks; ++k) {
+        const int32_t buf = ring ? (int32_t)(k % (uint64_t)depth) : -1;
+        const int32_t e = (int32_t)(k % kPlanP);
+        if (ring && k >= (uint64_t)depth && (int64_t)k > covered) {
+            op(kOpWait, 0, freed + (int32_t)((k - 2) % kPlanP), 0, -1, -1);
+            covered = (int64_t)k + depth - 2;
+        }
+        op(kOpCopy, 0, -1, k, buf, -1);
+        op(kOpRecord, 0, copied + e, 0, -1, -1);
+        if (mode == FASTRACK_PIPE_OTP && k + 1 < nchunks)
+            op(kOpKeystream, 1, -1, k + 1, (int32_t)((k + 1) % (uint64_t)depth), -1);
+        op(kOpWait, 1, copied + e, 0, -1, -1);
+        if (mode == FASTRACK_PIPE_FUSED) {
+            op(kOpFused, 1, -1, k, buf, -1);
+        } else if (mode == FASTRACK_PIPE_OTP) {
+            op(kOpApply, 1, -1, k, buf, (int32_t)(k % (uint64_t)depth));
+        } else {   // eager: plaintext on the compute stream, the tag check beside it
+            op(kOpCtr, 1, -1, k, buf, -1);
+            op(kOpRecord, 1, decrypted + e, 0, -1, -1);
+            op(kOpWait, VS, copied + e, 0, -1, -1);
+            op(kOpVerify, VS, -1, k, buf, -1);
+            op(kOpWait, VS, decrypted + e, 0, -1, -1);   // the slot is free once both have read it
+        }
+        if (ring)
+            op(kOpRecord, VS, freed + e, 0, -1, -1);
+    }
+    return ops;
+}
+
 int pipeline_impl(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes, const uint8_t *h_ct, uint64_t len,
                   const uint8_t *h_tags, const uint8_t *h_aad, uint32_t aad_bytes, uint64_t chunk_bytes, int depth,
                   uint32_t mode, uint8_t *d_stage, uint64_t stage_bytes, uint8_t *d_pt, uint8_t *d_ok,
@@ -614,17 +699,17 @@ int pipeline_impl(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_byt
     uint8_t *d_tags = d_stage + (uint64_t)depth * slot_bytes;
     uint8_t *d_aad = d_tags + round256(16 * n);
     const uint8_t *aad = aad_bytes ? d_aad : nullptr;
+    const uint64_t cpc = chunk_bytes / chain_bytes;
+    auto chunk_len = [&](uint64_t k) { return len - k * chunk_bytes < chunk_bytes ? len - k * chunk_bytes : chunk_bytes; };
+    auto slot = [&](int32_t i) { return d_stage + (uint64_t)i * slot_bytes; };
+    auto buf_of = [&](const PlanOp &o) { return o.slot < 0 ? d_pt + o.chunk * chunk_bytes : slot(o.slot); };
 
-    // Event pools: copied[k % P] is waited on right after it is recorded, decrypted[k % P]
-    // at once by the verify stream, freed[k % P] at most two chunks later; P = 4 suffices
-    // (a wait takes the event's state at the time it is enqueued).
-    constexpr int P = 4;
     std::vector<hipEvent_t> ev;
     auto cleanup = [&]() {
         for (auto e : ev)
             (void)hipEventDestroy(e);
     };
-    for (int i = 0; i < 3 * P + 1; ++i) {
+    for (int i = 0; i < kPlanEvents; ++i) {
         hipEvent_t e;
         he = hipEventCreateWithFlags(&e, hipEventDisableTiming);
         if (he != hipSuccess) {
@@ -633,111 +718,53 @@ int pipeline_impl(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_byt
         }
         ev.push_back(e);
     }
-    hipEvent_t meta = ev[0];
-    hipEvent_t *copied = &ev[1], *freed = &ev[1 + P], *decrypted = &ev[1 + 2 * P];
-
-    he = hipMemcpyAsync(d_tags, h_tags, 16 * n, hipMemcpyHostToDevice, cs);
-    if (he == hipSuccess && aad_bytes)
-        he = hipMemcpyAsync(d_aad, h_aad, (size_t)aad_bytes * n, hipMemcpyHostToDevice, cs);
-    if (he == hipSuccess)
-        he = hipEventRecord(meta, cs);
-    if (he == hipSuccess)
-        he = hipStreamWaitEvent(ks, meta, 0);
-    if (he == hipSuccess && vs != ks)
-        he = hipStreamWaitEvent(vs, meta, 0);
-    if (he != hipSuccess) {
-        cleanup();
-        return hip_fail(he, "pipeline tag/AAD upload");
-    }
-    const uint64_t nchunks = (len + chunk_bytes - 1) / chunk_bytes;
-    const uint64_t cpc = chunk_bytes / chain_bytes;
-    auto chunk_len = [&](uint64_t k) { return len - k * chunk_bytes < chunk_bytes ? len - k * chunk_bytes : chunk_bytes; };
-    auto slot = [&](uint64_t k) { return d_stage + (k % (uint64_t)depth) * slot_bytes; };
-    if (mode == FASTRACK_PIPE_OTP) {
-        // The keystream of chunk 0 before anything arrives; that of chunk k+1 while
-        // chunk k+1 is on the bus, in ring slot (k+1) % depth. A slot is rewritten only
-        // after the XOR that read it, earlier on the same stream.
-        rc = run_gcm(false, kKeystream, ctx, base_iv, chain_bytes, 0, nullptr, nullptr, chunk_len(0), slot(0), nullptr,
-                     0, nullptr, nullptr, nullptr, 0, dev, ncu, ks);
-        if (rc) {
-            cleanup();
-            return rc;
+    const hipStream_t streams[3] = {cs, ks, vs};
+    for (const PlanOp &o : h2d_plan(len, chunk_bytes, depth, mode)) {
+        const hipStream_t st = streams[o.stream];
+        const uint64_t k = o.chunk;
+        switch (o.kind) {
+        case kOpMeta:
+            he = hipMemcpyAsync(d_tags, h_tags, 16 * n, hipMemcpyHostToDevice, st);
+            if (he == hipSuccess && aad_bytes)
+                he = hipMemcpyAsync(d_aad, h_aad, (size_t)aad_bytes * n, hipMemcpyHostToDevice, st);
+            break;
+        case kOpRecord:
+            he = hipEventRecord(ev[o.event], st);
+            break;
+        case kOpWait:
+            he = hipStreamWaitEvent(st, ev[o.event], 0);
+            break;
+        case kOpCopy:
+            he = hipMemcpyAsync(buf_of(o), h_ct + k * chunk_bytes, chunk_len(k), hipMemcpyHostToDevice, st);
+            break;
+        case kOpKeystream:
+            rc = run_gcm(false, kKeystream, ctx, base_iv, chain_bytes, k * cpc, nullptr, nullptr, chunk_len(k),
+                         buf_of(o), nullptr, 0, nullptr, nullptr, nullptr, 0, dev, ncu, st);
+            break;
+        case kOpFused:
+            rc = run_gcm(false, kFused, ctx, base_iv, chain_bytes, k * cpc, buf_of(o), nullptr, chunk_len(k),
+                         d_pt + k * chunk_bytes, aad, aad_bytes, d_tags, nullptr, d_ok, 0, dev, ncu, st);
+            break;
+        case kOpApply:
+            rc = run_gcm(false, kApplyKs, ctx, base_iv, chain_bytes, k * cpc, buf_of(o), slot(o.aux), chunk_len(k),
+                         d_pt + k * chunk_bytes, aad, aad_bytes, d_tags, nullptr, d_ok, 0, dev, ncu, st);
+            break;
+        case kOpCtr:
+            rc = run_gcm(false, kCtr, ctx, base_iv, chain_bytes, k * cpc, buf_of(o), nullptr, chunk_len(k),
+                         d_pt + k * chunk_bytes, nullptr, 0, nullptr, nullptr, nullptr, 0, dev, ncu, st);
+            break;
+        case kOpVerify:
+            rc = run_gcm(false, kVerify, ctx, base_iv, chain_bytes, k * cpc, buf_of(o), nullptr, chunk_len(k), nullptr,
+                         aad, aad_bytes, d_tags, nullptr, d_ok, 0, dev, ncu, st);
+            break;
         }
-    }
-    // depth 0: each chunk is copied straight to its place in d_pt and decrypted
-    // there, so no buffer is reused and the copy stream never waits. A ring of
-    // `depth` slots must not overwrite slot k % depth before chunk k - depth has
-    // been read; the copy stream waits for the release two chunks back, which
-    // covers the next depth - 1 copies and, with decrypts faster than copies,
-    // has happened by then (a wait on copy_stream costs the copy engine time).
-    const bool ring = mode != FASTRACK_PIPE_OTP && depth > 0;
-    int64_t covered = -1;   // copies up to this chunk index have their slot's wait enqueued
-    for (uint64_t k = 0; k < nchunks; ++k) {
-        const uint64_t off = k * chunk_bytes;
-        const uint64_t bytes = chunk_len(k);
-        uint8_t *buf = ring ? slot(k) : d_pt + off;
-        if (ring && k >= (uint64_t)depth && (int64_t)k > covered) {
-            he = hipStreamWaitEvent(cs, freed[(k - 2) % P], 0);
-            covered = (int64_t)k + depth - 2;
-        }
-        if (he == hipSuccess)
-            he = hipMemcpyAsync(buf, h_ct + off, bytes, hipMemcpyHostToDevice, cs);
-        if (he == hipSuccess)
-            he = hipEventRecord(copied[k % P], cs);
         if (he != hipSuccess) {
             cleanup();
-            return hip_fail(he, "pipeline copy");
-        }
-        if (mode == FASTRACK_PIPE_OTP && k + 1 < nchunks) {
-            rc = run_gcm(false, kKeystream, ctx, base_iv, chain_bytes, (k + 1) * cpc, nullptr, nullptr, chunk_len(k + 1),
-                         slot(k + 1), nullptr, 0, nullptr, nullptr, nullptr, 0, dev, ncu, ks);
-            if (rc) {
-                cleanup();
-                return rc;
-            }
-        }
-        he = hipStreamWaitEvent(ks, copied[k % P], 0);
-        if (he != hipSuccess) {
-            cleanup();
-            return hip_fail(he, "hipStreamWaitEvent");
-        }
-        if (mode == FASTRACK_PIPE_FUSED) {
-            rc = run_gcm(false, kFused, ctx, base_iv, chain_bytes, k * cpc, buf, nullptr, bytes, d_pt + off, aad, aad_bytes,
-                         d_tags, nullptr, d_ok, 0, dev, ncu, ks);
-        } else if (mode == FASTRACK_PIPE_OTP) {
-            rc = run_gcm(false, kApplyKs, ctx, base_iv, chain_bytes, k * cpc, buf, slot(k), bytes, d_pt + off, aad,
-                         aad_bytes, d_tags, nullptr, d_ok, 0, dev, ncu, ks);
-        } else {   // eager: plaintext on the compute stream, the tag check beside it
-            rc = run_gcm(false, kCtr, ctx, base_iv, chain_bytes, k * cpc, buf, nullptr, bytes, d_pt + off, nullptr, 0,
-                         nullptr, nullptr, nullptr, 0, dev, ncu, ks);
-            if (!rc) {
-                he = hipEventRecord(decrypted[k % P], ks);
-                if (he == hipSuccess)
-                    he = hipStreamWaitEvent(vs, copied[k % P], 0);
-                if (he != hipSuccess) {
-                    cleanup();
-                    return hip_fail(he, "eager pipeline events");
-                }
-                rc = run_gcm(false, kVerify, ctx, base_iv, chain_bytes, k * cpc, buf, nullptr, bytes, nullptr, aad,
-                             aad_bytes, d_tags, nullptr, d_ok, 0, dev, ncu, vs);
-                if (!rc)
-                    he = hipStreamWaitEvent(vs, decrypted[k % P], 0);   // the slot is free once both have read it
-                if (!rc && he != hipSuccess) {
-                    cleanup();
-                    return hip_fail(he, "hipStreamWaitEvent");
-                }
-            }
+            return hip_fail(he, "pipeline");
         }
         if (rc) {
             cleanup();
             return rc;
-        }
-        if (ring) {
-            he = hipEventRecord(freed[k % P], vs);
-            if (he != hipSuccess) {
-                cleanup();
-                return hip_fail(he, "hipEventRecord");
-            }
         }
     }
     cleanup();
@@ -745,6 +772,36 @@ int pipeline_impl(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_byt
 }
 
 }  // namespace
+
+FT_EXPORT int64_t fastrack_pipeline_plan(uint64_t len, uint64_t chain_bytes, uint64_t chunk_bytes, int depth,
+                                         uint32_t mode, int64_t *h_ops, uint64_t max_ops)
+{
+    g_err.clear();
+    if (chain_bytes == 0 || chain_bytes % 16 != 0)
+        return fail(FASTRACK_EINVAL, "chain_bytes must be a nonzero multiple of 16");
+    if (chunk_bytes == 0 || chunk_bytes % chain_bytes != 0)
+        return fail(FASTRACK_EINVAL, "chunk_bytes must be a nonzero multiple of chain_bytes");
+    if (mode > FASTRACK_PIPE_OTP)
+        return fail(FASTRACK_EINVAL, "unknown pipeline mode %u", mode);
+    if (depth < 0 || depth == 1 || depth > kMaxPipelineDepth)
+        return fail(FASTRACK_EINVAL, "depth must be 0 (in place) or 2..%d (staging ring)", kMaxPipelineDepth);
+    if (mode != FASTRACK_PIPE_FUSED && depth == 0)
+        return fail(FASTRACK_EINVAL, "the eager and keystream pipelines need depth >= 2 staging slots");
+    if (len == 0)
+        return 0;
+    const std::vector<PlanOp> ops = h2d_plan(len, chunk_bytes, depth, mode);
+    for (uint64_t i = 0; h_ops && i < ops.size() && i < max_ops; ++i) {
+        const PlanOp &o = ops[i];
+        int64_t *w = h_ops + 6 * i;
+        w[0] = o.kind;
+        w[1] = o.stream;
+        w[2] = o.event;
+        w[3] = (int64_t)o.chunk;
+        w[4] = o.slot;
+        w[5] = o.aux;
+    }
+    return (int64_t)ops.size();
+}
 
 FT_EXPORT int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
                                     const uint8_t *h_ct, uint64_t len, const uint8_t *h_tags, const uint8_t *h_aad,
