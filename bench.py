@@ -13,6 +13,7 @@ pipelined 4 GiB host-to-device decrypt against a plain pinned copy, and the
 CPU oracle on the host cores. One JSON line is printed.
 """
 import argparse
+import ctypes
 import json
 import os
 import sys
@@ -351,6 +352,17 @@ def extras(F, W, torch, np, dev, stream, args):
     return res
 
 
+def hip_runtime_path():
+    """The HIP runtime this process already uses (the one torch loaded), so that ctypes
+    calls go to the same runtime instance as torch's streams."""
+    with open("/proc/self/maps") as f:
+        for line in f:
+            path = line.split()[-1]
+            if os.path.basename(path).startswith("libamdhip64.so"):
+                return path
+    raise RuntimeError("the HIP runtime is not loaded")
+
+
 def pipeline(F, W, torch, np, dev):
     length, chain, chunk = 4 * GiB, MiB, 8 * MiB
     rng = W.rng_for(5)
@@ -372,19 +384,28 @@ def pipeline(F, W, torch, np, dev):
     out = torch.empty(length, dtype=torch.uint8, device=dev)
     ok = torch.empty(n, dtype=torch.uint8, device=dev)
     cs, ks, vs = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
+    def median_s(fn, streams, reps=3):
+        # one untimed pass, then the median of `reps` timed passes (host clock, all
+        # streams the pass uses drained)
+        fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            fn()
+            for st in streams:
+                st.synchronize()
+            ts.append(time.perf_counter() - t0)
+        return sorted(ts)[len(ts) // 2]
+
     for name, mode, depth in (("depth0", 0, 0), ("depth2", 0, 2), ("depth3", 0, 3), ("eager_depth2", 1, 2),
-                              ("otp_depth2", 2, 2)):
+                              ("otp_depth2", 2, 2), ("direct", 3, 0)):
         run = lambda: F.pipeline_h2d(key, iv, chain, h_ct, h_tags, None, chunk, depth, stage, out, ok, cs, ks,
                                      mode=mode, verify_stream=vs)
-        run()
-        torch.cuda.synchronize()
         ok.zero_()
-        t0 = time.perf_counter()
-        run()
-        ks.synchronize()
-        vs.synchronize()
-        cs.synchronize()
-        dt = time.perf_counter() - t0
+        out.zero_()
+        dt = median_s(run, (ks, vs, cs))
         assert bool(ok.all()) and torch.equal(out, d_pt), "pipeline produced wrong output"
         res["%s_gbps" % name] = round(length / dt / 1e9, 2)
         log("pipeline %s: %.2f GB/s" % (name, length / dt / 1e9))
@@ -393,40 +414,35 @@ def pipeline(F, W, torch, np, dev):
     h_tg = torch.empty((n, 16), dtype=torch.uint8, pin_memory=True)
     d_ctb = torch.empty_like(d_pt)
     d_tg = torch.empty((n, 16), dtype=torch.uint8, device=dev)
-    for rep in range(2):
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        F.pipeline_d2h(key, iv, chain, d_pt, chunk_bytes=chunk, out=d_ctb, tags=d_tg, h_ct=h_out, h_tags=h_tg,
-                       copy_stream=cs, compute_stream=ks)
-        cs.synchronize()
-        dt = time.perf_counter() - t0
-    assert torch.equal(h_out, h_ct) and torch.equal(h_tg, h_tags), "D2H pipeline produced wrong ciphertext"
-    res["d2h_gbps"] = round(length / dt / 1e9, 2)
-    log("pipeline d2h: %.2f GB/s" % res["d2h_gbps"])
-    with torch.cuda.stream(cs):
-        for rep in range(2):
-            torch.cuda.synchronize()
-            t0 = time.perf_counter()
-            for off in range(0, length, chunk):
-                h_out[off:off + chunk].copy_(d_ctb[off:off + chunk], non_blocking=True)
-            cs.synchronize()
-            dt = time.perf_counter() - t0
+    for name, mode in (("d2h", F.PIPE_FUSED), ("d2h_direct", F.PIPE_DIRECT)):
+        h_out.zero_()
+        dt = median_s(lambda: F.pipeline_d2h(key, iv, chain, d_pt, chunk_bytes=chunk, out=d_ctb, tags=d_tg,
+                                             h_ct=h_out, h_tags=h_tg, copy_stream=cs, compute_stream=ks, mode=mode),
+                      (cs, ks))
+        assert torch.equal(h_out, h_ct) and torch.equal(h_tg, h_tags), "%s produced wrong ciphertext" % name
+        res["%s_gbps" % name] = round(length / dt / 1e9, 2)
+        log("pipeline %s: %.2f GB/s" % (name, res["%s_gbps" % name]))
+    # plain pinned copies of the same bytes in the same chunks on one stream, through
+    # the runtime's hipMemcpyAsync (the copy engine's rate, nothing else enqueued)
+    hip = ctypes.CDLL(hip_runtime_path())
+    hip.hipMemcpyAsync.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p]
+    hip.hipMemcpyAsync.restype = ctypes.c_int
+
+    def copies(dst, src, kind):
+        for off in range(0, length, chunk):
+            assert hip.hipMemcpyAsync(dst + off, src + off, chunk, kind, cs.cuda_stream) == 0
+
+    dt = median_s(lambda: copies(h_out.data_ptr(), d_ctb.data_ptr(), 2), (cs,))
     res["pinned_copy_d2h_gbps"] = round(length / dt / 1e9, 2)
     res["d2h_ratio_vs_copy"] = round(res["d2h_gbps"] / res["pinned_copy_d2h_gbps"], 3)
+    res["d2h_direct_ratio_vs_copy"] = round(res["d2h_direct_gbps"] / res["pinned_copy_d2h_gbps"], 3)
     log("pinned d2h copy %.2f GB/s" % res["pinned_copy_d2h_gbps"])
     del h_out, d_ctb, d_tg
-    # plain pinned copy of the same bytes in the same chunks on one stream
-    with torch.cuda.stream(cs):
-        for rep in range(2):
-            torch.cuda.synchronize()
-            t0 = time.perf_counter()
-            for off in range(0, length, chunk):
-                out[off:off + chunk].copy_(h_ct[off:off + chunk], non_blocking=True)
-            cs.synchronize()
-            dt = time.perf_counter() - t0
+    dt = median_s(lambda: copies(out.data_ptr(), h_ct.data_ptr(), 1), (cs,))
     res["pinned_copy_gbps"] = round(length / dt / 1e9, 2)
     best = max(res["depth0_gbps"], res["depth2_gbps"], res["depth3_gbps"])
     res["ratio_vs_copy"] = round(best / res["pinned_copy_gbps"], 3)
+    res["direct_ratio_vs_copy"] = round(res["direct_gbps"] / res["pinned_copy_gbps"], 3)
     log("pinned copy %.2f GB/s" % res["pinned_copy_gbps"])
     del stage, out, ok, h_ct, d_pt
     torch.cuda.empty_cache()

@@ -61,6 +61,7 @@ enum fastrack_status {
 #define FASTRACK_PIPE_FUSED 0u   /* decrypt + verify each chunk in one kernel */
 #define FASTRACK_PIPE_EAGER 1u   /* plaintext first, the tag check beside it (section 5.3) */
 #define FASTRACK_PIPE_OTP   2u   /* keystream of the next chunk while it is in flight (section 5.3) */
+#define FASTRACK_PIPE_DIRECT 3u  /* the kernel reads the pinned buffer over the host link itself */
 
 /* Number of chains, ceil(len / chain_bytes); 0 when chain_bytes is 0. */
 uint64_t fastrack_num_chains(uint64_t len, uint64_t chain_bytes);
@@ -141,18 +142,23 @@ uint64_t fastrack_pipeline_stage_bytes(uint64_t len, uint64_t chain_bytes, uint3
  * pipeline): ciphertext in a pinned host "bounce buffer" (section 3.1) is
  * copied in chunks of chunk_bytes on copy_stream, and each chunk's chains are
  * decrypted and verified on compute_stream while the next chunks are in flight.
- *   h_ct         [len] ciphertext, PINNED host memory (ENOTPINNED otherwise)
+ *   h_ct         [len] ciphertext, PINNED host memory: all of [h_ct, h_ct + len)
+ *                inside one pinned allocation (ENOTPINNED otherwise)
  *   h_tags       [n][16] host tags; h_aad [n][aad_bytes] host AAD (or NULL)
  *   chunk_bytes  a nonzero multiple of chain_bytes
  *   depth        0: each chunk is copied to its place in d_pt and decrypted in
- *                place (no slot is reused, so the copies never wait);
- *                2..8: a ring of `depth` device staging slots in d_stage, the
- *                copy into a slot waiting for the decrypt that last used it
+ *                place (no slot is reused);
+ *                2..8: a ring of `depth` device staging slots in d_stage; a
+ *                slot is refilled only after the decrypt that last read it
  *   d_stage      device workspace, 256-byte aligned, of
  *                stage_bytes >= fastrack_pipeline_stage_bytes(...): the ring
  *                (depth > 0), then the tags and the AAD
  *   d_pt, d_ok   device outputs as in fastrack_gcm_decrypt_verify
- * Results are valid once compute_stream has completed (it waits on the copies).
+ * The calling thread paces the copies: before enqueueing the copy of chunk k it
+ * waits until chunk k - W has been decrypted (W = depth with a ring, 4 in place),
+ * so the call returns about W chunks before the transfer ends and copy_stream
+ * never waits on the device for compute_stream. Results are valid once
+ * compute_stream has completed (it waits on the copies).
  * EINVAL additionally covers chunk_bytes, depth and an undersized d_stage.
  */
 int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
@@ -172,8 +178,11 @@ int fastrack_pipeline_h2d(const uint8_t *key, const uint8_t *base_iv, uint64_t c
  *            of chunk `chunk` into ring slot `slot`, 5 decrypt + verify chunk
  *            `chunk` read from buffer `slot`, 6 XOR keystream slot `aux` into chunk
  *            `chunk` read from buffer `slot` + tag check, 7 decrypt only, 8 tag
- *            check only. Buffer slot -1 is the chunk's own place in d_pt, 0..depth-1
- *            a staging slot. stream: 0 copy, 1 compute, 2 verify. event: -1 none.
+ *            check only, 9 the calling thread waits until the last record of
+ *            `event` (that of chunk `chunk`) has completed, 10 decrypt + verify of
+ *            the whole buffer read from host memory by the kernel. Buffer slot -1
+ *            is the chunk's own place in d_pt, 0..depth-1 a staging slot.
+ *            stream: 0 copy, 1 compute, 2 verify. event: -1 none.
  * Returns the number of operations (>= 0; 0 for len = 0) or FASTRACK_EINVAL for
  * the argument errors the pipeline itself rejects (chunk_bytes, depth, mode).
  */
@@ -193,8 +202,16 @@ int64_t fastrack_pipeline_plan(uint64_t len, uint64_t chain_bytes, uint64_t chun
  *                        of chunk k+1 is generated on compute_stream into one of
  *                        depth >= 2 slots while chunk k+1 is in flight, so once
  *                        it lands only the XOR and the tag check remain.
+ *   FASTRACK_PIPE_DIRECT no copy engine and no chunks: after the tags and AAD
+ *                        are uploaded on copy_stream, one decrypt + verify
+ *                        launch on compute_stream reads h_ct through its device
+ *                        mapping, so the transfer and the decryption are the
+ *                        same loads. Needs depth 0. The launch occupies every
+ *                        compute unit for the whole transfer (PCIe-bound), where
+ *                        the chunked modes leave them free between chunks.
  * d_stage is sized by fastrack_pipeline_stage_bytes(..., depth) for every mode.
- * EINVAL additionally covers an unknown mode and depth 0 with EAGER or OTP.
+ * EINVAL additionally covers an unknown mode, depth 0 with EAGER or OTP, and
+ * depth > 0 with DIRECT.
  */
 int fastrack_pipeline_h2d_mode(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
                                const uint8_t *h_ct, uint64_t len, const uint8_t *h_tags, const uint8_t *h_aad,
@@ -214,7 +231,8 @@ int fastrack_pipeline_h2d_mode(const uint8_t *key, const uint8_t *base_iv, uint6
  * before enqueueing its copies, and returns once all copies are enqueued (the
  * encryptions are then done; the copies may still be running).
  *   d_aad        [n][aad_bytes] device AAD, or NULL with aad_bytes = 0
- *   h_ct         [len] PINNED host memory (ENOTPINNED otherwise)
+ *   h_ct         [len] PINNED host memory, all of it inside one pinned
+ *                allocation (ENOTPINNED otherwise)
  * h_ct and h_tags are valid once copy_stream has completed.
  * EINVAL covers the checks of fastrack_gcm_encrypt_tag, chunk_bytes (a nonzero
  * multiple of chain_bytes) and NULL h_ct, h_tags or d_tags.
@@ -223,6 +241,24 @@ int fastrack_pipeline_d2h(const uint8_t *key, const uint8_t *base_iv, uint64_t c
                           uint64_t len, const uint8_t *d_aad, uint32_t aad_bytes, uint64_t chunk_bytes,
                           uint8_t *d_ct, uint8_t *d_tags, uint8_t *h_ct, uint8_t *h_tags, void *copy_stream,
                           void *compute_stream);
+
+/*
+ * fastrack_pipeline_d2h with a mode:
+ *   FASTRACK_PIPE_FUSED  as fastrack_pipeline_d2h
+ *   FASTRACK_PIPE_DIRECT one encrypt + tag launch on compute_stream writes the
+ *                        ciphertext straight into h_ct through its device
+ *                        mapping (d_ct is not used and may be NULL); the tags
+ *                        follow to h_tags on compute_stream, and copy_stream
+ *                        waits for both. The launch occupies every compute unit
+ *                        for the whole transfer.
+ * h_ct must lie inside one pinned allocation for both modes (ENOTPINNED).
+ * EINVAL additionally covers the other modes; chunk_bytes is checked as for the
+ * chunked mode in both.
+ */
+int fastrack_pipeline_d2h_mode(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                               const uint8_t *d_pt, uint64_t len, const uint8_t *d_aad, uint32_t aad_bytes,
+                               uint64_t chunk_bytes, uint8_t *d_ct, uint8_t *d_tags, uint8_t *h_ct, uint8_t *h_tags,
+                               void *copy_stream, void *compute_stream, uint32_t mode);
 
 /*
  * Ragged chains: the paper's per-sample layout (section 5.2: every input sample

@@ -16,10 +16,10 @@ from . import build as _build
 
 __all__ = ["FastrackError", "decrypt_verify", "encrypt_tag", "decrypt_eager", "Eager", "keystream", "apply_verify",
            "pipeline_h2d", "pipeline_d2h", "decrypt_verify_ragged", "encrypt_tag_ragged", "sample_chains", "num_chains", "stage_bytes", "shutdown", "library_path", "F_SEQ_GHASH", "PIPE_FUSED",
-           "PIPE_EAGER", "PIPE_OTP"]
+           "PIPE_EAGER", "PIPE_OTP", "PIPE_DIRECT"]
 
 F_SEQ_GHASH = 1
-PIPE_FUSED, PIPE_EAGER, PIPE_OTP = 0, 1, 2
+PIPE_FUSED, PIPE_EAGER, PIPE_OTP, PIPE_DIRECT = 0, 1, 2, 3
 
 OK, EINVAL, EHIP, ENOTPINNED, ENOMEM = 0, -1, -2, -3, -4
 _NAMES = {EINVAL: "EINVAL", EHIP: "EHIP", ENOTPINNED: "ENOTPINNED", ENOMEM: "ENOMEM"}
@@ -63,6 +63,9 @@ def lib():
         L.fastrack_pipeline_h2d_mode.restype = _ct.c_int
         L.fastrack_pipeline_d2h.argtypes = [u8p, u8p, u64, u8p, u64, u8p, u32, u64, u8p, u8p, u8p, u8p, vp, vp]
         L.fastrack_pipeline_d2h.restype = _ct.c_int
+        L.fastrack_pipeline_d2h_mode.argtypes = [u8p, u8p, u64, u8p, u64, u8p, u32, u64, u8p, u8p, u8p, u8p, vp, vp,
+                                                 u32]
+        L.fastrack_pipeline_d2h_mode.restype = _ct.c_int
         L.fastrack_gcm_decrypt_eager.argtypes = [u8p, u8p, u64, u8p, u64, u8p, u8p, u32, u8p, u8p, vp, vp]
         L.fastrack_gcm_decrypt_eager.restype = _ct.c_int
         L.fastrack_gcm_keystream.argtypes = [u8p, u8p, u64, u64, u64, u8p, vp]
@@ -248,7 +251,7 @@ def pipeline_h2d(key, base_iv, chain_bytes, h_ct, h_tags, h_aad=None, chunk_byte
                  verify_stream=None):
     """Chunked H2D copy of pinned ciphertext overlapped with decrypt + verify. Returns (pt, ok) on the device.
     mode PIPE_EAGER checks the tags on verify_stream; PIPE_OTP generates each chunk's keystream while it is
-    in flight. Both need depth >= 2."""
+    in flight. Both need depth >= 2. PIPE_DIRECT (depth 0) has the decrypt kernel read h_ct itself."""
     if not (isinstance(h_ct, _torch.Tensor) and h_ct.device.type == "cpu" and h_ct.dtype == _torch.uint8):
         raise ValueError("h_ct must be a uint8 CPU tensor in pinned memory")
     device = _torch.device("cuda", _torch.cuda.current_device()) if device is None else _torch.device(device)
@@ -276,15 +279,16 @@ def pipeline_h2d(key, base_iv, chain_bytes, h_ct, h_tags, h_aad=None, chunk_byte
 
 
 def pipeline_d2h(key, base_iv, chain_bytes, pt, aad=None, chunk_bytes=8 << 20, out=None, tags=None, h_ct=None,
-                 h_tags=None, copy_stream=None, compute_stream=None):
+                 h_tags=None, copy_stream=None, compute_stream=None, mode=PIPE_FUSED):
     """Encrypt + tag pt (uint8 CUDA tensor) chunk by chunk into `out` (device; may be pt) and copy each
-    chunk to the pinned host tensor h_ct while later chunks are encrypted. Returns (h_ct, h_tags)."""
+    chunk to the pinned host tensor h_ct while later chunks are encrypted. Returns (h_ct, h_tags).
+    mode PIPE_DIRECT writes the ciphertext straight into h_ct from the kernel (`out` is not used)."""
     _u8_dev(pt, "pt")
     n = num_chains(pt.numel(), chain_bytes)
     aad_bytes = 0 if aad is None else aad.numel() // max(n, 1)
     if aad is not None:
         _u8_dev(aad, "aad")
-    if out is None:
+    if out is None and mode != PIPE_DIRECT:
         out = _torch.empty_like(pt)
     if tags is None:
         tags = _torch.empty((n, 16), dtype=_torch.uint8, device=pt.device)
@@ -296,10 +300,10 @@ def pipeline_d2h(key, base_iv, chain_bytes, pt, aad=None, chunk_bytes=8 << 20, o
         raise ValueError("h_ct must be a pinned uint8 CPU tensor of at least len bytes")
     if h_tags.device.type != "cpu" or h_tags.numel() < 16 * n:
         raise ValueError("h_tags must be a uint8 CPU tensor of n x 16 bytes")
-    _check(lib().fastrack_pipeline_d2h(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"), chain_bytes,
-                                       _dptr(pt), pt.numel(), _dptr(aad), aad_bytes, chunk_bytes, _dptr(out),
-                                       _dptr(tags), h_ct.data_ptr(), h_tags.data_ptr(), _stream(copy_stream),
-                                       _stream(compute_stream)))
+    _check(lib().fastrack_pipeline_d2h_mode(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
+                                            chain_bytes, _dptr(pt), pt.numel(), _dptr(aad), aad_bytes, chunk_bytes,
+                                            _dptr(out), _dptr(tags), h_ct.data_ptr(), h_tags.data_ptr(),
+                                            _stream(copy_stream), _stream(compute_stream), mode))
     return h_ct, h_tags
 
 

@@ -576,6 +576,8 @@ enum PlanKind : uint32_t {
     kOpApply = 6,      // XOR keystream slot `aux` into chunk `chunk` (read from `slot`) + tag check
     kOpCtr = 7,        // decrypt chunk `chunk` from buffer `slot` into d_pt (no tag check)
     kOpVerify = 8,     // tag check of chunk `chunk` read from buffer `slot`
+    kOpHostWait = 9,   // the calling thread waits until the last record of `event` has completed
+    kOpDirect = 10,    // decrypt + verify all of h_ct, read over the host link by the kernel itself
 };
 struct PlanOp {
     uint32_t kind;
@@ -585,13 +587,24 @@ struct PlanOp {
     int32_t slot;
     int32_t aux;
 };
-// Events: meta (0); copied[i] (1..P), freed[i] (1+P..2P), decrypted[i] (1+2P..3P), reused modulo
-// P = 4: copied[k % P] is waited on right after it is recorded, decrypted[k % P] at once by the
-// verify stream, freed[k % P] at most two chunks later (a wait takes the event's state at the
-// time it is enqueued).
-constexpr int kPlanP = 4;
+// Events: meta (0); copied[i] (1..P), done[i] (1+P..2P), decrypted[i] (1+2P..3P), reused modulo
+// P = 8. copied[k % P] and decrypted[k % P] are waited on right after they are recorded;
+// done[k % P] is waited on by the calling thread before the copy of chunk k + W, W <= 8, which
+// comes before chunk k + P records it again (a wait takes the event's last record at the time).
+constexpr int kPlanP = 8;
 constexpr int kPlanEvents = 3 * kPlanP + 1;
+// Chunks the calling thread lets the copies run ahead of the last finished chunk when no
+// staging slot bounds it (in place and keystream-ahead schedules).
+constexpr uint64_t kPaceChunks = 4;
 
+// The operations of one H2D pipeline call, in the order they are enqueued. Streams:
+// 0 copy, 1 compute, 2 verify (eager mode). The copy stream never waits for an event
+// of another stream: a ring slot is reused only after the calling thread has seen the
+// event of its last read complete (kOpHostWait). A device-side wait there would also
+// be correct, but the runtime then holds the calling thread inside the next copy's
+// enqueue until the event completes, which delays the launches queued behind it and
+// leaves the copy engine idle between chunks; waiting explicitly, and early, keeps
+// the copies back to back.
 std::vector<PlanOp> h2d_plan(uint64_t len, uint64_t chunk_bytes, int depth, uint32_t mode)
 {
     std::vector<PlanOp> ops;
@@ -599,12 +612,16 @@ std::vector<PlanOp> h2d_plan(uint64_t len, uint64_t chunk_bytes, int depth, uint
     auto op = [&](uint32_t kind, uint32_t stream, int32_t event, uint64_t chunk, int32_t slot, int32_t aux) {
         ops.push_back(PlanOp{kind, stream, event, chunk, slot, aux});
     };
-    const int32_t meta = 0, copied = 1, freed = 1 + kPlanP, decrypted = 1 + 2 * kPlanP;
+    const int32_t meta = 0, copied = 1, done = 1 + kPlanP, decrypted = 1 + 2 * kPlanP;
     op(kOpMeta, 0, -1, 0, -1, -1);
     op(kOpRecord, 0, meta, 0, -1, -1);
     op(kOpWait, 1, meta, 0, -1, -1);
     if (VS != 1)
         op(kOpWait, VS, meta, 0, -1, -1);
+    if (mode == FASTRACK_PIPE_DIRECT) {   // no copies: the kernel reads the pinned buffer itself
+        op(kOpDirect, 1, -1, 0, -1, -1);
+        return ops;
+    }
     const uint64_t nchunks = (len + chunk_bytes - 1) / chunk_bytes;
     // OTP: the keystream of chunk 0 before anything arrives; that of chunk k+1 while
     // chunk k+1 is on the bus, in ring slot (k+1) % depth. A slot is rewritten only
@@ -612,20 +629,16 @@ std::vector<PlanOp> h2d_plan(uint64_t len, uint64_t chunk_bytes, int depth, uint
     if (mode == FASTRACK_PIPE_OTP)
         op(kOpKeystream, 1, -1, 0, 0, -1);
     // depth 0 (and OTP): each chunk is copied straight to its place in d_pt and
-    // decrypted there, so no buffer is reused and the copy stream never waits. A ring
-    // of `depth` slots must not overwrite slot k % depth before chunk k - depth has
-    // been read; the copy stream waits for the release two chunks back, which covers
-    // the next depth - 1 copies and, with decrypts faster than copies, has happened by
-    // then (a wait on the copy stream costs the copy engine time).
+    // decrypted there, so no buffer is reused; the calling thread still keeps the
+    // copies at most kPaceChunks ahead of the decrypts. A ring of `depth` slots must
+    // not overwrite slot k % depth before chunk k - depth has been read.
     const bool ring = mode != FASTRACK_PIPE_OTP && depth > 0;
-    int64_t covered = -1;   // copies up to this chunk index have their slot's wait enqueued
+    const uint64_t window = ring ? (uint64_t)depth : kPaceChunks;
     for (uint64_t k = 0; k < nchunks; ++k) {
         const int32_t buf = ring ? (int32_t)(k % (uint64_t)depth) : -1;
         const int32_t e = (int32_t)(k % kPlanP);
-        if (ring && k >= (uint64_t)depth && (int64_t)k > covered) {
-            op(kOpWait, 0, freed + (int32_t)((k - 2) % kPlanP), 0, -1, -1);
-            covered = (int64_t)k + depth - 2;
-        }
+        if (k >= window)
+            op(kOpHostWait, 0, done + (int32_t)((k - window) % kPlanP), k - window, -1, -1);
         op(kOpCopy, 0, -1, k, buf, -1);
         op(kOpRecord, 0, copied + e, 0, -1, -1);
         if (mode == FASTRACK_PIPE_OTP && k + 1 < nchunks)
@@ -642,10 +655,44 @@ std::vector<PlanOp> h2d_plan(uint64_t len, uint64_t chunk_bytes, int depth, uint
             op(kOpVerify, VS, -1, k, buf, -1);
             op(kOpWait, VS, decrypted + e, 0, -1, -1);   // the slot is free once both have read it
         }
-        if (ring)
-            op(kOpRecord, VS, freed + e, 0, -1, -1);
+        op(kOpRecord, VS, done + e, 0, -1, -1);
     }
     return ops;
+}
+
+int check_pipe_mode(uint32_t mode, int depth)
+{
+    if (mode > FASTRACK_PIPE_DIRECT)
+        return fail(FASTRACK_EINVAL, "unknown pipeline mode %u", mode);
+    if (depth < 0 || depth == 1 || depth > kMaxPipelineDepth)
+        return fail(FASTRACK_EINVAL, "depth must be 0 (in place) or 2..%d (staging ring)", kMaxPipelineDepth);
+    if ((mode == FASTRACK_PIPE_EAGER || mode == FASTRACK_PIPE_OTP) && depth == 0)
+        return fail(FASTRACK_EINVAL, "the eager and keystream pipelines need depth >= 2 staging slots");
+    if (mode == FASTRACK_PIPE_DIRECT && depth != 0)
+        return fail(FASTRACK_EINVAL, "the direct pipeline reads the host buffer in place and takes depth 0");
+    return FASTRACK_OK;
+}
+
+// [p, p + len) must lie inside one pinned host allocation: the copy engine (or, in the
+// direct mode, the kernel) reads all of it through the allocation's device mapping.
+// Returns the device address of p, or nullptr.
+const uint8_t *pinned_range(const uint8_t *p, uint64_t len)
+{
+    hipPointerAttribute_t attr;
+    if (hipPointerGetAttributes(&attr, p) != hipSuccess || attr.type != hipMemoryTypeHost || !attr.devicePointer) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    hipDeviceptr_t base = 0;
+    size_t size = 0;
+    if (hipMemGetAddressRange(&base, &size, (hipDeviceptr_t)const_cast<uint8_t *>(p)) != hipSuccess) {
+        (void)hipGetLastError();
+        return nullptr;
+    }
+    const uintptr_t b = (uintptr_t)base, a = (uintptr_t)p;
+    if (a < b || a - b > size || len > size - (a - b))
+        return nullptr;
+    return static_cast<const uint8_t *>(attr.devicePointer);
 }
 
 int pipeline_impl(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes, const uint8_t *h_ct, uint64_t len,
@@ -661,12 +708,8 @@ int pipeline_impl(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_byt
         return fail(FASTRACK_EINVAL, "h_tags, d_ok and d_stage must be non-NULL");
     if (chunk_bytes == 0 || chunk_bytes % chain_bytes != 0)
         return fail(FASTRACK_EINVAL, "chunk_bytes must be a nonzero multiple of chain_bytes");
-    if (mode > FASTRACK_PIPE_OTP)
-        return fail(FASTRACK_EINVAL, "unknown pipeline mode %u", mode);
-    if (depth < 0 || depth == 1 || depth > kMaxPipelineDepth)
-        return fail(FASTRACK_EINVAL, "depth must be 0 (in place) or 2..%d (staging ring)", kMaxPipelineDepth);
-    if (mode != FASTRACK_PIPE_FUSED && depth == 0)
-        return fail(FASTRACK_EINVAL, "the eager and keystream pipelines need depth >= 2 staging slots");
+    if ((rc = check_pipe_mode(mode, depth)))
+        return rc;
     if ((uintptr_t)d_stage & 255)
         return fail(FASTRACK_EINVAL, "d_stage must be 256-byte aligned");
     const uint64_t need = fastrack_pipeline_stage_bytes(len, chain_bytes, aad_bytes, chunk_bytes, depth);
@@ -674,12 +717,10 @@ int pipeline_impl(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_byt
         return fail(FASTRACK_EINVAL, "d_stage holds %llu bytes, the pipeline needs %llu",
                     (unsigned long long)stage_bytes, (unsigned long long)need);
 
-    hipPointerAttribute_t attr;
-    hipError_t he = hipPointerGetAttributes(&attr, h_ct);
-    if (he != hipSuccess || attr.type != hipMemoryTypeHost) {
-        (void)hipGetLastError();
-        return fail(FASTRACK_ENOTPINNED, "h_ct is not pinned host memory");
-    }
+    const uint8_t *h_ct_dev = pinned_range(h_ct, len);
+    if (!h_ct_dev)
+        return fail(FASTRACK_ENOTPINNED, "h_ct .. h_ct + len is not inside one pinned host allocation");
+    hipError_t he = hipSuccess;
 
     std::lock_guard<std::mutex> lk(g_mu);
     int dev, ncu;
@@ -757,6 +798,13 @@ int pipeline_impl(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_byt
             rc = run_gcm(false, kVerify, ctx, base_iv, chain_bytes, k * cpc, buf_of(o), nullptr, chunk_len(k), nullptr,
                          aad, aad_bytes, d_tags, nullptr, d_ok, 0, dev, ncu, st);
             break;
+        case kOpHostWait:
+            he = hipEventSynchronize(ev[o.event]);
+            break;
+        case kOpDirect:
+            rc = run_gcm(false, kFused, ctx, base_iv, chain_bytes, 0, h_ct_dev, nullptr, len, d_pt, aad, aad_bytes,
+                         d_tags, nullptr, d_ok, 0, dev, ncu, st);
+            break;
         }
         if (he != hipSuccess) {
             cleanup();
@@ -781,12 +829,8 @@ FT_EXPORT int64_t fastrack_pipeline_plan(uint64_t len, uint64_t chain_bytes, uin
         return fail(FASTRACK_EINVAL, "chain_bytes must be a nonzero multiple of 16");
     if (chunk_bytes == 0 || chunk_bytes % chain_bytes != 0)
         return fail(FASTRACK_EINVAL, "chunk_bytes must be a nonzero multiple of chain_bytes");
-    if (mode > FASTRACK_PIPE_OTP)
-        return fail(FASTRACK_EINVAL, "unknown pipeline mode %u", mode);
-    if (depth < 0 || depth == 1 || depth > kMaxPipelineDepth)
-        return fail(FASTRACK_EINVAL, "depth must be 0 (in place) or 2..%d (staging ring)", kMaxPipelineDepth);
-    if (mode != FASTRACK_PIPE_FUSED && depth == 0)
-        return fail(FASTRACK_EINVAL, "the eager and keystream pipelines need depth >= 2 staging slots");
+    if (int rc = check_pipe_mode(mode, depth))
+        return rc;
     if (len == 0)
         return 0;
     const std::vector<PlanOp> ops = h2d_plan(len, chunk_bytes, depth, mode);
@@ -824,27 +868,66 @@ FT_EXPORT int fastrack_pipeline_h2d_mode(const uint8_t *key, const uint8_t *base
                          d_stage, stage_bytes, d_pt, d_ok, copy_stream, compute_stream, verify_stream);
 }
 
-FT_EXPORT int fastrack_pipeline_d2h(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
-                                    const uint8_t *d_pt, uint64_t len, const uint8_t *d_aad, uint32_t aad_bytes,
-                                    uint64_t chunk_bytes, uint8_t *d_ct, uint8_t *d_tags, uint8_t *h_ct,
-                                    uint8_t *h_tags, void *copy_stream, void *compute_stream)
+namespace {
+
+// Direct D2H: one encrypt + tag launch writes the ciphertext through the device
+// mapping of the pinned buffer; the tags follow on the same stream, and copy_stream
+// is ordered after both so that the results are valid when it completes, as in the
+// chunked mode.
+int d2h_direct(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes, const uint8_t *d_pt, uint64_t len,
+               const uint8_t *d_aad, uint32_t aad_bytes, uint8_t *d_tags, uint8_t *h_ct_dev, uint8_t *h_tags,
+               hipStream_t cs, hipStream_t ks)
+{
+    const uint64_t n = (len + chain_bytes - 1) / chain_bytes;
+    hipEvent_t e;
+    hipError_t he = hipEventCreateWithFlags(&e, hipEventDisableTiming);
+    if (he != hipSuccess)
+        return hip_fail(he, "hipEventCreate");
+    int rc;
+    {
+        std::lock_guard<std::mutex> lk(g_mu);
+        int dev, ncu;
+        const KeyCtx *ctx;
+        if (!(rc = current_device(&dev, &ncu)) && !(rc = key_ctx(key, ks, dev, &ctx)))
+            rc = run_gcm(true, kFused, ctx, base_iv, chain_bytes, 0, d_pt, nullptr, len, h_ct_dev,
+                         aad_bytes ? d_aad : nullptr, aad_bytes, nullptr, d_tags, nullptr, 0, dev, ncu, ks);
+    }
+    if (!rc) {
+        he = hipMemcpyAsync(h_tags, d_tags, 16 * n, hipMemcpyDeviceToHost, ks);
+        if (he == hipSuccess)
+            he = hipEventRecord(e, ks);
+        if (he == hipSuccess && cs != ks)
+            he = hipStreamWaitEvent(cs, e, 0);
+        if (he != hipSuccess)
+            rc = hip_fail(he, "direct D2H ordering");
+    }
+    (void)hipEventDestroy(e);
+    return rc;
+}
+
+int d2h_impl(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes, const uint8_t *d_pt, uint64_t len,
+             const uint8_t *d_aad, uint32_t aad_bytes, uint64_t chunk_bytes, uint8_t *d_ct, uint8_t *d_tags,
+             uint8_t *h_ct, uint8_t *h_tags, void *copy_stream, void *compute_stream, uint32_t mode)
 {
     g_err.clear();
-    int rc = check_common(key, base_iv, chain_bytes, len, d_pt, d_ct, d_aad, aad_bytes, 0);
+    if (mode != FASTRACK_PIPE_FUSED && mode != FASTRACK_PIPE_DIRECT)
+        return fail(FASTRACK_EINVAL, "the D2H pipeline takes FASTRACK_PIPE_FUSED or FASTRACK_PIPE_DIRECT (got %u)", mode);
+    const bool direct = mode == FASTRACK_PIPE_DIRECT;
+    int rc = check_common(key, base_iv, chain_bytes, len, d_pt, direct ? h_ct : d_ct, d_aad, aad_bytes, 0);
     if (rc || len == 0)
         return rc;
     if (!d_tags || !h_ct || !h_tags)
         return fail(FASTRACK_EINVAL, "d_tags, h_ct and h_tags must be non-NULL");
     if (chunk_bytes == 0 || chunk_bytes % chain_bytes != 0)
         return fail(FASTRACK_EINVAL, "chunk_bytes must be a nonzero multiple of chain_bytes");
-    hipPointerAttribute_t attr;
-    hipError_t he = hipPointerGetAttributes(&attr, h_ct);
-    if (he != hipSuccess || attr.type != hipMemoryTypeHost) {
-        (void)hipGetLastError();
-        return fail(FASTRACK_ENOTPINNED, "h_ct is not pinned host memory");
-    }
+    uint8_t *h_ct_dev = const_cast<uint8_t *>(pinned_range(h_ct, len));
+    if (!h_ct_dev)
+        return fail(FASTRACK_ENOTPINNED, "h_ct .. h_ct + len is not inside one pinned host allocation");
+    hipError_t he = hipSuccess;
     hipStream_t cs = reinterpret_cast<hipStream_t>(copy_stream);
     hipStream_t ks = reinterpret_cast<hipStream_t>(compute_stream);
+    if (direct)
+        return d2h_direct(key, base_iv, chain_bytes, d_pt, len, d_aad, aad_bytes, d_tags, h_ct_dev, h_tags, cs, ks);
     const uint64_t n = (len + chain_bytes - 1) / chain_bytes;
     const uint64_t nchunks = (len + chunk_bytes - 1) / chunk_bytes;
     const uint64_t cpc = chunk_bytes / chain_bytes;
@@ -917,6 +1000,26 @@ FT_EXPORT int fastrack_pipeline_d2h(const uint8_t *key, const uint8_t *base_iv, 
     if (he != hipSuccess)
         return hip_fail(he, "tag copy");
     return FASTRACK_OK;
+}
+
+}  // namespace
+
+FT_EXPORT int fastrack_pipeline_d2h(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                                    const uint8_t *d_pt, uint64_t len, const uint8_t *d_aad, uint32_t aad_bytes,
+                                    uint64_t chunk_bytes, uint8_t *d_ct, uint8_t *d_tags, uint8_t *h_ct,
+                                    uint8_t *h_tags, void *copy_stream, void *compute_stream)
+{
+    return d2h_impl(key, base_iv, chain_bytes, d_pt, len, d_aad, aad_bytes, chunk_bytes, d_ct, d_tags, h_ct, h_tags,
+                    copy_stream, compute_stream, FASTRACK_PIPE_FUSED);
+}
+
+FT_EXPORT int fastrack_pipeline_d2h_mode(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                                         const uint8_t *d_pt, uint64_t len, const uint8_t *d_aad, uint32_t aad_bytes,
+                                         uint64_t chunk_bytes, uint8_t *d_ct, uint8_t *d_tags, uint8_t *h_ct,
+                                         uint8_t *h_tags, void *copy_stream, void *compute_stream, uint32_t mode)
+{
+    return d2h_impl(key, base_iv, chain_bytes, d_pt, len, d_aad, aad_bytes, chunk_bytes, d_ct, d_tags, h_ct, h_tags,
+                    copy_stream, compute_stream, mode);
 }
 
 namespace {

@@ -122,7 +122,7 @@ def test_apply_verify_matches_oracle(F, length, chain, abytes):
         assert got[0] == 7 and got[n - 1] == 7                # chains outside the run untouched
 
 
-@pytest.mark.parametrize("mode,depth", [(1, 2), (1, 3), (2, 2), (2, 3), (0, 0), (0, 2)])
+@pytest.mark.parametrize("mode,depth", [(1, 2), (1, 3), (1, 8), (2, 2), (2, 3), (0, 0), (0, 2), (0, 8), (3, 0)])
 def test_pipeline_modes_small(F, mode, depth):
     import torch
     say("pipeline mode", mode, "depth", depth)
@@ -145,21 +145,23 @@ def test_pipeline_modes_small(F, mode, depth):
     assert np.array_equal(host(ok), want_ok)
 
 
-@pytest.mark.parametrize("length,chain,chunk,abytes,inplace", [
-    (24 * MiB + 3 * 64 * KiB + 100, 64 * KiB, 1 * MiB, 32, False),
-    (5 * MiB + 16, 256 * KiB, 2 * MiB, 0, True),
-    (40 * 4096 + 5, 4096, 4 * 4096, 13, False),
+@pytest.mark.parametrize("length,chain,chunk,abytes,inplace,mode", [
+    (24 * MiB + 3 * 64 * KiB + 100, 64 * KiB, 1 * MiB, 32, False, 0),
+    (5 * MiB + 16, 256 * KiB, 2 * MiB, 0, True, 0),
+    (40 * 4096 + 5, 4096, 4 * 4096, 13, False, 0),
+    (24 * MiB + 3 * 64 * KiB + 100, 64 * KiB, 1 * MiB, 32, False, 3),
+    (40 * 4096 + 5, 4096, 4 * 4096, 13, False, 3),
 ])
-def test_pipeline_d2h_matches_oracle(F, length, chain, chunk, abytes, inplace):
+def test_pipeline_d2h_matches_oracle(F, length, chain, chunk, abytes, inplace, mode):
     import torch
-    say("d2h", length, chain, chunk, abytes, inplace)
+    say("d2h", length, chain, chunk, abytes, inplace, "mode", mode)
     w = W.random_case(length % 977 + abytes, length, chain, abytes)
     aad = W.case_aad(w, chain)
     want_ct, want_tags = oracle.chains_encrypt(w.key, w.base_iv, chain, w.payload, aad, abytes)
     cs, ks = torch.cuda.Stream(), torch.cuda.Stream()
     d_pt = dev(w.payload)
     h_ct, h_tags = F.pipeline_d2h(w.key, w.base_iv, chain, d_pt, dev(aad) if abytes else None, chunk_bytes=chunk,
-                                  out=d_pt if inplace else None, copy_stream=cs, compute_stream=ks)
+                                  out=d_pt if inplace else None, copy_stream=cs, compute_stream=ks, mode=mode)
     cs.synchronize()
     assert np.array_equal(h_tags.numpy(), want_tags)
     assert np.array_equal(h_ct.numpy()[:length], want_ct)
@@ -180,3 +182,68 @@ def test_pipeline_d2h_gradients_256mib(F):
     cs.synchronize()
     assert np.array_equal(h_tags.numpy(), want_tags)
     assert np.array_equal(h_ct.numpy(), want_ct)
+
+
+def test_direct_modes_inside_a_larger_pinned_buffer(F):
+    # h_ct is a 16-byte-aligned view inside a larger pinned allocation: the kernel
+    # reads (H2D) or writes (D2H) exactly its bytes through the device mapping and
+    # leaves the guard bytes on both sides alone.
+    import torch
+    chain, length, front, back = 64 * KiB, 3 * MiB + 5 * 16 + 7, 4096 + 48, 4096
+    say("direct modes in a larger pinned buffer")
+    w = W.random_case(77, length, chain, 32)
+    aad = W.case_aad(w, chain)
+    ct, tags = oracle.chains_encrypt(w.key, w.base_iv, chain, w.payload, aad, 32)
+    W.flip_bit(ct[2 * chain:], 5)
+    want_pt, want_ok = oracle.chains_decrypt(w.key, w.base_iv, chain, ct, tags, aad, 32)
+    big = torch.full((front + length + back,), 0xA5, dtype=torch.uint8).pin_memory()
+    big[front:front + length].copy_(torch.from_numpy(ct))
+    cs, ks = torch.cuda.Stream(), torch.cuda.Stream()
+    pt, ok = F.pipeline_h2d(w.key, w.base_iv, chain, big[front:front + length], torch.from_numpy(tags),
+                            torch.from_numpy(aad), chunk_bytes=MiB, depth=0, copy_stream=cs, compute_stream=ks,
+                            mode=F.PIPE_DIRECT)
+    ks.synchronize()
+    assert np.array_equal(host(pt), want_pt)
+    assert np.array_equal(host(ok), want_ok)
+    # D2H: encrypt the plaintext into the middle of a guarded pinned buffer
+    want_ct, want_tags = oracle.chains_encrypt(w.key, w.base_iv, chain, w.payload, aad, 32)
+    big.fill_(0x5A)
+    h_tags = torch.empty((tags.shape[0], 16), dtype=torch.uint8).pin_memory()
+    F.pipeline_d2h(w.key, w.base_iv, chain, dev(w.payload), dev(aad), chunk_bytes=MiB, h_ct=big[front:front + length],
+                   h_tags=h_tags, copy_stream=cs, compute_stream=ks, mode=F.PIPE_DIRECT)
+    cs.synchronize()
+    b = big.numpy()
+    assert np.array_equal(b[front:front + length], want_ct)
+    assert np.array_equal(h_tags.numpy(), want_tags)
+    assert (b[:front] == 0x5A).all() and (b[front + length:] == 0x5A).all()
+
+
+def test_pipelines_reject_ranges_outside_one_pinned_allocation(F):
+    # [h_ct, h_ct + len) must lie inside one pinned allocation. The check runs on the
+    # host before any copy or launch: a range that runs 4 KiB past the end of a 1 MiB
+    # pinned block (a power of two, so the allocator's block is exactly that) and a
+    # pageable buffer are both rejected with ENOTPINNED, in both directions and modes.
+    import ctypes
+    import torch
+    L = F.lib()
+    chain, length = 64 * KiB, MiB
+    h = torch.zeros(length, dtype=torch.uint8).pin_memory()
+    pageable = torch.zeros(length, dtype=torch.uint8)
+    tags = torch.zeros((16, 16), dtype=torch.uint8)
+    d_pt = torch.empty(length, dtype=torch.uint8, device="cuda")
+    d_ct = torch.empty(length, dtype=torch.uint8, device="cuda")
+    d_tags = torch.empty((16, 16), dtype=torch.uint8, device="cuda")
+    ok = torch.empty(16, dtype=torch.uint8, device="cuda")
+    stage = torch.empty(F.stage_bytes(length, chain, 0, MiB, 0), dtype=torch.uint8, device="cuda")
+    key, iv = (ctypes.c_uint8 * 32)(), (ctypes.c_uint8 * 12)()
+    s = torch.cuda.current_stream().cuda_stream
+    for what, ptr in (("overrun", h.data_ptr() + 4096), ("pageable", pageable.data_ptr())):
+        for mode in (F.PIPE_FUSED, F.PIPE_DIRECT):
+            say("reject", what, "mode", mode)
+            rc = L.fastrack_pipeline_h2d_mode(key, iv, chain, ptr, length, tags.data_ptr(), None, 0, MiB, 0, mode,
+                                              stage.data_ptr(), stage.numel(), d_pt.data_ptr(), ok.data_ptr(), s, s, s)
+            assert rc == -3 and b"pinned" in L.fastrack_last_error(), (what, mode, rc)
+            rc = L.fastrack_pipeline_d2h_mode(key, iv, chain, d_pt.data_ptr(), length, None, 0, MiB, d_ct.data_ptr(),
+                                              d_tags.data_ptr(), ptr, tags.data_ptr(), s, s, mode)
+            assert rc == -3 and b"pinned" in L.fastrack_last_error(), (what, mode, rc)
+    torch.cuda.synchronize()

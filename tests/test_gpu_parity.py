@@ -197,7 +197,7 @@ def config5_data():
     del h_pt, h_ct
 
 
-@pytest.mark.parametrize("mode,depth", [(0, 0), (0, 2), (0, 3), (1, 2), (2, 2)])
+@pytest.mark.parametrize("mode,depth", [(0, 0), (0, 2), (0, 3), (1, 2), (2, 2), (3, 0)])
 def test_config5_pipeline_4gib(F, config5_data, mode, depth):
     import torch
     w, h_pt, h_ct, tags, want = config5_data

@@ -2,7 +2,9 @@
 operations the pipeline enqueues, in order, and a fake executor replays them with
 random operation durations under the stream and event rules the pipeline relies on
 (work on one stream runs in order; a wait holds its stream until the work recorded
-before the most recent record of the event, as of the wait's enqueue, has finished).
+before the most recent record of the event, as of the wait's enqueue, has finished;
+a host wait holds the calling thread, and so every operation enqueued after it,
+until then).
 For every duration draw: a staging slot is rewritten only after every read of its
 previous chunk has finished, a chunk is decrypted (and checked) only after its copy
 landed, a keystream slot is overwritten only after the XOR that read it, and every
@@ -16,7 +18,8 @@ import pytest
 
 MiB = 1 << 20
 FUSED, EAGER, OTP = 0, 1, 2
-META, RECORD, WAIT, COPY, KEYSTREAM, DECRYPT, APPLY, CTR, VERIFY = range(9)
+META, RECORD, WAIT, COPY, KEYSTREAM, DECRYPT, APPLY, CTR, VERIFY, HOST_WAIT, DIRECT = range(11)
+DIRECT_MODE = 3
 READS = (DECRYPT, APPLY, CTR, VERIFY)
 
 
@@ -46,7 +49,13 @@ def replay(ops, rng):
     stream_t = [0.0, 0.0, 0.0]
     event_t = {}
     times = []
+    host_t = 0.0   # nothing enqueued after a host wait starts before the wait returns
     for kind, stream, event, chunk, slot, aux in ops:
+        if kind == HOST_WAIT:
+            host_t = max(host_t, event_t[event])
+            times.append((host_t, host_t))
+            continue
+        stream_t[stream] = max(stream_t[stream], host_t)
         if kind == RECORD:
             event_t[event] = stream_t[stream]
             times.append((stream_t[stream], stream_t[stream]))
@@ -134,18 +143,58 @@ def test_schedule_is_safe_under_any_timing(L, length, chain, chunk, depth, mode)
 
 
 def test_a_missing_wait_is_caught(L):
-    # The copy stream's wait before reusing a ring slot is what keeps the slot safe:
-    # drop the first one and some duration draw must let a copy overrun a read.
+    # The host's wait before reusing a ring slot is what keeps the slot safe: drop
+    # the first one and some duration draw must let a copy overrun a read.
     ops = plan(L, 64 * MiB, MiB, 8 * MiB, 2, FUSED)
-    first_wait = next(i for i, o in enumerate(ops) if o[0] == WAIT and o[1] == 0)
+    first_wait = next(i for i, o in enumerate(ops) if o[0] == HOST_WAIT)
     broken = ops[:first_wait] + ops[first_wait + 1:]
     rng = random.Random(7)
     assert any(violations(broken, replay(broken, rng), 8) for _ in range(200))
 
 
+@pytest.mark.parametrize("length,chain,chunk,depth,mode", SCHEDULES)
+def test_copy_stream_never_waits_on_the_device(L, length, chain, chunk, depth, mode):
+    # Every device-side wait is on the compute or verify stream; the copies are held
+    # back only by the calling thread, at most `window` chunks ahead of the last
+    # finished chunk (depth with a ring, 4 otherwise).
+    ops = plan(L, length, chain, chunk, depth, mode)
+    assert not [o for o in ops if o[0] == WAIT and o[1] == 0]
+    window = depth if (mode != OTP and depth > 0) else 4
+    waited = {}
+    for i, o in enumerate(ops):
+        if o[0] == HOST_WAIT:
+            waited[i] = o[3]
+        if o[0] == COPY and o[3] >= window:
+            prev = [c for j, c in waited.items() if j < i]
+            assert prev and max(prev) == o[3] - window, (o, prev[-3:])
+
+
+def test_host_wait_names_the_record_of_its_chunk(L):
+    # A host wait takes the last record of its event at the time of the wait: that
+    # record must be the one made for the chunk the wait names.
+    for depth, mode in ((2, FUSED), (8, FUSED), (0, FUSED), (2, EAGER), (8, EAGER), (3, OTP)):
+        ops = plan(L, 200 * MiB, MiB, 8 * MiB, depth, mode)
+        last_record = {}
+        k = -1   # the chunk whose operations are being enqueued
+        for o in ops:
+            if o[0] == COPY:
+                k = o[3]
+            if o[0] == RECORD:
+                last_record[o[2]] = k
+            if o[0] == HOST_WAIT:
+                assert last_record[o[2]] == o[3], (depth, mode, o, last_record[o[2]])
+
+
+def test_direct_plan(L):
+    ops = plan(L, 64 * MiB + 16, MiB, 8 * MiB, 0, DIRECT_MODE)
+    assert [o[0] for o in ops] == [META, RECORD, WAIT, DIRECT]
+    assert ops[2][1] == 1 and ops[3][1] == 1
+
+
 def test_plan_rejects_what_the_pipeline_rejects(L):
     for args in ((64 * MiB, MiB, 3 * MiB // 2, 2, FUSED), (64 * MiB, MiB, 8 * MiB, 1, FUSED),
                  (64 * MiB, MiB, 8 * MiB, 0, EAGER), (64 * MiB, MiB, 8 * MiB, 0, OTP),
-                 (64 * MiB, MiB, 8 * MiB, 9, FUSED), (64 * MiB, MiB, 8 * MiB, 2, 3), (64 * MiB, 0, 8 * MiB, 2, FUSED)):
+                 (64 * MiB, MiB, 8 * MiB, 9, FUSED), (64 * MiB, MiB, 8 * MiB, 2, DIRECT_MODE),
+                 (64 * MiB, MiB, 8 * MiB, 0, 4), (64 * MiB, 0, 8 * MiB, 2, FUSED)):
         assert L.fastrack_pipeline_plan(*args, None, 0) == -1, args
     assert L.fastrack_pipeline_plan(0, MiB, 8 * MiB, 2, FUSED, None, 0) == 0
