@@ -48,6 +48,8 @@ def main():
     ap.add_argument("--skip-pipeline", action="store_true")
     ap.add_argument("--skip-cpu", action="store_true")
     ap.add_argument("--skip-extras", action="store_true", help="only the timed decrypt sweep")
+    ap.add_argument("--pipeline-only", action="store_true",
+                    help="only the 4 GiB pipeline leg; prints its results as one JSON line (for tracing)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the path is per-GPU and shards by whole chains with no exchange "
@@ -67,6 +69,9 @@ def main():
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
+    if args.pipeline_only:
+        print(json.dumps(pipeline(F, W, torch, np, dev)), flush=True)
+        return
 
     # ---------------- inputs (config: image batch, chain sweep) ----------------
     w = W.config2()
