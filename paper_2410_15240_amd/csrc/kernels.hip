@@ -156,7 +156,7 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
     }
 
     // 8-bit positional tables of H^16, H^32, H^64:
-    // g8[i][k][v] = (byte v at byte k) . H^(16 << i), v's bit 7 = degree 8k.
+    // g16[i][v][k] = (byte v at byte k) . H^(16 << i), v's bit 7 = degree 8k.
     if (tid < 3 * 128)
         s_basis[tid >> 7][tid & 127] = be_mul_xk_any(to_be(s_hp[16 << (tid >> 7)]), tid & 127);
     __syncthreads();
@@ -168,7 +168,7 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
                 e = xor4(e, s_basis[i][8 * k + b]);
         const u4 le = from_be(e);
         for (int j = 0; j < 4; ++j)
-            ctx->g8[i][k][v][j] = le.w[j];
+            ctx->g16[i][v][k][j] = le.w[j];
     }
 }
 
@@ -264,11 +264,13 @@ __device__ __forceinline__ ItemPos item_pos(const GcmLaunch &p, uint64_t item)
 // The streaming kernel
 // ===========================================================================
 //
-// LDS layout (160 KiB, one 1024-thread workgroup per CU):
+// LDS layout (152 KiB + 64 B, one 1024-thread workgroup per CU):
 //   [0, 64 KiB)        row x (256 B) = T0[x] for lanes 0..31 | T1[x] for lanes 0..31
-//   [64, 112 KiB)      4-bit tables of H^(2^t), t = 0..5 (8 KiB each): the lane-combine tree
-//   [112 KiB, +64 B)   per-wave progress counters (see the priority steps in the kernel)
-//   [128, 160 KiB)     positions 0..7 of the 8-bit table of H^L: entry (k, v) at 128 KiB + (k*256 + v)*16
+//   [64, 128 KiB)      the 8-bit table of H^L: entry (k, v) at 64 KiB + (v*16 + k)*16
+//   [128, 152 KiB)     4-bit tables of H^(2^t), t = 0..2 (8 KiB each): the first levels of
+//                      the lane-combine tree (levels 3..5, with at most four active lanes
+//                      per item, read the key's tables in global memory)
+//   [152 KiB, +64 B)   per-wave progress counters (see the priority steps in the kernel)
 // T_r[x] = rotl(T0[x], 8r), so T2[x] = rotl16(T0[x]) and T3[x] = rotl16(T1[x]): a
 // round column T0[a] ^ T1[b] ^ T2[c] ^ T3[d] ^ k is T0[a] ^ T1[b] ^ rotl16(T0[c] ^
 // T1[d] ^ rotl16(k)), one rotate more than with four tables, and the 64 KiB saved
@@ -276,21 +278,25 @@ __device__ __forceinline__ ItemPos item_pos(const GcmLaunch &p, uint64_t item)
 // serves a wave's 32-bit reads 32 lanes at a time, so the 32 copies make every
 // lookup conflict-free. A T0/T1 address is one v_perm_b32: byte 0 = (lane%32)*4 +
 // 128*table, byte 1 = the state byte, bytes 2..3 = 0.
-// GHASH multiplies by H^L with the byte positions 8..15 folded onto 0..7: the
-// entry for byte position k+8 is the entry for position k times x^64, so
-//   X . H^L = sum_{k<8} E_k[x_k]  xor  (sum_{k<8} E_k[x_(k+8)]) . x^64.
+// GHASH multiplies by H^L as X . H^L = sum_k E_k[x_k] over the 16 byte positions k.
+// The 16 entries of one byte value sit side by side in a 256-byte row, so position
+// k lies in the k-th 16-byte bank group. The LDS serves a wave's 16-byte reads 16
+// lanes at a time; lane l takes position k = j xor (l mod 16) at lookup j, so the 16
+// lanes served together always hit 16 different bank groups, whatever the data.
 
 constexpr int kThreads = kGcmThreads;
 constexpr int kWavesPerWg = kGcmWavesPerWg;
-constexpr uint32_t kLdsBytes = 160 * 1024;
-constexpr uint32_t kG8Base = 8192;           // uint4 index of the GHASH table in LDS
 constexpr int kTreeTabs = 6;                 // H^(2^t), t = 0..5: lanes per item up to 64
-constexpr uint32_t kTreeBase = 4096;         // uint4 index of the tree tables (64 KiB)
-// Modes without data AES: the GHASH table, T0 (for the J0 masks) and the tree tables.
-constexpr uint32_t kTreeBaseGhashOnly = 2112;   // 33 KiB
-constexpr uint32_t kLdsGhashOnly = (33 + 8 * kTreeTabs) * 1024 + 64;
-// Per-wave progress counters (16 words): at 112 KiB, or the last 64 B of the GHASH-only layout.
-constexpr uint32_t kProgBase = 112 * 1024 / 4;
+constexpr int kTreeLds = 3;                  // of which levels 0..2 in LDS (the AES modes)
+constexpr uint32_t kGhBase = 4096;           // uint4 index of the GHASH table (64 KiB)
+constexpr uint32_t kTreeBase = 8192;         // uint4 index of the tree tables (128 KiB)
+constexpr uint32_t kLdsBytes = (128 + 8 * kTreeLds) * 1024 + 64;
+// Modes without data AES: the GHASH table, T0 (for the J0 masks) and all six tree tables.
+constexpr uint32_t kT0GhashOnly = 4096;         // uint4 index: 64 KiB
+constexpr uint32_t kTreeBaseGhashOnly = 4160;   // 65 KiB
+constexpr uint32_t kLdsGhashOnly = (65 + 8 * kTreeTabs) * 1024 + 64;
+// Per-wave progress counters (16 words): the last 64 B of either layout.
+constexpr uint32_t kProgBase = kLdsBytes / 4 - 16;
 constexpr uint32_t kProgBaseGhashOnly = kLdsGhashOnly / 4 - 16;
 
 
@@ -339,23 +345,6 @@ __device__ __forceinline__ uint32_t lane_down(uint32_t x)
         static_assert(D == 32, "shift of 1..8, 16 or 32 lanes");
         return __builtin_amdgcn_permlane32_swap(x, x, false, false)[1];
     }
-}
-
-// Y . x^64 in little-endian-word form: bytes 0..7 move to bytes 8..15 and the
-// bytes that pass degree 127, F, come back as F . (1 + x + x^2 + x^7).
-__device__ __forceinline__ u4 mul_x64(const u4 &y)
-{
-    const uint32_t fh = bswap32(y.w[2]), fl = bswap32(y.w[3]);   // F big-endian: degree d at bit 63-d
-    const uint32_t rh = xor3(fh, fh >> 1, xor3(fh >> 2, fh >> 7, 0u));
-    const uint32_t rl = xor3(fl, __builtin_amdgcn_alignbit(fh, fl, 1),
-                             xor3(__builtin_amdgcn_alignbit(fh, fl, 2), __builtin_amdgcn_alignbit(fh, fl, 7), 0u));
-    const uint32_t ro = xor3(fl << 31, fl << 30, fl << 25);      // degrees 64..70 of F . R
-    u4 r;
-    r.w[0] = bswap32(rh);
-    r.w[1] = bswap32(rl);
-    r.w[2] = y.w[0] ^ bswap32(ro);
-    r.w[3] = y.w[1];
-    return r;
 }
 
 // X . Y where the L = 2^LL lanes of each aligned lane group hold one X (the
@@ -481,29 +470,49 @@ __device__ inline u4 aes_block_lds(const char *lds, const uint32_t *rk, const u4
 
 // acc . H^L xor g with the 8-bit table of H^L in LDS: byte positions 0..7
 // directly, 8..15 through x^64.
-__device__ __forceinline__ u4 ghash_step(const uint4 *g8, const u4 &acc, const u4 &g)
+// The lane constants of the GHASH lookups: l = lane mod 16.
+struct GhLane {
+    uint32_t sel;   // v_perm selector: byte b <- byte b xor (l mod 4) of this word (l & 4: of the paired word)
+    uint32_t row;   // (l << 4) | the table's LDS byte address
+    bool swap;      // l & 8: words 0,1 <-> 2,3
+};
+
+__device__ __forceinline__ GhLane ghash_lane(uint32_t lane, uint32_t table_bytes)
 {
-    u4 lo = g, hi = zero4();
+    const uint32_t l = lane & 15;
+    GhLane k;
+    k.sel = 0u;
+    for (uint32_t b = 0; b < 4; ++b)
+        k.sel |= ((b ^ (l & 3)) + (l & 4)) << (8 * b);
+    k.row = (l << 4) | table_bytes;
+    k.swap = (l & 8) != 0;
+    return k;
+}
+
+// Horner step acc . H^L xor g: the bytes of acc are permuted so that byte j of p is
+// byte j xor l of acc; lookup j then reads position j xor l, whose entry for value
+// v is at row v, column (j xor l) of the table: address (v << 8 | row) xor (j << 4).
+__device__ __forceinline__ u4 ghash_step(const char *lds, const u4 &acc, const u4 &g, const GhLane &k)
+{
+    uint32_t q[4];
 #pragma unroll
-    for (int kb = 0; kb < 8; kb += 2) {
-        const uint32_t a0 = (acc.w[kb >> 2] >> (8 * (kb & 3))) & 0xFFu;
-        const uint32_t a1 = (acc.w[kb >> 2] >> (8 * ((kb + 1) & 3))) & 0xFFu;
-        const uint32_t b0 = (acc.w[2 + (kb >> 2)] >> (8 * (kb & 3))) & 0xFFu;
-        const uint32_t b1 = (acc.w[2 + (kb >> 2)] >> (8 * ((kb + 1) & 3))) & 0xFFu;
-        const uint4 ea = g8[(kb << 8) | a0];
-        const uint4 eb = g8[((kb + 1) << 8) | a1];
-        const uint4 fa = g8[(kb << 8) | b0];
-        const uint4 fb = g8[((kb + 1) << 8) | b1];
-        lo.w[0] = xor3(lo.w[0], ea.x, eb.x);
-        lo.w[1] = xor3(lo.w[1], ea.y, eb.y);
-        lo.w[2] = xor3(lo.w[2], ea.z, eb.z);
-        lo.w[3] = xor3(lo.w[3], ea.w, eb.w);
-        hi.w[0] = xor3(hi.w[0], fa.x, fb.x);
-        hi.w[1] = xor3(hi.w[1], fa.y, fb.y);
-        hi.w[2] = xor3(hi.w[2], fa.z, fb.z);
-        hi.w[3] = xor3(hi.w[3], fa.w, fb.w);
+    for (int w = 0; w < 4; ++w)
+        q[w] = __builtin_amdgcn_perm(acc.w[w ^ 1], acc.w[w], k.sel);
+    const uint32_t p[4] = {k.swap ? q[2] : q[0], k.swap ? q[3] : q[1], k.swap ? q[0] : q[2], k.swap ? q[1] : q[3]};
+    u4 r = g;
+#pragma unroll
+    for (int j = 0; j < 16; j += 2) {
+        // byte j of p into bits 8..15 (v_perm selector 0x0C: a zero byte)
+        const uint32_t v0 = __builtin_amdgcn_perm(0u, p[j >> 2], 0x0C0C000Cu | ((uint32_t)(j & 3) << 8));
+        const uint32_t v1 = __builtin_amdgcn_perm(0u, p[(j + 1) >> 2], 0x0C0C000Cu | ((uint32_t)((j + 1) & 3) << 8));
+        const uint4 ea = *reinterpret_cast<const uint4 *>(lds + ((v0 | k.row) ^ ((uint32_t)j << 4)));
+        const uint4 eb = *reinterpret_cast<const uint4 *>(lds + ((v1 | k.row) ^ ((uint32_t)(j + 1) << 4)));
+        r.w[0] = xor3(r.w[0], ea.x, eb.x);
+        r.w[1] = xor3(r.w[1], ea.y, eb.y);
+        r.w[2] = xor3(r.w[2], ea.z, eb.z);
+        r.w[3] = xor3(r.w[3], ea.w, eb.w);
     }
-    return xor4(lo, mul_x64(hi));
+    return r;
 }
 
 // Lanes per item L = 2^LL. Item slot g of a wave (lanes g*L .. g*L+L-1) takes
@@ -529,9 +538,10 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
     constexpr uint32_t kLdsUse = kAes ? kLdsBytes : kLdsGhashOnly;
     __shared__ uint4 lds4[kLdsUse / 16];
     const char *lds = reinterpret_cast<const char *>(lds4);
-    const uint4 *g8 = lds4 + (kAes ? kG8Base : 0);
-    uint32_t *t0l = reinterpret_cast<uint32_t *>(lds4 + 2048);   // GHASH-only modes: T0 after the table
+    constexpr uint32_t kGh = kAes ? kGhBase : 0u;                     // uint4 index of the GHASH table
+    uint32_t *t0l = reinterpret_cast<uint32_t *>(lds4 + kT0GhashOnly);   // GHASH-only modes: T0 after the table
     constexpr uint32_t kTree = kAes ? kTreeBase : kTreeBaseGhashOnly;
+    constexpr int kTreeInLds = kAes ? kTreeLds : kTreeTabs;           // tree levels held in LDS
     const Tab4 *tree = reinterpret_cast<const Tab4 *>(lds4 + kTree);   // tree[t]: 4-bit table of H^(2^t)
     constexpr uint32_t kProg = kAes ? kProgBase : kProgBaseGhashOnly;
     const int tid = threadIdx.x;
@@ -565,22 +575,22 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
         if (tid < 16)
             reinterpret_cast<uint32_t *>(lds4)[kProg + tid] = 0u;
         if (kGhash) {   // all loads of the 32 KiB GHASH table and the tree tables first, then the stores
-            const uint4 *g = reinterpret_cast<const uint4 *>(c->g8[LL - 4]);
+            const uint4 *g = reinterpret_cast<const uint4 *>(c->g16[LL - 4]);
             const uint4 *sq = reinterpret_cast<const uint4 *>(c->sq_tab);
-            constexpr int kTreeU4 = kTreeTabs * (int)(sizeof(Tab4) / 16);
-            constexpr int kPer = (2048 + kThreads - 1) / kThreads;
+            constexpr int kTreeU4 = kTreeInLds * (int)(sizeof(Tab4) / 16);
+            constexpr int kPer = (4096 + kThreads - 1) / kThreads;
             constexpr int kPerT = (kTreeU4 + kThreads - 1) / kThreads;
             uint4 gv[kPer], tv[kPerT];
 #pragma unroll
             for (int r = 0; r < kPer; ++r)
-                gv[r] = g[min(tid + r * kThreads, 2047)];
+                gv[r] = g[min(tid + r * kThreads, 4095)];
 #pragma unroll
             for (int r = 0; r < kPerT; ++r)
                 tv[r] = sq[min(tid + r * kThreads, kTreeU4 - 1)];
 #pragma unroll
             for (int r = 0; r < kPer; ++r)
-                if (tid + r * kThreads < 2048)
-                    lds4[(kAes ? kG8Base : 0) + tid + r * kThreads] = gv[r];
+                if (tid + r * kThreads < 4096)
+                    lds4[kGh + tid + r * kThreads] = gv[r];
 #pragma unroll
             for (int r = 0; r < kPerT; ++r)
                 if (tid + r * kThreads < kTreeU4)
@@ -591,6 +601,7 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
 
     const uint32_t lb = (lane & 31) << 2;
     const uint32_t lc0 = lb, lc1 = lb | 0x80u;
+    const GhLane gk = ghash_lane(lane, kGh * 16);
     // The 60 round-key words are uniform: they stay in scalar registers (the XORs
     // take them as scalar operands), which keeps the kernel within the 128 VGPRs
     // that four waves per SIMD allow. Rounds 1..13 use them rotated by 16 bits (the
@@ -732,7 +743,7 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
             for (int k = kmin; k < 0; ++k) {
                 const int v = k * (int)L + (int)jl - pad;
                 const u4 g = v >= -na ? aad_block(aad_c, (uint32_t)(v + na), p.aad_bytes) : zero4();
-                acc = k == kmin ? g : ghash_step(g8, acc, g);
+                acc = k == kmin ? g : ghash_step(lds, acc, g, gk);
             }
         }
         // The lane's slot in iteration k: v = k L + jl - pad (below 0: a padding slot),
@@ -838,7 +849,7 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                 }
                 if ((int)k <= kmax && q.v < 0 && q.v >= -na)    // an AAD block in a padding slot
                     g = aad_block(aad_c, (uint32_t)(q.v + na), p.aad_bytes);
-                acc = (k == 0 && kmin == 0) ? g : ghash_step(g8, acc, g);
+                acc = (k == 0 && kmin == 0) ? g : ghash_step(lds, acc, g, gk);
             }
         };
         for (uint32_t k = 0; k < Ku; ++k) {
@@ -869,8 +880,7 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
             // for the tag). sum_j acc_j H^(L-1-j) is a tree over the lanes: level t folds
             // lane j + 2^t into lane j with the factor H^(2^t), every lane active at a
             // level reading the same LDS table; then one multiply by H^2 in lane 0.
-#pragma unroll 1
-            for (uint32_t lv = 0; lv < (uint32_t)LL; ++lv) {
+            auto fold_in = [&](uint32_t lv) {   // lane j takes lane j + 2^lv's sum
                 u4 right;
                 for (int w = 0; w < 4; ++w) {
                     const uint32_t x = acc.w[w];
@@ -883,8 +893,21 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                     default: right.w[w] = lane_down<32>(x); break;
                     }
                 }
+                return right;
+            };
+            constexpr uint32_t kLvLds = (uint32_t)LL < (uint32_t)kTreeInLds ? (uint32_t)LL : (uint32_t)kTreeInLds;
+#pragma unroll 1
+            for (uint32_t lv = 0; lv < kLvLds; ++lv) {
+                const u4 right = fold_in(lv);
                 if ((jl & ((2u << lv) - 1)) == 0)
                     acc = xor4(mul_tab4_b8(acc, &tree[lv]), right);
+            }
+            // levels past those in LDS (at most four active lanes): the key's tables in global memory
+#pragma unroll 1
+            for (uint32_t lv = kLvLds; lv < (uint32_t)LL; ++lv) {
+                const u4 right = fold_in(lv);
+                if ((jl & ((2u << lv) - 1)) == 0)
+                    acc = xor4(mul_tab4_b4(acc, &c->sq_tab[lv]), right);
             }
             if (jl == 0)
                 acc = mul_tab4_b8(acc, &tree[1]);

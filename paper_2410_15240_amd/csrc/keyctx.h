@@ -37,8 +37,9 @@ struct KeyCtx {
     Tab4 h1_tab;                // table of H
     Tab4 sq_tab[kSquares];      // sq_tab[t]: table of H^(2^t) (t = 0..5 also combine the lanes of an item)
     // 8-bit positional tables of the Horner multipliers H^16, H^32 and H^64 (lanes per
-    // chain 16, 32, 64): g8[i][k][v] = (byte v at byte k) . H^(16 << i)
-    uint32_t g8[3][16][256][4];
+    // chain 16, 32, 64), the 16 byte positions of one value side by side:
+    // g16[i][v][k] = (byte v at byte k) . H^(16 << i)
+    uint32_t g16[3][256][16][4];
 };
 
 }  // namespace fastrack
