@@ -140,27 +140,28 @@ __device__ inline u4 mul_tab4_b8(const u4 &x, const Tab4 *__restrict__ t)
     return z;
 }
 
-// The same product from a table in global memory, four lookups in flight per batch:
-// for the few lanes of the last levels of a lane combine (a few registers, since
-// it runs where the rest of the kernel's state is still live).
-__device__ inline u4 mul_tab4_b4(const u4 &x, const Tab4 *__restrict__ t)
+// X . Y with Y's 8-bit positional table in global memory, entry (byte position k,
+// value v) at t[v * 16 + k], the 16 lookups in two batches of eight: for the few
+// lanes of the last levels of a lane combine.
+__device__ inline u4 mul_tab8_b8(const u4 &x, const uint4 *__restrict__ t)
 {
     u4 z = {{0u, 0u, 0u, 0u}};
 #pragma unroll
-    for (int h = 0; h < 8; ++h) {
-        const uint32_t w = x.w[h >> 1];
-        uint4 e[4];
+    for (int h = 0; h < 2; ++h) {
+        uint4 e[8];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int pos = 4 * h + q;   // nibble position: byte 4j+b holds 8j+2b (high), 8j+2b+1 (low)
-            const uint32_t byte = (w >> (8 * ((pos & 7) >> 1))) & 0xFFu;
-            const uint32_t nib = (pos & 1) ? (byte & 0xFu) : (byte >> 4);
-            e[q] = *reinterpret_cast<const uint4 *>(t->e[pos][nib]);
+        for (int q = 0; q < 8; ++q) {
+            const int k = 8 * h + q;
+            const uint32_t v = (x.w[k >> 2] >> (8 * (k & 3))) & 0xFFu;
+            e[q] = t[v * 16 + k];
         }
-        z.w[0] = xor3(z.w[0], e[0].x, e[1].x ^ e[2].x ^ e[3].x);
-        z.w[1] = xor3(z.w[1], e[0].y, e[1].y ^ e[2].y ^ e[3].y);
-        z.w[2] = xor3(z.w[2], e[0].z, e[1].z ^ e[2].z ^ e[3].z);
-        z.w[3] = xor3(z.w[3], e[0].w, e[1].w ^ e[2].w ^ e[3].w);
+#pragma unroll
+        for (int q = 0; q < 8; q += 2) {
+            z.w[0] = xor3(z.w[0], e[q].x, e[q + 1].x);
+            z.w[1] = xor3(z.w[1], e[q].y, e[q + 1].y);
+            z.w[2] = xor3(z.w[2], e[q].z, e[q + 1].z);
+            z.w[3] = xor3(z.w[3], e[q].w, e[q + 1].w);
+        }
         __builtin_amdgcn_sched_barrier(0);
     }
     return z;

@@ -76,7 +76,7 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
     __shared__ uint32_t s_rk[60];
     __shared__ u4 s_hp[kMaxPow + 2];
     __shared__ u4 s_hsq[kSquares];
-    __shared__ u4 s_basis[3][128];
+    __shared__ u4 s_basis[4][128];
     __shared__ Tab4 s_tab;
     const int tid = threadIdx.x;
 
@@ -155,12 +155,12 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
             build_tab4_row(s_hsq[tbl - 1], p, &ctx->sq_tab[tbl - 1]);
     }
 
-    // 8-bit positional tables of H^16, H^32, H^64:
-    // g16[i][v][k] = (byte v at byte k) . H^(16 << i), v's bit 7 = degree 8k.
-    if (tid < 3 * 128)
-        s_basis[tid >> 7][tid & 127] = be_mul_xk_any(to_be(s_hp[16 << (tid >> 7)]), tid & 127);
+    // 8-bit positional tables of H^8, H^16, H^32, H^64:
+    // g16[i][v][k] = (byte v at byte k) . H^(8 << i), v's bit 7 = degree 8k.
+    if (tid < 4 * 128)
+        s_basis[tid >> 7][tid & 127] = be_mul_xk_any(to_be(s_hp[8 << (tid >> 7)]), tid & 127);
     __syncthreads();
-    for (int ent = tid; ent < 3 * 16 * 256; ent += blockDim.x) {
+    for (int ent = tid; ent < 4 * 16 * 256; ent += blockDim.x) {
         const int i = ent >> 12, k = (ent >> 8) & 15, v = ent & 255;
         u4 e = {{0u, 0u, 0u, 0u}};
         for (int b = 0; b < 8; ++b)
@@ -406,10 +406,18 @@ __device__ inline LenTerms len_terms(const GcmLaunch &p, const Tab4 *h1, uint32_
     const uint32_t nib = (pos & 1) ? (byte & 0xFu) : (byte >> 4);
     const uint4 e = *reinterpret_cast<const uint4 *>(h1->e[pos][nib]);
     u4 r = {{e.x, e.y, e.z, e.w}};
-#pragma unroll
-    for (int off = 16; off >= 1; off >>= 1)
-        for (int w = 0; w < 4; ++w)
-            r.w[w] ^= __shfl_xor(r.w[w], off, 64);
+    // XOR over lanes 0..31 into lane 0 and 32..63 into lane 32 with VALU cross-lane
+    // moves (DPP row shifts, the half-row swap): no LDS round trips, which queue
+    // behind the table reads of the waves already streaming
+    for (int w = 0; w < 4; ++w) {
+        uint32_t x = r.w[w];
+        x ^= lane_down<16>(x);
+        x ^= lane_down<8>(x);
+        x ^= lane_down<4>(x);
+        x ^= lane_down<2>(x);
+        x ^= lane_down<1>(x);
+        r.w[w] = x;
+    }
     LenTerms t;
     for (int w = 0; w < 4; ++w) {
         t.full.w[w] = __builtin_amdgcn_readlane(r.w[w], 0);
@@ -575,7 +583,7 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
         if (tid < 16)
             reinterpret_cast<uint32_t *>(lds4)[kProg + tid] = 0u;
         if (kGhash) {   // all loads of the 32 KiB GHASH table and the tree tables first, then the stores
-            const uint4 *g = reinterpret_cast<const uint4 *>(c->g16[LL - 4]);
+            const uint4 *g = reinterpret_cast<const uint4 *>(c->g16[LL - 3]);
             const uint4 *sq = reinterpret_cast<const uint4 *>(c->sq_tab);
             constexpr int kTreeU4 = kTreeInLds * (int)(sizeof(Tab4) / 16);
             constexpr int kPer = (4096 + kThreads - 1) / kThreads;
@@ -902,12 +910,13 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                 if ((jl & ((2u << lv) - 1)) == 0)
                     acc = xor4(mul_tab4_b8(acc, &tree[lv]), right);
             }
-            // levels past those in LDS (at most four active lanes): the key's tables in global memory
+            // levels past those in LDS (at most four active lanes): the key's 8-bit tables
+            // of H^8, H^16, H^32 in global memory, half the lookups of a 4-bit table
 #pragma unroll 1
             for (uint32_t lv = kLvLds; lv < (uint32_t)LL; ++lv) {
                 const u4 right = fold_in(lv);
                 if ((jl & ((2u << lv) - 1)) == 0)
-                    acc = xor4(mul_tab4_b4(acc, &c->sq_tab[lv]), right);
+                    acc = xor4(mul_tab8_b8(acc, reinterpret_cast<const uint4 *>(c->g16[lv - 3])), right);
             }
             if (jl == 0)
                 acc = mul_tab4_b8(acc, &tree[1]);
