@@ -347,6 +347,58 @@ __device__ __forceinline__ uint32_t lane_down(uint32_t x)
     }
 }
 
+// Wave-wide maximum / minimum, returned uniform: VALU cross-lane moves folding
+// every lane into lane 0 (no LDS permutes, which queue behind the table reads of
+// the waves already streaming). All lanes must be active.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x)
+{
+    x = max(x, lane_down<32>(x));
+    x = max(x, lane_down<16>(x));
+    x = max(x, lane_down<8>(x));
+    x = max(x, lane_down<4>(x));
+    x = max(x, lane_down<2>(x));
+    x = max(x, lane_down<1>(x));
+    return __builtin_amdgcn_readlane(x, 0);
+}
+
+__device__ __forceinline__ int wave_min_i32(int x)
+{
+    x = min(x, (int)lane_down<32>((uint32_t)x));
+    x = min(x, (int)lane_down<16>((uint32_t)x));
+    x = min(x, (int)lane_down<8>((uint32_t)x));
+    x = min(x, (int)lane_down<4>((uint32_t)x));
+    x = min(x, (int)lane_down<2>((uint32_t)x));
+    x = min(x, (int)lane_down<1>((uint32_t)x));
+    return (int)__builtin_amdgcn_readlane((uint32_t)x, 0);
+}
+
+// XOR of x over each aligned group of 2^LL lanes, in every lane of the group: a
+// butterfly of VALU moves. Quad permutes pair lanes 1 and 2 apart; once each quad
+// (eight) holds one sum, the half-row (row) mirror pairs it with the neighbouring
+// quad (eight); the half-row and half-wave swaps return both halves, whose XOR is
+// a lane's own value xor its partner's.
+template <int LL>
+__device__ __forceinline__ uint32_t group_xor_sum(uint32_t x)
+{
+    if constexpr (LL >= 1)
+        x ^= __builtin_amdgcn_update_dpp(0u, x, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
+    if constexpr (LL >= 2)
+        x ^= __builtin_amdgcn_update_dpp(0u, x, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
+    if constexpr (LL >= 3)
+        x ^= __builtin_amdgcn_update_dpp(0u, x, 0x141, 0xF, 0xF, false);  // row_half_mirror
+    if constexpr (LL >= 4)
+        x ^= __builtin_amdgcn_update_dpp(0u, x, 0x140, 0xF, 0xF, false);  // row_mirror
+    if constexpr (LL >= 5) {
+        const auto sw = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+        x = sw[0] ^ sw[1];
+    }
+    if constexpr (LL >= 6) {
+        const auto sw = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+        x = sw[0] ^ sw[1];
+    }
+    return x;
+}
+
 // X . Y where the L = 2^LL lanes of each aligned lane group hold one X (the
 // groups may differ) and t points to Y's 4-bit table (it may differ per group
 // as well): lane j of a group looks up the nibble positions j, j + L, ... < 32
@@ -369,10 +421,8 @@ __device__ inline u4 group_mul_tab4(const u4 &x, const Tab4 *__restrict__ t, uin
             r.w[0] ^= e.x; r.w[1] ^= e.y; r.w[2] ^= e.z; r.w[3] ^= e.w;
         }
     }
-#pragma unroll
-    for (uint32_t off = L / 2; off >= 1; off >>= 1)
-        for (int w = 0; w < 4; ++w)
-            r.w[w] ^= __shfl_xor(r.w[w], off, 64);
+    for (int w = 0; w < 4; ++w)
+        r.w[w] = group_xor_sum<LL>(r.w[w]);
     return r;
 }
 
@@ -691,11 +741,7 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
         // the longest of the wave's segments (shorter ones are padded in front).
         uint32_t Ku = Ku_uniform;
         if constexpr (RAG) {
-            uint32_t ku = valid ? (ip.e - ip.b + L - 1) >> LL : 0u;
-#pragma unroll
-            for (int off = 32; off >= 1; off >>= 1)
-                ku = max(ku, (uint32_t)__shfl_xor((int)ku, off, 64));
-            Ku = __builtin_amdgcn_readfirstlane(ku);
+            Ku = wave_max_u32(valid ? (ip.e - ip.b + L - 1) >> LL : 0u);
         }
         uint32_t iv[3];
         chain_iv(p, gchain, iv);
@@ -733,14 +779,8 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                 k_hi = -1;
             }
         }
-        int kmin = k_lo < 0 ? k_lo : 0, kmax = k_hi;
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) {
-            kmin = min(kmin, __shfl_xor(kmin, off, 64));
-            kmax = max(kmax, __shfl_xor(kmax, off, 64));
-        }
-        kmin = __builtin_amdgcn_readfirstlane(kmin);
-        kmax = __builtin_amdgcn_readfirstlane(kmax);
+        const int kmin = wave_min_i32(k_lo < 0 ? k_lo : 0);
+        const int kmax = (int)wave_max_u32((uint32_t)(k_hi + 1)) - 1;   // k_hi >= -1
         u4 acc = zero4();
         if (kmin == -1) {
             // One extra iteration (at most L AAD blocks in front): its blocks seed the
@@ -922,7 +962,7 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                 acc = mul_tab4_b8(acc, &tree[1]);
             if (SPLIT)   // the segment weights below take the sum in every lane of the group
                 for (int w = 0; w < 4; ++w)
-                    acc.w[w] = __shfl(acc.w[w], (int)(lane - jl), 64);
+                    acc.w[w] = LL == 6 ? __builtin_amdgcn_readlane(acc.w[w], 0) : __shfl(acc.w[w], (int)(lane - jl), 64);
             if (SPLIT) {
                 // A chain cut into S segments: segment s carries the weight
                 // H^((S-1-s) . 2^seg_log2) inside its chain, one multiply by a
@@ -930,11 +970,7 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                 // item's lanes. The partials and segment 0's mask go to memory; the
                 // chain kernel sums them.
                 uint32_t m = valid ? ip.S - 1 - ip.s : 0u;
-                uint32_t rounds = __popc(m);
-#pragma unroll
-                for (int off = 32; off >= 1; off >>= 1)
-                    rounds = max(rounds, (uint32_t)__shfl_xor((int)rounds, off, 64));
-                rounds = __builtin_amdgcn_readfirstlane(rounds);
+                const uint32_t rounds = wave_max_u32(__popc(m));
                 for (uint32_t r = 0; r < rounds; ++r) {
                     const uint32_t b = m ? (uint32_t)__builtin_ctz(m) : 0u;
                     const u4 prod = group_mul_tab4<LL>(acc, &c->sq_tab[p.seg_log2 + b], jl);
@@ -945,8 +981,8 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                 }
                 const uint32_t src_lane = bi * G + gs;
                 u4 e;
-                for (int w = 0; w < 4; ++w)
-                    e.w[w] = __shfl(jmask.w[w], (int)src_lane, 64);
+                for (int w = 0; w < 4; ++w)   // one item per wave: the mask's lane bi is uniform
+                    e.w[w] = LL == 6 ? __builtin_amdgcn_readlane(jmask.w[w], bi) : __shfl(jmask.w[w], (int)src_lane, 64);
                 if (valid && jl == 0) {
                     p.partials[item] = make_uint4(acc.w[0], acc.w[1], acc.w[2], acc.w[3]);
                     if (ip.s == 0)
@@ -957,7 +993,7 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                 // T = GHASH(A || C) . H xor L . H xor AES_K(J0).
                 u4 e;
                 for (int w = 0; w < 4; ++w)
-                    e.w[w] = __shfl(jmask.w[w], (int)(bi * G + gs), 64);
+                    e.w[w] = LL == 6 ? __builtin_amdgcn_readlane(jmask.w[w], bi) : __shfl(jmask.w[w], (int)(bi * G + gs), 64);
                 if (valid && jl == 0)
                     emit_tag<ENC>(p, gchain, xor4(acc, e), got);
             }
