@@ -353,6 +353,8 @@ int run_gcm(bool encrypt, GcmMode mode, const KeyCtx *ctx, const uint8_t *base_i
     GcmLaunch p;
     std::memset(&p, 0, sizeof p);
     make_plan(len, chain_bytes, chain_base, (uint64_t)num_cu * kGcmWavesPerWg * gcm_wgs_per_cu(mode), p);
+    if (p.n_items > 0xFFFFFFFFull)   // the kernel indexes a launch's items in 32 bits
+        return fail(FASTRACK_EINVAL, "more than 2^32-1 work items in one launch");
     p.ctx = ctx;
     p.in = in;
     p.ks = ks;

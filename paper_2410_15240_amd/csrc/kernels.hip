@@ -245,8 +245,9 @@ __device__ __forceinline__ ItemPos item_pos(const GcmLaunch &p, uint64_t item)
         r.len = rc.len;
         r.tail = (uint32_t)(rc.len & 15);
     } else {
-        r.chain = (uint32_t)(item / p.segs_full);
-        r.s = (uint32_t)(item - (uint64_t)r.chain * p.segs_full);
+        const uint32_t it32 = (uint32_t)item;   // the host keeps a launch's items below 2^32
+        r.chain = it32 / p.segs_full;
+        r.s = it32 - r.chain * p.segs_full;
         const bool last = r.chain == p.n_chains - 1;
         r.q = last ? p.q_last : p.qc;
         r.S = last ? p.segs_last : p.segs_full;
