@@ -76,7 +76,7 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
     __shared__ uint32_t s_rk[60];
     __shared__ u4 s_hp[kMaxPow + 2];
     __shared__ u4 s_hsq[kSquares];
-    __shared__ u4 s_basis[4][128];
+    __shared__ u4 s_basis[8][128];
     __shared__ Tab4 s_tab;
     const int tid = threadIdx.x;
 
@@ -155,12 +155,12 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
             build_tab4_row(s_hsq[tbl - 1], p, &ctx->sq_tab[tbl - 1]);
     }
 
-    // 8-bit positional tables of H^8, H^16, H^32, H^64:
-    // g16[i][v][k] = (byte v at byte k) . H^(8 << i), v's bit 7 = degree 8k.
-    if (tid < 4 * 128)
-        s_basis[tid >> 7][tid & 127] = be_mul_xk_any(to_be(s_hp[8 << (tid >> 7)]), tid & 127);
+    // 8-bit positional tables of H^8, H^16, ..., H^64:
+    // g16[i][v][k] = (byte v at byte k) . H^(8 (i + 1)), v's bit 7 = degree 8k.
+    for (int b = tid; b < 8 * 128; b += blockDim.x)
+        s_basis[b >> 7][b & 127] = be_mul_xk_any(to_be(s_hp[8 * ((b >> 7) + 1)]), b & 127);
     __syncthreads();
-    for (int ent = tid; ent < 4 * 16 * 256; ent += blockDim.x) {
+    for (int ent = tid; ent < 8 * 16 * 256; ent += blockDim.x) {
         const int i = ent >> 12, k = (ent >> 8) & 15, v = ent & 255;
         u4 e = {{0u, 0u, 0u, 0u}};
         for (int b = 0; b < 8; ++b)
@@ -634,7 +634,7 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
         if (tid < 16)
             reinterpret_cast<uint32_t *>(lds4)[kProg + tid] = 0u;
         if (kGhash) {   // all loads of the 32 KiB GHASH table and the tree tables first, then the stores
-            const uint4 *g = reinterpret_cast<const uint4 *>(c->g16[LL - 3]);
+            const uint4 *g = reinterpret_cast<const uint4 *>(c->g16[(L >> 3) - 1]);
             const uint4 *sq = reinterpret_cast<const uint4 *>(c->sq_tab);
             constexpr int kTreeU4 = kTreeInLds * (int)(sizeof(Tab4) / 16);
             constexpr int kPer = (4096 + kThreads - 1) / kThreads;
@@ -951,13 +951,25 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                 if ((jl & ((2u << lv) - 1)) == 0)
                     acc = xor4(mul_tab4_b8(acc, &tree[lv]), right);
             }
-            // levels past those in LDS (at most four active lanes): the key's 8-bit tables
-            // of H^8, H^16, H^32 in global memory, half the lookups of a 4-bit table
-#pragma unroll 1
-            for (uint32_t lv = kLvLds; lv < (uint32_t)LL; ++lv) {
-                const u4 right = fold_in(lv);
-                if ((jl & ((2u << lv) - 1)) == 0)
-                    acc = xor4(mul_tab8_b8(acc, reinterpret_cast<const uint4 *>(c->g16[lv - 3])), right);
+            if constexpr (kTreeInLds == 3) {
+                // After the three LDS levels, lane 8m of an item holds the sum C_m of its
+                // eight-lane group m (of M = L/8). The remaining levels would multiply these
+                // by H^8, H^16, H^32 one level after another; instead lane 8m multiplies C_m
+                // by its own weight H^(8 (M-1-m)) from the key's 8-bit tables in global
+                // memory (all groups at once, one multiply's latency), and the M products
+                // are XOR-folded into lane 0 by VALU cross-lane moves.
+                constexpr uint32_t M = L >> 3;
+                const uint32_t m = jl >> 3;
+                if ((jl & 7u) == 0 && m + 1 < M)   // M = 2: one group multiplies, by H^8 (a uniform table)
+                    acc = mul_tab8_b8(acc, reinterpret_cast<const uint4 *>(c->g16[M == 2 ? 0u : M - 2 - m]));
+                if constexpr (LL >= 6)
+                    for (int w = 0; w < 4; ++w)
+                        acc.w[w] ^= lane_down<32>(acc.w[w]);
+                if constexpr (LL >= 5)
+                    for (int w = 0; w < 4; ++w)
+                        acc.w[w] ^= lane_down<16>(acc.w[w]);
+                for (int w = 0; w < 4; ++w)
+                    acc.w[w] ^= lane_down<8>(acc.w[w]);
             }
             if (jl == 0)
                 acc = mul_tab4_b8(acc, &tree[1]);

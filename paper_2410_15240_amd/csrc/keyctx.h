@@ -36,11 +36,11 @@ struct KeyCtx {
     uint32_t hsq[kSquares][4];        // hsq[t] = H^(2^t)
     Tab4 h1_tab;                // table of H
     Tab4 sq_tab[kSquares];      // sq_tab[t]: table of H^(2^t) (t = 0..5 also combine the lanes of an item)
-    // 8-bit positional tables of H^8, H^16, H^32 and H^64, the 16 byte positions of one
-    // value side by side: g16[i][v][k] = (byte v at byte k) . H^(8 << i). Entries 1..3
-    // are the Horner multipliers H^L of L = 16, 32, 64 lanes per chain; 0..2 also serve
-    // the last levels of the lane combine.
-    uint32_t g16[4][256][16][4];
+    // 8-bit positional tables of H^8, H^16, ..., H^64, the 16 byte positions of one value
+    // side by side: g16[i][v][k] = (byte v at byte k) . H^(8 (i + 1)). g16[L/8 - 1] is the
+    // Horner multiplier H^L of L = 16, 32, 64 lanes per chain; g16[0..6] also weight the
+    // partial sums of an item's eight-lane groups at the end of the lane combine.
+    uint32_t g16[8][256][16][4];
 };
 
 }  // namespace fastrack
