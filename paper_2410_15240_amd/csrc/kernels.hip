@@ -269,9 +269,10 @@ __device__ __forceinline__ ItemPos item_pos(const GcmLaunch &p, uint64_t item)
 //   [0, 64 KiB)        row x (256 B) = T0[x] for lanes 0..31 | T1[x] for lanes 0..31
 //   [64, 128 KiB)      the 8-bit table of H^L: entry (k, v) at 64 KiB + (v*16 + k)*16
 //   [128, 152 KiB)     4-bit tables of H^(2^t), t = 0..2 (8 KiB each): the first levels of
-//                      the lane-combine tree (levels 3..5, with at most four active lanes
-//                      per item, read the key's tables in global memory)
-//   [152 KiB, +64 B)   per-wave progress counters (see the priority steps in the kernel)
+//                      the lane-combine tree (the rest weights eight-lane group sums from
+//                      the key's tables in global memory)
+//   [152 KiB, +512 B)  per-wave segment partials and tag masks (workgroup tag combine)
+//   then 64 B          per-wave progress counters (see the priority steps in the kernel)
 // T_r[x] = rotl(T0[x], 8r), so T2[x] = rotl16(T0[x]) and T3[x] = rotl16(T1[x]): a
 // round column T0[a] ^ T1[b] ^ T2[c] ^ T3[d] ^ k is T0[a] ^ T1[b] ^ rotl16(T0[c] ^
 // T1[d] ^ rotl16(k)), one rotate more than with four tables, and the 64 KiB saved
@@ -291,7 +292,9 @@ constexpr int kTreeTabs = 6;                 // H^(2^t), t = 0..5: lanes per ite
 constexpr int kTreeLds = 3;                  // of which levels 0..2 in LDS (the AES modes)
 constexpr uint32_t kGhBase = 4096;           // uint4 index of the GHASH table (64 KiB)
 constexpr uint32_t kTreeBase = 8192;         // uint4 index of the tree tables (128 KiB)
-constexpr uint32_t kLdsBytes = (128 + 8 * kTreeLds) * 1024 + 64;
+constexpr uint32_t kWgTagBase = (128 + 8 * kTreeLds) * 1024 / 16;   // uint4 index: 16 partials, 16 masks
+static_assert(kWavesPerWg == 16, "one workgroup-combine slot per wave");
+constexpr uint32_t kLdsBytes = (128 + 8 * kTreeLds) * 1024 + 512 + 64;
 // Modes without data AES: the GHASH table, T0 (for the J0 masks) and all six tree tables.
 constexpr uint32_t kT0GhashOnly = 4096;         // uint4 index: 64 KiB
 constexpr uint32_t kTreeBaseGhashOnly = 4160;   // 65 KiB
@@ -697,6 +700,8 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
     const uint32_t wslot = (uint32_t)tid >> 6;
     const uint32_t pidx = (wslot & 3) * 4 + (wslot >> 2);
     uint32_t iters_done = 0;
+    // Workgroup tag combine (fused uniform launches of one item per wave).
+    constexpr bool kWgCombine = SPLIT && LL == 6 && MODE == kFused && !RAG;
     __builtin_amdgcn_s_setprio(3);
     for (uint64_t wi = wave; wi < n_wave_items; wi += nwaves, ++it) {
         const uint32_t bi = it & (L - 1);
@@ -735,8 +740,8 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
         const uint64_t gchain = p.chain_base + ip.chain;
         // A whole-chain item checks its tag at the end: fetch the received tag now.
         u4 got = zero4();
-        if constexpr (!ENC && !SPLIT && kGhash)
-            if (valid && jl == 0)
+        if constexpr (!ENC && kGhash)
+            if (valid && jl == 0 && (!SPLIT || (p.wg_tag && ip.s == 0)))
                 got = load16(p.tags_in + 16 * gchain);
         // Iterations of this wave-item: uniform for uniform chains; for ragged chains
         // the longest of the wave's segments (shorter ones are padded in front).
@@ -996,7 +1001,14 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                 u4 e;
                 for (int w = 0; w < 4; ++w)   // one item per wave: the mask's lane bi is uniform
                     e.w[w] = LL == 6 ? __builtin_amdgcn_readlane(jmask.w[w], bi) : __shfl(jmask.w[w], (int)src_lane, 64);
-                if (valid && jl == 0) {
+                if (kWgCombine && p.wg_tag) {   // the workgroup tags the chain after its barrier
+                    if (valid && jl == 0) {
+                        lds4[kWgTagBase + wslot] = make_uint4(acc.w[0], acc.w[1], acc.w[2], acc.w[3]);
+                        if (ip.s == 0)   // decrypt: the mask xor the received tag, so a good chain sums to 0
+                            lds4[kWgTagBase + 16 + wslot] = make_uint4(e.w[0] ^ got.w[0], e.w[1] ^ got.w[1],
+                                                                       e.w[2] ^ got.w[2], e.w[3] ^ got.w[3]);
+                    }
+                } else if (valid && jl == 0) {
                     p.partials[item] = make_uint4(acc.w[0], acc.w[1], acc.w[2], acc.w[3]);
                     if (ip.s == 0)
                         p.masks[ip.chain] = make_uint4(e.w[0], e.w[1], e.w[2], e.w[3]);
@@ -1014,6 +1026,25 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
     }
     if (lane == 0)   // a finished wave no longer holds the others of its SIMD back
         prog[pidx] = 0xFFFFFFFFu;
+    if constexpr (kWgCombine) {
+        // Every wave took exactly one item (the item index is the wave index) and a
+        // chain's S segments sit on waves w .. w+S-1 of this workgroup: the wave with
+        // segment 0 XORs their partials into its mask (decrypt: mask xor received tag,
+        // so the chain verifies when the sum is 0) and tags the chain.
+        if (p.wg_tag) {
+            __syncthreads();
+            const uint32_t chain = (uint32_t)wave / p.segs_full;
+            if ((uint64_t)wave < p.n_items && (uint32_t)wave == chain * p.segs_full && lane == 0) {
+                const uint32_t S = chain == p.n_chains - 1 ? p.segs_last : p.segs_full;
+                uint4 m = lds4[kWgTagBase + 16 + wslot];
+                for (uint32_t s = 0; s < S; ++s) {
+                    const uint4 g = lds4[kWgTagBase + wslot + s];
+                    m.x ^= g.x; m.y ^= g.y; m.z ^= g.z; m.w ^= g.w;
+                }
+                emit_tag<ENC>(p, p.chain_base + chain, u4{{m.x, m.y, m.z, m.w}}, zero4());
+            }
+        }
+    }
 }
 
 // Chains cut into segments: T = mask xor the XOR of the chain's weighted
@@ -1114,20 +1145,25 @@ static hipError_t launch_mode(const GcmLaunch &p, int num_cu, hipStream_t s)
     if (wgs > (uint64_t)num_cu * gcm_wgs_per_cu(MODE))
         wgs = (uint64_t)num_cu * gcm_wgs_per_cu(MODE);
     const bool split = ghash && p.split;
+    // One item per wave with every chain's segments inside one workgroup: the
+    // workgroup tags the chains itself and the per-chain tag kernel is not needed.
+    GcmLaunch q = p;
+    q.wg_tag = MODE == kFused && !RAG && split && p.lanes_log2 == 6 && p.n_items == wgs * kWavesPerWg &&
+               p.segs_full <= (uint32_t)kWavesPerWg && kWavesPerWg % p.segs_full == 0;
     if (p.lanes_log2 == 4 && !split)
-        hipLaunchKernelGGL((gcm_kernel<ENC, 4, false, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+        hipLaunchKernelGGL((gcm_kernel<ENC, 4, false, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, q);
     else if (p.lanes_log2 == 4)
-        hipLaunchKernelGGL((gcm_kernel<ENC, 4, ghash, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+        hipLaunchKernelGGL((gcm_kernel<ENC, 4, ghash, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, q);
     else if (p.lanes_log2 == 5 && !split)
-        hipLaunchKernelGGL((gcm_kernel<ENC, 5, false, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+        hipLaunchKernelGGL((gcm_kernel<ENC, 5, false, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, q);
     else if (p.lanes_log2 == 5)
-        hipLaunchKernelGGL((gcm_kernel<ENC, 5, ghash, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+        hipLaunchKernelGGL((gcm_kernel<ENC, 5, ghash, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, q);
     else if (!split)
-        hipLaunchKernelGGL((gcm_kernel<ENC, 6, false, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+        hipLaunchKernelGGL((gcm_kernel<ENC, 6, false, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, q);
     else
-        hipLaunchKernelGGL((gcm_kernel<ENC, 6, ghash, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, p);
+        hipLaunchKernelGGL((gcm_kernel<ENC, 6, ghash, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, q);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || !ghash || !p.split)
+    if (e != hipSuccess || !ghash || !p.split || q.wg_tag)
         return e;
     constexpr uint32_t per_block = kTagThreads / 64;
     hipLaunchKernelGGL((chain_tag_kernel<ENC, RAG>), dim3((p.n_chains + per_block - 1) / per_block), dim3(kTagThreads),

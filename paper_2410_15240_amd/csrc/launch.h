@@ -79,6 +79,10 @@ struct GcmLaunch {
     uint4 *partials;
     uint4 *masks;
     uint32_t split;
+    // Fused launches whose every wave takes exactly one item, with each chain's
+    // segments on consecutive waves of one workgroup (a segment count dividing 16):
+    // the workgroup sums them in LDS and tags the chain itself (no second kernel).
+    uint32_t wg_tag;
     // Ragged launches (chains of their own lengths and offsets): the chain table
     // and each item's chain; chain_bytes, qc, last_len and the segs_* fields
     // are then unused. NULL for uniform chains.
