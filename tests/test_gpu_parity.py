@@ -157,6 +157,29 @@ def test_config4_gradients_encrypt(F):
     check_encrypt(F, w.key, w.base_iv, chain, w.payload, None, 0, label="config4")
 
 
+def test_workgroup_tag_combine_edges(F):
+    """64 KiB chains over 64 MiB - 16 KiB + 100 bytes: on 256 CUs the plan cuts the 1024
+    chains into 4 segments each (the short last chain, 48 KiB + 100 bytes with a partial
+    last block, also into 4), 4096 items for 4096 waves, so each chain is summed and tagged
+    inside its workgroup. Tampering in a middle segment, in the last partial block, in a tag
+    and in an AAD is rejected exactly; decrypt (also in place) and encrypt match the oracle."""
+    chain, length, abytes = 64 * KiB, 64 * MiB - 16 * KiB + 100, 32
+    say("workgroup tag combine edges")
+    w = W.random_case(88, length, chain, abytes)
+    aad = W.case_aad(w, chain)
+    n = aad.shape[0]
+    ct, tags = oracle.chains_encrypt(w.key, w.base_iv, chain, w.payload, aad, abytes)
+    bad, tg, ad = ct.copy(), tags.copy(), aad.copy()
+    W.flip_bit(bad, 8 * (5 * chain + 2 * 16 * KiB + 77))   # chain 5, segment 2
+    W.flip_bit(bad, 8 * (length - 1) + 3)                  # the last chain's partial last block
+    tg[700, 3] ^= 0x10
+    ad[300, 0] ^= 1
+    ok = check_decrypt(F, w.key, w.base_iv, chain, bad, tg, ad, abytes, label="workgroup decrypt")
+    assert int(ok.sum()) == n - 4 and not ok[[5, 300, 700, n - 1]].any()
+    check_decrypt(F, w.key, w.base_iv, chain, bad, tg, ad, abytes, inplace=True, label="workgroup decrypt in place")
+    check_encrypt(F, w.key, w.base_iv, chain, w.payload, aad, abytes, label="workgroup encrypt")
+
+
 @pytest.mark.parametrize("depth", [0, 2, 3])
 def test_config5_pipeline_small(F, depth):
     """The pipeline on 64 MiB with a ragged last chunk and AAD, vs the oracle."""
