@@ -389,9 +389,9 @@ def pipeline(F, W, torch, np, dev):
     out = torch.empty(length, dtype=torch.uint8, device=dev)
     ok = torch.empty(n, dtype=torch.uint8, device=dev)
     cs, ks, vs = torch.cuda.Stream(), torch.cuda.Stream(), torch.cuda.Stream()
-    def median_s(fn, streams, reps=3):
-        # one untimed pass, then the median of `reps` timed passes (host clock, all
-        # streams the pass uses drained)
+    def timed_s(fn, streams, reps=3):
+        # one untimed pass, then `reps` timed passes (host clock, all streams the pass
+        # uses drained), sorted
         fn()
         torch.cuda.synchronize()
         ts = []
@@ -402,7 +402,10 @@ def pipeline(F, W, torch, np, dev):
             for st in streams:
                 st.synchronize()
             ts.append(time.perf_counter() - t0)
-        return sorted(ts)[len(ts) // 2]
+        return sorted(ts)
+
+    median_s = lambda fn, streams: timed_s(fn, streams)[1]   # the pipelines: median of three
+    best_s = lambda fn, streams: timed_s(fn, streams, 5)[0]  # the copy ceiling: the best of five
 
     for name, mode, depth in (("depth0", 0, 0), ("depth2", 0, 2), ("depth3", 0, 3), ("eager_depth2", 1, 2),
                               ("otp_depth2", 2, 2), ("direct", 3, 0)):
@@ -428,7 +431,8 @@ def pipeline(F, W, torch, np, dev):
         res["%s_gbps" % name] = round(length / dt / 1e9, 2)
         log("pipeline %s: %.2f GB/s" % (name, res["%s_gbps" % name]))
     # plain pinned copies of the same bytes in the same chunks on one stream, through
-    # the runtime's hipMemcpyAsync (the copy engine's rate, nothing else enqueued)
+    # the runtime's hipMemcpyAsync (the copy engine's rate, nothing else enqueued); the
+    # ceiling the pipelines are compared with is the best of five passes
     hip = ctypes.CDLL(hip_runtime_path())
     hip.hipMemcpyAsync.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p]
     hip.hipMemcpyAsync.restype = ctypes.c_int
@@ -437,13 +441,13 @@ def pipeline(F, W, torch, np, dev):
         for off in range(0, length, chunk):
             assert hip.hipMemcpyAsync(dst + off, src + off, chunk, kind, cs.cuda_stream) == 0
 
-    dt = median_s(lambda: copies(h_out.data_ptr(), d_ctb.data_ptr(), 2), (cs,))
+    dt = best_s(lambda: copies(h_out.data_ptr(), d_ctb.data_ptr(), 2), (cs,))
     res["pinned_copy_d2h_gbps"] = round(length / dt / 1e9, 2)
     res["d2h_ratio_vs_copy"] = round(res["d2h_gbps"] / res["pinned_copy_d2h_gbps"], 3)
     res["d2h_direct_ratio_vs_copy"] = round(res["d2h_direct_gbps"] / res["pinned_copy_d2h_gbps"], 3)
     log("pinned d2h copy %.2f GB/s" % res["pinned_copy_d2h_gbps"])
     del h_out, d_ctb, d_tg
-    dt = median_s(lambda: copies(out.data_ptr(), h_ct.data_ptr(), 1), (cs,))
+    dt = best_s(lambda: copies(out.data_ptr(), h_ct.data_ptr(), 1), (cs,))
     res["pinned_copy_gbps"] = round(length / dt / 1e9, 2)
     best = max(res["depth0_gbps"], res["depth2_gbps"], res["depth3_gbps"])
     res["ratio_vs_copy"] = round(best / res["pinned_copy_gbps"], 3)
