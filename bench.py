@@ -263,6 +263,28 @@ def extras(F, W, torch, np, dev, stream, args):
     res["config1_1MiB"] = seq
     log("1 MiB:", seq)
 
+    # bf16 weights, 1 GiB, 1 MiB chains: decrypt + verify, then the 1% tampered chains rejected exactly
+    w3 = W.config3()
+    p3 = torch.from_numpy(w3.payload).to(dev)
+    c3 = w3.chain_sizes[0]
+    ct3, tg3 = F.encrypt_tag(w3.key, w3.base_iv, c3, p3)
+    o3 = torch.empty_like(ct3)
+    k3 = torch.empty(tg3.shape[0], dtype=torch.uint8, device=dev)
+    ms = time_calls(torch, stream, lambda: F.decrypt_verify(w3.key, w3.base_iv, c3, ct3, tg3, out=o3, ok=k3), 10)
+    assert bool(k3.all()) and torch.equal(o3, p3), "1 GiB decrypt failed"
+    for c, b in zip(w3.tamper_chains, w3.tamper_bits):   # one bit per chosen chain, as the parity test flips it
+        byte = int(c) * c3 + int(b) // 8
+        ct3[byte] ^= 0x80 >> (int(b) % 8)   # bit 0 is the most significant bit of byte 0
+    F.decrypt_verify(w3.key, w3.base_iv, c3, ct3, tg3, out=o3, ok=k3)
+    torch.cuda.synchronize()
+    rejected = torch.nonzero(k3 == 0).flatten().cpu().tolist()
+    res["weights_1GiB"] = {"workload": "bf16-weights-1GiB, 1 MiB chains, no AAD", "gbps": round(p3.numel() / ms / 1e6, 1),
+                           "us": round(ms * 1e3, 1), "chains": int(tg3.shape[0]),
+                           "tampered": len(w3.tamper_chains),
+                           "rejected_exactly_the_tampered": rejected == [int(x) for x in w3.tamper_chains]}
+    log("1 GiB weights:", res["weights_1GiB"])
+    del p3, ct3, o3, w3
+
     # eager evaluation: plaintext released before the tag check (64 MiB image batch, 64 KiB chains)
     w2 = W.config2()
     chain2 = 64 * KiB
