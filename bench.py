@@ -26,7 +26,7 @@ HBM_PEAK_GBS = 8000.0            # MI355X HBM3E peak
 # Integer VALU peak: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (one 32-bit op per lane per clock).
 ALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
 # Algorithmic 32-bit integer operations per 16-byte block of decrypt + verify in
-# the T-table formulation (derivation in the design doc): AES-256 rounds 1-13 at 16
+# the T-table formulation: AES-256 rounds 1-13 at 16
 # table lookups + 16 XORs each, the final round at 16 S-box lookups + 16 byte
 # merges/XORs, the initial AddRoundKey (4), the data XOR (4), the counter (1),
 # and one GF(2^128) multiply by a fixed element through 8-bit tables
@@ -53,7 +53,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the path is per-GPU and shards by whole chains with no exchange "
-              "(see DESIGN.md); run with --gpus 1", file=sys.stderr)
+              "(each GPU would take its own range of chains); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
