@@ -46,7 +46,7 @@ def lib():
         L.orc_chains_decrypt.argtypes = [u8p, u8p, u64, u8p, u64, u8p, u8p, u64, u8p, u8p, _ct.c_int, _ct.c_int]
         L.orc_chains_decrypt.restype = _ct.c_int
         L.orc_chains_decrypt_subset.argtypes = [u8p, u8p, u64, u8p, u64, u8p, u8p, u64,
-                                                _ct.POINTER(_ct.c_uint64), u64, u8p, u8p, _ct.c_int]
+                                                _ct.POINTER(_ct.c_uint64), u64, u8p, u8p, _ct.c_int, _ct.c_int]
         L.orc_chains_decrypt_subset.restype = _ct.c_int
         L.orc_max_threads.restype = _ct.c_int
         L.orc_count_aes.argtypes = [_ct.c_int]
@@ -184,8 +184,11 @@ def chains_decrypt(key, base_iv, chain_bytes, ct, tags, aad=None, aad_bytes=0, b
     return pt, ok
 
 
-def chains_decrypt_subset(key, base_iv, chain_bytes, ct, tags, idx, aad=None, aad_bytes=0, nthreads=0):
-    """Decrypt + verify only the chains in idx: returns (pt uint8[len(idx), chain_bytes], ok uint8[len(idx)])."""
+def chains_decrypt_subset(key, base_iv, chain_bytes, ct, tags, idx, aad=None, aad_bytes=0, bitserial=False,
+                          nthreads=0):
+    """Decrypt + verify only the chains in idx: returns (pt uint8[len(idx), chain_bytes], ok uint8[len(idx)]).
+    Row j is chain idx[j] exactly as chains_decrypt computes it (a short last chain fills the front of its row,
+    the rest of the row stays zero)."""
     c = _u8(ct)
     n = num_chains(c.size, chain_bytes)
     t = _u8(tags, 16 * n)
@@ -195,7 +198,7 @@ def chains_decrypt_subset(key, base_iv, chain_bytes, ct, tags, idx, aad=None, aa
     ok = _np.zeros(ix.size, _np.uint8)
     rc = lib().orc_chains_decrypt_subset(_p(_u8(key, 32)), _p(_u8(base_iv, 12)), chain_bytes, _p(c), c.size,
                                          _p(t), _p(a), aad_bytes, ix.ctypes.data_as(_ct.POINTER(_ct.c_uint64)),
-                                         ix.size, _p(pt), _p(ok), nthreads)
+                                         ix.size, _p(pt), _p(ok), int(bitserial), nthreads)
     if rc != 0:
         raise ValueError("bad chain index or chain_bytes")
     return pt, ok

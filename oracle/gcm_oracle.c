@@ -674,12 +674,15 @@ EXPORT int orc_chains_decrypt(const uint8_t key[32], const uint8_t base_iv[12], 
 /*
  * Decrypt + verify a chosen subset of chains of a large buffer (for sampled
  * checks at full size). pt_out receives the chosen chains back to back, each
- * chain_bytes long (a short last chain leaves the remainder untouched).
+ * chain_bytes long (a short last chain leaves the remainder untouched). Each
+ * chosen chain is the same independent GCM message (section 5.2) that
+ * orc_chains_decrypt checks at its index; bitserial selects Algorithm 1 or the
+ * table multiply exactly as there.
  */
 EXPORT int orc_chains_decrypt_subset(const uint8_t key[32], const uint8_t base_iv[12], uint64_t chain_bytes,
                                      const uint8_t *ct, uint64_t len, const uint8_t *tags, const uint8_t *aad,
                                      uint64_t aad_bytes, const uint64_t *idx, uint64_t nidx, uint8_t *pt_out,
-                                     uint8_t *ok_out, int nthreads)
+                                     uint8_t *ok_out, int bitserial, int nthreads)
 {
     if (chain_bytes == 0)
         return -1;
@@ -700,7 +703,7 @@ EXPORT int orc_chains_decrypt_subset(const uint8_t key[32], const uint8_t base_i
         uint8_t iv[12];
         orc_chain_iv(base_iv, i, iv);
         ok_out[j] = (uint8_t)gcm_ad(w, H, iv, ct + off, li, aad ? aad + i * aad_bytes : NULL, aad_bytes,
-                                    tags + 16 * i, 0, pt_out + (uint64_t)j * chain_bytes);
+                                    tags + 16 * i, bitserial, pt_out + (uint64_t)j * chain_bytes);
     }
     return 0;
 }

@@ -397,6 +397,40 @@ def test_tamper_is_exact_per_chain():
     assert np.unpackbits(p2 ^ pt).sum() == len(bad)
 
 
+@needs_libcrypto
+@pytest.mark.parametrize("bitserial", [False, True])
+def test_decrypt_subset_rows_are_the_chains(bitserial):
+    """Sampled checks (section 5.2: every chain is its own GCM message): row j of the subset
+    decrypt is chain idx[j], as libcrypto decrypts it under IV_i and as chains_decrypt does,
+    for index sets with a short last chain, 32-byte AAD, tampered chains and repeats."""
+    r = rng(66 + int(bitserial))
+    key, base_iv = rbytes(r, 32), rbytes(r, 12)
+    chain, alen = 1024, 32
+    pt = rbytes(r, 9 * chain + 200)   # chain 9 is 200 bytes
+    n = W.n_chains(pt.size, chain)
+    aad = rbytes(r, n * alen).reshape(n, alen)
+    ct, tags = oracle.chains_encrypt(key, base_iv, chain, pt, aad, alen)
+    bad_ct, bad_tags, bad_aad = ct.copy(), tags.copy(), aad.copy()
+    W.flip_bit(bad_ct[3 * chain:4 * chain], 77)       # chain 3: ciphertext bit
+    bad_tags[6, 15] ^= 0x01                            # chain 6: tag bit
+    bad_aad[9, 0] ^= 0x80                              # chain 9 (short): AAD bit
+    full_pt, full_ok = oracle.chains_decrypt(key, base_iv, chain, bad_ct, bad_tags, bad_aad, alen, bitserial=bitserial)
+    assert full_ok.tolist() == [1, 1, 1, 0, 1, 1, 0, 1, 1, 0]
+    for idx in ([9], [0, 9, 3], [6, 6, 2], list(range(n))[::-1], [3, 5, 7, 9]):
+        sub_pt, sub_ok = oracle.chains_decrypt_subset(key, base_iv, chain, bad_ct, bad_tags, idx, bad_aad, alen,
+                                                      bitserial=bitserial)
+        assert sub_pt.shape == (len(idx), chain) and sub_ok.shape == (len(idx),)
+        for j, i in enumerate(idx):
+            lo, hi = i * chain, min(pt.size, (i + 1) * chain)
+            want_pt, want_ok = LC.gcm_decrypt(key, oracle.chain_iv(base_iv, i), bad_ct[lo:hi], bad_tags[i],
+                                              bad_aad[i])
+            assert bytes(sub_pt[j, :hi - lo]) == want_pt == bytes(full_pt[lo:hi])
+            assert not sub_pt[j, hi - lo:].any()       # the rest of a short chain's row stays zero
+            assert int(sub_ok[j]) == int(want_ok) == int(full_ok[i])
+    with pytest.raises(ValueError):
+        oracle.chains_decrypt_subset(key, base_iv, chain, bad_ct, bad_tags, [n], bad_aad, alen)
+
+
 def test_multichain_costs_match_the_paper():
     facts = json.load(open(os.path.join(GOLDEN, "paper_facts.json")))
     assert facts["tag_bits"]["value"] == 128 and facts["key_bits"]["value"] == 256
