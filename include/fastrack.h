@@ -294,7 +294,9 @@ int fastrack_gcm_encrypt_tag_ragged(const uint8_t *key, const uint8_t *base_iv, 
  * Host helper for the per-sample layout: samples of h_sample_len[s] bytes are
  * packed back to back, each starting 16-byte aligned, and each is cut into
  * chains_per_sample chains of equal whole-block parts (the last part shorter,
- * parts past the end of a short sample empty). Writes n_samples *
+ * parts past the end of a short sample empty and placed at the sample's
+ * 16-byte-rounded end, so every offset is 16-byte aligned and the layout passes
+ * the ragged entry points' chain checks). Writes n_samples *
  * chains_per_sample entries to h_chain_off / h_chain_len and returns the
  * packed buffer size in bytes (0 on NULL arrays or chains_per_sample == 0).
  */

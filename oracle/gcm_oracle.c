@@ -19,7 +19,7 @@
  *   - GCTR: SP 800-38D section 6.5, Algorithm 3 (the AES-CTR keystream of
  *     section 3.2 and its figure of AES-CTR).
  *   - GCM-AE / GCM-AD with a 96-bit IV: SP 800-38D sections 7.1 and 7.2,
- *     Algorithms 4 and 5, with a full 128-bit tag (section 1.1 of the paper:
+ *     Algorithms 4 and 5, with a full 128-bit tag (section 1.2 of the paper:
  *     "128-bit MAC tag").
  *   - Multi-chaining authentication (paper section 5.2): the buffer is split
  *     into chains of chain_bytes; chain i is an independent GCM message with

@@ -104,16 +104,85 @@ def _dptr(t):
     return None if t is None else t.data_ptr()
 
 
+def _u8(t, what, numel=None, min_numel=None, cuda=True, device=None, pinned=False):
+    """Check a caller's buffer before its address reaches the library: a uint8,
+    contiguous tensor of the size the call reads or writes, on the data's device
+    (cuda=True) or in host memory (cuda=False; pinned where the library needs it)."""
+    if not isinstance(t, _torch.Tensor):
+        raise ValueError("%s must be a torch tensor" % what)
+    if t.dtype != _torch.uint8:
+        raise ValueError("%s must be uint8, got %s" % (what, t.dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % what)
+    if numel is not None and t.numel() != numel:
+        raise ValueError("%s holds %d bytes, the call needs exactly %d" % (what, t.numel(), numel))
+    if min_numel is not None and t.numel() < min_numel:
+        raise ValueError("%s holds %d bytes, the call needs at least %d" % (what, t.numel(), min_numel))
+    if cuda:
+        if not t.is_cuda:
+            raise ValueError("%s must be a CUDA tensor" % what)
+        if device is not None and t.device != device:
+            raise ValueError("%s is on %s, the data on %s" % (what, t.device, device))
+    else:
+        if t.device.type != "cpu":
+            raise ValueError("%s must be a host (CPU) tensor" % what)
+        if pinned and not t.is_pinned():
+            raise ValueError("%s must be in pinned host memory" % what)
+    return t
+
+
+def _aad_bytes(aad, n, what="aad", aad_bytes=None, **kw):
+    """AAD bytes per chain of an n-chain call: aad must hold exactly n x aad_bytes
+    bytes (a (n, a) tensor, or a flat one whose size n divides)."""
+    if aad is None:
+        if aad_bytes:
+            raise ValueError("aad_bytes = %d but no aad tensor" % aad_bytes)
+        return 0
+    if not isinstance(aad, _torch.Tensor):
+        raise ValueError("%s must be a torch tensor" % what)
+    if aad_bytes is None:
+        if aad.dim() == 2 and aad.shape[0] == n:
+            aad_bytes = int(aad.shape[1])
+        elif n > 0 and aad.numel() % n == 0:
+            aad_bytes = aad.numel() // n
+        elif n == 0 and aad.numel() == 0:
+            aad_bytes = 0
+        else:
+            raise ValueError("%s holds %d bytes, not a whole number of bytes for each of the %d chains"
+                             % (what, aad.numel(), n))
+    if aad_bytes < 0 or aad_bytes > 0xFFFFFFFF:
+        raise ValueError("aad_bytes out of range: %d" % aad_bytes)
+    _u8(aad, what, numel=n * aad_bytes, **kw)
+    return aad_bytes
+
+
 def _stream(s):
     if s is None:
         return _torch.cuda.current_stream().cuda_stream
     return s.cuda_stream if hasattr(s, "cuda_stream") else int(s)
 
 
-def _u8_dev(t, what):
-    if not (isinstance(t, _torch.Tensor) and t.is_cuda and t.dtype == _torch.uint8 and t.is_contiguous()):
-        raise ValueError("%s must be a contiguous uint8 CUDA tensor" % what)
-    return t
+def _stream_obj(s, device):
+    if s is None:
+        return _torch.cuda.current_stream(device)
+    if isinstance(s, _torch.cuda.Stream):
+        return s
+    return _torch.cuda.ExternalStream(_stream(s), device=device)
+
+
+def _used_on(tensors, streams, device):
+    """The binding allocated `tensors` on the current stream, and the library's work
+    on `streams` still reads or writes them after the call returns: tell the caching
+    allocator, so that freeing one does not hand its memory to a new allocation
+    while that work is in flight."""
+    cur = _torch.cuda.current_stream(device)
+    for s in streams:
+        so = _stream_obj(s, device)
+        if so.cuda_stream == cur.cuda_stream:
+            continue
+        for t in tensors:
+            if t is not None:
+                t.record_stream(so)
 
 
 def num_chains(length, chain_bytes):
@@ -125,37 +194,50 @@ def stage_bytes(length, chain_bytes, aad_bytes, chunk_bytes, depth):
 
 
 def decrypt_verify(key, base_iv, chain_bytes, ct, tags, aad=None, out=None, ok=None, flags=0, stream=None):
-    """Decrypt + verify every chain of ct (uint8 CUDA tensor). Returns (pt, ok)."""
-    _u8_dev(ct, "ct")
+    """Decrypt + verify every chain of ct (uint8 CUDA tensor). Returns (pt, ok).
+    tags holds n x 16 bytes and aad (optional) n x aad_bytes bytes, n = num_chains."""
+    _u8(ct, "ct")
+    dev = ct.device
     n = num_chains(ct.numel(), chain_bytes)
-    _u8_dev(tags, "tags")
-    aad_bytes = 0 if aad is None else aad.numel() // max(n, 1)
-    if aad is not None:
-        _u8_dev(aad, "aad")
+    _u8(tags, "tags", numel=16 * n, device=dev)
+    aad_bytes = _aad_bytes(aad, n, device=dev)
+    new = []
     if out is None:
         out = _torch.empty_like(ct)
+        new.append(out)
     if ok is None:
-        ok = _torch.empty(n, dtype=_torch.uint8, device=ct.device)
-    _check(lib().fastrack_gcm_decrypt_verify(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
-                                             chain_bytes, _dptr(ct), ct.numel(), _dptr(tags), _dptr(aad), aad_bytes,
-                                             _dptr(out), _dptr(ok), flags, _stream(stream)))
+        ok = _torch.empty(n, dtype=_torch.uint8, device=dev)
+        new.append(ok)
+    _u8(out, "out", numel=ct.numel(), device=dev)
+    _u8(ok, "ok", numel=n, device=dev)
+    with _torch.cuda.device(dev):
+        _check(lib().fastrack_gcm_decrypt_verify(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
+                                                 chain_bytes, _dptr(ct), ct.numel(), _dptr(tags), _dptr(aad),
+                                                 aad_bytes, _dptr(out), _dptr(ok), flags, _stream(stream)))
+        _used_on(new, [stream], dev)
     return out, ok
 
 
 def encrypt_tag(key, base_iv, chain_bytes, pt, aad=None, out=None, tags=None, flags=0, stream=None):
     """Encrypt every chain of pt (uint8 CUDA tensor) and produce its tag. Returns (ct, tags)."""
-    _u8_dev(pt, "pt")
+    _u8(pt, "pt")
+    dev = pt.device
     n = num_chains(pt.numel(), chain_bytes)
-    aad_bytes = 0 if aad is None else aad.numel() // max(n, 1)
-    if aad is not None:
-        _u8_dev(aad, "aad")
+    aad_bytes = _aad_bytes(aad, n, device=dev)
+    new = []
     if out is None:
         out = _torch.empty_like(pt)
+        new.append(out)
     if tags is None:
-        tags = _torch.empty((n, 16), dtype=_torch.uint8, device=pt.device)
-    _check(lib().fastrack_gcm_encrypt_tag(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
-                                          chain_bytes, _dptr(pt), pt.numel(), _dptr(aad), aad_bytes, _dptr(out),
-                                          _dptr(tags), flags, _stream(stream)))
+        tags = _torch.empty((n, 16), dtype=_torch.uint8, device=dev)
+        new.append(tags)
+    _u8(out, "out", numel=pt.numel(), device=dev)
+    _u8(tags, "tags", numel=16 * n, device=dev)
+    with _torch.cuda.device(dev):
+        _check(lib().fastrack_gcm_encrypt_tag(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
+                                              chain_bytes, _dptr(pt), pt.numel(), _dptr(aad), aad_bytes, _dptr(out),
+                                              _dptr(tags), flags, _stream(stream)))
+        _used_on(new, [stream], dev)
     return out, tags
 
 
@@ -187,36 +269,44 @@ class Eager:
 def decrypt_eager(key, base_iv, chain_bytes, ct, tags, aad=None, out=None, ok=None, decrypt_stream=None,
                   verify_stream=None):
     """Decrypt on decrypt_stream and check the tags on verify_stream. Returns an Eager."""
-    _u8_dev(ct, "ct")
+    _u8(ct, "ct")
+    dev = ct.device
     n = num_chains(ct.numel(), chain_bytes)
-    _u8_dev(tags, "tags")
-    aad_bytes = 0 if aad is None else aad.numel() // max(n, 1)
-    if aad is not None:
-        _u8_dev(aad, "aad")
+    _u8(tags, "tags", numel=16 * n, device=dev)
+    aad_bytes = _aad_bytes(aad, n, device=dev)
+    new = []
     if out is None:
         out = _torch.empty_like(ct)
+        new.append(out)
     if ok is None:
-        ok = _torch.empty(n, dtype=_torch.uint8, device=ct.device)
-    ds = decrypt_stream if decrypt_stream is not None else _torch.cuda.current_stream(ct.device)
-    vs = verify_stream if verify_stream is not None else ds
-    _check(lib().fastrack_gcm_decrypt_eager(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
-                                            chain_bytes, _dptr(ct), ct.numel(), _dptr(tags), _dptr(aad), aad_bytes,
-                                            _dptr(out), _dptr(ok), _stream(ds), _stream(vs)))
-    ev = _torch.cuda.Event()
-    ev.record(vs)
+        ok = _torch.empty(n, dtype=_torch.uint8, device=dev)
+        new.append(ok)
+    _u8(out, "out", numel=ct.numel(), device=dev)
+    _u8(ok, "ok", numel=n, device=dev)
+    with _torch.cuda.device(dev):
+        ds = decrypt_stream if decrypt_stream is not None else _torch.cuda.current_stream(dev)
+        vs = verify_stream if verify_stream is not None else ds
+        _check(lib().fastrack_gcm_decrypt_eager(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
+                                                chain_bytes, _dptr(ct), ct.numel(), _dptr(tags), _dptr(aad),
+                                                aad_bytes, _dptr(out), _dptr(ok), _stream(ds), _stream(vs)))
+        _used_on(new, [ds, vs], dev)
+        ev = _torch.cuda.Event()
+        ev.record(_stream_obj(vs, dev))
     return Eager(out, ok, ev)
 
 
 def keystream(key, base_iv, chain_bytes, length, chain_base=0, out=None, stream=None, device=None):
     """The CTR keystream of chains chain_base.. covering `length` bytes (a uint8 CUDA tensor)."""
+    new = []
     if out is None:
         device = _torch.device("cuda", _torch.cuda.current_device()) if device is None else _torch.device(device)
         out = _torch.empty(length, dtype=_torch.uint8, device=device)
-    _u8_dev(out, "out")
-    if out.numel() < length:
-        raise ValueError("out holds %d bytes, need %d" % (out.numel(), length))
-    _check(lib().fastrack_gcm_keystream(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
-                                        chain_bytes, chain_base, length, _dptr(out), _stream(stream)))
+        new.append(out)
+    _u8(out, "out", min_numel=length)
+    with _torch.cuda.device(out.device):
+        _check(lib().fastrack_gcm_keystream(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
+                                            chain_bytes, chain_base, length, _dptr(out), _stream(stream)))
+        _used_on(new, [stream], out.device)
     return out
 
 
@@ -224,25 +314,31 @@ def apply_verify(key, base_iv, chain_bytes, ct, ks, tags, aad=None, aad_bytes=No
                  stream=None):
     """pt = ct XOR ks and the tag check of chains chain_base.. of ct. tags, aad and ok
     are the whole message's arrays, indexed by global chain index. Returns (pt, ok)."""
-    _u8_dev(ct, "ct")
-    _u8_dev(ks, "ks")
-    _u8_dev(tags, "tags")
+    _u8(ct, "ct")
+    dev = ct.device
+    _u8(ks, "ks", min_numel=ct.numel(), device=dev)
+    _u8(tags, "tags", device=dev)
+    if tags.numel() % 16:
+        raise ValueError("tags must hold whole 16-byte tags, got %d bytes" % tags.numel())
     total = tags.numel() // 16
     n = num_chains(ct.numel(), chain_bytes)
     if chain_base + n > total:
         raise ValueError("tags hold %d chains, need %d" % (total, chain_base + n))
-    if aad is not None:
-        _u8_dev(aad, "aad")
-        aad_bytes = aad.numel() // max(total, 1) if aad_bytes is None else aad_bytes
-    else:
-        aad_bytes = 0
+    aad_bytes = _aad_bytes(aad, total, aad_bytes=aad_bytes, device=dev)
+    new = []
     if out is None:
         out = _torch.empty_like(ct)
+        new.append(out)
     if ok is None:
-        ok = _torch.empty(total, dtype=_torch.uint8, device=ct.device)
-    _check(lib().fastrack_gcm_apply_verify(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
-                                           chain_bytes, chain_base, _dptr(ct), ct.numel(), _dptr(ks), _dptr(tags),
-                                           _dptr(aad), aad_bytes, _dptr(out), _dptr(ok), _stream(stream)))
+        ok = _torch.empty(total, dtype=_torch.uint8, device=dev)
+        new.append(ok)
+    _u8(out, "out", numel=ct.numel(), device=dev)
+    _u8(ok, "ok", min_numel=chain_base + n, device=dev)
+    with _torch.cuda.device(dev):
+        _check(lib().fastrack_gcm_apply_verify(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
+                                               chain_bytes, chain_base, _dptr(ct), ct.numel(), _dptr(ks), _dptr(tags),
+                                               _dptr(aad), aad_bytes, _dptr(out), _dptr(ok), _stream(stream)))
+        _used_on(new, [stream], dev)
     return out, ok
 
 
@@ -251,30 +347,37 @@ def pipeline_h2d(key, base_iv, chain_bytes, h_ct, h_tags, h_aad=None, chunk_byte
                  verify_stream=None):
     """Chunked H2D copy of pinned ciphertext overlapped with decrypt + verify. Returns (pt, ok) on the device.
     mode PIPE_EAGER checks the tags on verify_stream; PIPE_OTP generates each chunk's keystream while it is
-    in flight. Both need depth >= 2. PIPE_DIRECT (depth 0) has the decrypt kernel read h_ct itself."""
-    if not (isinstance(h_ct, _torch.Tensor) and h_ct.device.type == "cpu" and h_ct.dtype == _torch.uint8):
-        raise ValueError("h_ct must be a uint8 CPU tensor in pinned memory")
+    in flight. Both need depth >= 2. PIPE_DIRECT (depth 0) has the decrypt kernel read h_ct itself.
+    The call returns while the streams still work; buffers the caller passes (stage, out, ok, h_ct, h_tags,
+    h_aad) must stay allocated until copy_stream and compute_stream (and verify_stream) have finished."""
+    _u8(h_ct, "h_ct", cuda=False, pinned=True)
     device = _torch.device("cuda", _torch.cuda.current_device()) if device is None else _torch.device(device)
     length = h_ct.numel()
     n = num_chains(length, chain_bytes)
-    aad_bytes = 0 if h_aad is None else h_aad.numel() // max(n, 1)
+    _u8(h_tags, "h_tags", numel=16 * n, cuda=False)
+    aad_bytes = _aad_bytes(h_aad, n, "h_aad", cuda=False)
     need = stage_bytes(length, chain_bytes, aad_bytes, chunk_bytes, depth)
+    new = []
     if stage is None:
-        stage = _torch.empty(need, dtype=_torch.uint8, device=device)
+        stage = _torch.empty(max(need, 1), dtype=_torch.uint8, device=device)
+        new.append(stage)
     if out is None:
         out = _torch.empty(length, dtype=_torch.uint8, device=device)
+        new.append(out)
     if ok is None:
         ok = _torch.empty(n, dtype=_torch.uint8, device=device)
-    h_tags = h_tags.contiguous()
-    if h_aad is not None:
-        h_aad = h_aad.contiguous()
-    cs = _stream(copy_stream)
-    ks = _stream(compute_stream)
-    vs = _stream(verify_stream) if verify_stream is not None else ks
-    _check(lib().fastrack_pipeline_h2d_mode(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
-                                            chain_bytes, h_ct.data_ptr(), length, h_tags.data_ptr(), _dptr(h_aad),
-                                            aad_bytes, chunk_bytes, depth, mode, _dptr(stage), stage.numel(),
-                                            _dptr(out), _dptr(ok), cs, ks, vs))
+        new.append(ok)
+    _u8(stage, "stage", min_numel=need, device=device)
+    _u8(out, "out", numel=length, device=device)
+    _u8(ok, "ok", numel=n, device=device)
+    with _torch.cuda.device(device):
+        vstream = verify_stream if verify_stream is not None else compute_stream
+        _check(lib().fastrack_pipeline_h2d_mode(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
+                                                chain_bytes, h_ct.data_ptr(), length, h_tags.data_ptr(), _dptr(h_aad),
+                                                aad_bytes, chunk_bytes, depth, mode, _dptr(stage), stage.numel(),
+                                                _dptr(out), _dptr(ok), _stream(copy_stream), _stream(compute_stream),
+                                                _stream(vstream)))
+        _used_on(new, [copy_stream, compute_stream, vstream], device)
     return out, ok
 
 
@@ -282,28 +385,35 @@ def pipeline_d2h(key, base_iv, chain_bytes, pt, aad=None, chunk_bytes=8 << 20, o
                  h_tags=None, copy_stream=None, compute_stream=None, mode=PIPE_FUSED):
     """Encrypt + tag pt (uint8 CUDA tensor) chunk by chunk into `out` (device; may be pt) and copy each
     chunk to the pinned host tensor h_ct while later chunks are encrypted. Returns (h_ct, h_tags).
-    mode PIPE_DIRECT writes the ciphertext straight into h_ct from the kernel (`out` is not used)."""
-    _u8_dev(pt, "pt")
+    mode PIPE_DIRECT writes the ciphertext straight into h_ct from the kernel (`out` is not used).
+    The results are valid once copy_stream has finished."""
+    _u8(pt, "pt")
+    dev = pt.device
     n = num_chains(pt.numel(), chain_bytes)
-    aad_bytes = 0 if aad is None else aad.numel() // max(n, 1)
-    if aad is not None:
-        _u8_dev(aad, "aad")
+    aad_bytes = _aad_bytes(aad, n, device=dev)
+    new = []
     if out is None and mode != PIPE_DIRECT:
         out = _torch.empty_like(pt)
+        new.append(out)
     if tags is None:
-        tags = _torch.empty((n, 16), dtype=_torch.uint8, device=pt.device)
+        tags = _torch.empty((n, 16), dtype=_torch.uint8, device=dev)
+        new.append(tags)
     if h_ct is None:
         h_ct = _torch.empty(pt.numel(), dtype=_torch.uint8, pin_memory=True)
     if h_tags is None:
         h_tags = _torch.empty((n, 16), dtype=_torch.uint8, pin_memory=True)
-    if not (isinstance(h_ct, _torch.Tensor) and h_ct.device.type == "cpu" and h_ct.numel() >= pt.numel()):
-        raise ValueError("h_ct must be a pinned uint8 CPU tensor of at least len bytes")
-    if h_tags.device.type != "cpu" or h_tags.numel() < 16 * n:
-        raise ValueError("h_tags must be a uint8 CPU tensor of n x 16 bytes")
-    _check(lib().fastrack_pipeline_d2h_mode(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
-                                            chain_bytes, _dptr(pt), pt.numel(), _dptr(aad), aad_bytes, chunk_bytes,
-                                            _dptr(out), _dptr(tags), h_ct.data_ptr(), h_tags.data_ptr(),
-                                            _stream(copy_stream), _stream(compute_stream), mode))
+    if out is not None:
+        _u8(out, "out", numel=pt.numel(), device=dev)
+    _u8(tags, "tags", numel=16 * n, device=dev)
+    _u8(h_ct, "h_ct", min_numel=pt.numel(), cuda=False, pinned=True)
+    _u8(h_tags, "h_tags", numel=16 * n, cuda=False)
+    with _torch.cuda.device(dev):
+        _check(lib().fastrack_pipeline_d2h_mode(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
+                                                chain_bytes, _dptr(pt), pt.numel(), _dptr(aad), aad_bytes,
+                                                chunk_bytes, _dptr(out), _dptr(tags), h_ct.data_ptr(),
+                                                h_tags.data_ptr(), _stream(copy_stream), _stream(compute_stream),
+                                                mode))
+        _used_on(new, [copy_stream, compute_stream], dev)
     return h_ct, h_tags
 
 
@@ -329,49 +439,63 @@ def sample_chains(sample_lens, chains_per_sample):
     return off[:n], ln[:n], int(total)
 
 
-def decrypt_verify_ragged(key, base_iv, chain_off, chain_len, ct, tags, aad=None, out=None, ok=None, stream=None):
-    """Decrypt + verify chains of their own offsets and lengths in ct (uint8 CUDA tensor). Returns (pt, ok);
-    bytes of pt outside every chain are left as they were."""
-    _u8_dev(ct, "ct")
+def _ragged_layout(chain_off, chain_len, size, what):
     off, ln = _u64_host(chain_off, "chain_off"), _u64_host(chain_len, "chain_len")
     if off.size != ln.size:
         raise ValueError("chain_off and chain_len differ in length")
+    if off.size and int((off + ln).max()) > size:
+        raise ValueError("a chain ends past the end of %s" % what)
+    return off, ln
+
+
+def decrypt_verify_ragged(key, base_iv, chain_off, chain_len, ct, tags, aad=None, out=None, ok=None, stream=None):
+    """Decrypt + verify chains of their own offsets and lengths in ct (uint8 CUDA tensor). Returns (pt, ok);
+    bytes of pt outside every chain are left as they were."""
+    _u8(ct, "ct")
+    dev = ct.device
+    off, ln = _ragged_layout(chain_off, chain_len, ct.numel(), "ct")
     n = off.size
-    if n and int((off + ln).max()) > ct.numel():
-        raise ValueError("a chain ends past the end of ct")
-    _u8_dev(tags, "tags")
-    aad_bytes = 0 if aad is None else aad.numel() // max(n, 1)
-    if aad is not None:
-        _u8_dev(aad, "aad")
+    _u8(tags, "tags", numel=16 * n, device=dev)
+    aad_bytes = _aad_bytes(aad, n, device=dev)
+    new = []
     if out is None:
         out = _torch.empty_like(ct)
+        new.append(out)
     if ok is None:
-        ok = _torch.empty(n, dtype=_torch.uint8, device=ct.device)
-    _check(lib().fastrack_gcm_decrypt_verify_ragged(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
-                                                    off.ctypes.data, ln.ctypes.data, n, _dptr(ct), _dptr(tags),
-                                                    _dptr(aad), aad_bytes, _dptr(out), _dptr(ok), _stream(stream)))
+        ok = _torch.empty(n, dtype=_torch.uint8, device=dev)
+        new.append(ok)
+    _u8(out, "out", numel=ct.numel(), device=dev)
+    _u8(ok, "ok", numel=n, device=dev)
+    with _torch.cuda.device(dev):
+        _check(lib().fastrack_gcm_decrypt_verify_ragged(_host_bytes(key, 32, "key"),
+                                                        _host_bytes(base_iv, 12, "base_iv"), off.ctypes.data,
+                                                        ln.ctypes.data, n, _dptr(ct), _dptr(tags), _dptr(aad),
+                                                        aad_bytes, _dptr(out), _dptr(ok), _stream(stream)))
+        _used_on(new, [stream], dev)
     return out, ok
 
 
 def encrypt_tag_ragged(key, base_iv, chain_off, chain_len, pt, aad=None, out=None, tags=None, stream=None):
     """Encrypt + tag chains of their own offsets and lengths in pt (uint8 CUDA tensor). Returns (ct, tags)."""
-    _u8_dev(pt, "pt")
-    off, ln = _u64_host(chain_off, "chain_off"), _u64_host(chain_len, "chain_len")
-    if off.size != ln.size:
-        raise ValueError("chain_off and chain_len differ in length")
+    _u8(pt, "pt")
+    dev = pt.device
+    off, ln = _ragged_layout(chain_off, chain_len, pt.numel(), "pt")
     n = off.size
-    if n and int((off + ln).max()) > pt.numel():
-        raise ValueError("a chain ends past the end of pt")
-    aad_bytes = 0 if aad is None else aad.numel() // max(n, 1)
-    if aad is not None:
-        _u8_dev(aad, "aad")
+    aad_bytes = _aad_bytes(aad, n, device=dev)
+    new = []
     if out is None:
         out = _torch.empty_like(pt)
+        new.append(out)
     if tags is None:
-        tags = _torch.empty((n, 16), dtype=_torch.uint8, device=pt.device)
-    _check(lib().fastrack_gcm_encrypt_tag_ragged(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
-                                                 off.ctypes.data, ln.ctypes.data, n, _dptr(pt), _dptr(aad), aad_bytes,
-                                                 _dptr(out), _dptr(tags), _stream(stream)))
+        tags = _torch.empty((n, 16), dtype=_torch.uint8, device=dev)
+        new.append(tags)
+    _u8(out, "out", numel=pt.numel(), device=dev)
+    _u8(tags, "tags", numel=16 * n, device=dev)
+    with _torch.cuda.device(dev):
+        _check(lib().fastrack_gcm_encrypt_tag_ragged(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
+                                                     off.ctypes.data, ln.ctypes.data, n, _dptr(pt), _dptr(aad),
+                                                     aad_bytes, _dptr(out), _dptr(tags), _stream(stream)))
+        _used_on(new, [stream], dev)
     return out, tags
 
 

@@ -1200,12 +1200,14 @@ FT_EXPORT uint64_t fastrack_sample_chains(const uint64_t *h_sample_len, uint64_t
     uint64_t off = 0, c = 0;
     for (uint64_t s = 0; s < n_samples; ++s) {
         const uint64_t len = h_sample_len[s];
-        // equal parts rounded up to whole blocks, so every chain but the last starts aligned
+        // equal parts rounded up to whole blocks, so every part that holds data starts
+        // aligned; parts past the end are empty and sit at the sample's 16-byte-rounded end
         const uint64_t part = ((len + chains_per_sample - 1) / chains_per_sample + 15) & ~15ull;
+        const uint64_t end16 = (len + 15) & ~15ull;
         for (uint32_t j = 0; j < chains_per_sample; ++j) {
             const uint64_t b = (uint64_t)j * part;
             const uint64_t l = b >= len ? 0 : (len - b < part ? len - b : part);
-            h_chain_off[c] = off + (b < len ? b : len);
+            h_chain_off[c] = off + (b < len ? b : end16);
             h_chain_len[c] = l;
             ++c;
         }

@@ -595,8 +595,8 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
     constexpr uint32_t G = 64u >> LL;
     // Static, so its LDS address is a compile-time constant and a v_perm result
     // can be used as the ds_read address with no further add. Modes without
-    // data AES hold only the GHASH table and a plain T0 (for the J0 masks), 33
-    // KiB, so that more waves share a CU.
+    // data AES hold the GHASH table, a plain T0 (for the J0 masks) and all six
+    // lane-combine tables, 113 KiB.
     constexpr uint32_t kLdsUse = kAes ? kLdsBytes : kLdsGhashOnly;
     __shared__ uint4 lds4[kLdsUse / 16];
     const char *lds = reinterpret_cast<const char *>(lds4);

@@ -27,9 +27,10 @@ enum GcmMode : int {
     kApplyKs = 4,     // out = in XOR a precomputed keystream `ks`, GHASH over `in`, tag check
 };
 
-// Workgroups of the streaming kernel per CU: the modes with data AES take a
-// CU's whole LDS; the GHASH-only modes need 33 KiB and run 16 waves per CU too
-// (more would squeeze their registers).
+// Workgroups of the streaming kernel per CU: the modes with data AES take 152
+// KiB of a CU's LDS; the GHASH-only modes take 113 KiB (the GHASH table, a
+// plain T0 and the six lane-combine tables) and also run one 1024-thread
+// workgroup, 16 waves, per CU.
 constexpr int gcm_wgs_per_cu(int mode)
 {
     return (mode == kVerify || mode == kApplyKs) && kGcmWavesPerWg < 16 ? 16 / kGcmWavesPerWg : 1;

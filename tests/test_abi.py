@@ -233,11 +233,27 @@ def test_sample_chains_layout(L):
     want_off, want_len, pos = [], [], 0
     for s in lens:
         part = -(-(-(-s // k)) // 16) * 16          # ceil(ceil(s / k) / 16) * 16
+        end16 = -(-s // 16) * 16
         for j in range(k):
-            b = min(j * part, s)
-            want_off.append(pos + b)
-            want_len.append(min(part, s - b))
-        pos += -(-s // 16) * 16
+            b = j * part
+            want_off.append(pos + (b if b < s else end16))   # empty parts at the sample's aligned end
+            want_len.append(max(0, min(part, s - b)))
+        pos += end16
     assert list(off) == want_off and list(ln) == want_len and total == pos
     assert sum(want_len) == sum(lens)
     assert L.fastrack_sample_chains(u64s(*lens), len(lens), 0, off, ln) == 0
+
+
+@pytest.mark.parametrize("lens,k", [([100, 0, 33, 4096, 5], 4), ([1, 17, 3800, 3801, 15], 16), ([0, 0, 16], 3),
+                                    ([70000, 12345, 64], 16)])
+def test_sample_chains_layout_passes_the_ragged_checks(L, lens, k):
+    """Every offset the layout helper writes is accepted by the ragged entry points' chain checks
+    (16-byte aligned, increasing, not overlapping). The call is given no ok buffer, so it stops at
+    that last argument check, after the chain table has been checked and before any HIP call."""
+    L.fastrack_last_error.restype = ctypes.c_char_p
+    n = len(lens) * k
+    off, ln = (ctypes.c_uint64 * n)(), (ctypes.c_uint64 * n)()
+    L.fastrack_sample_chains(u64s(*lens), len(lens), k, off, ln)
+    assert all(o % 16 == 0 for o in off)
+    assert rag_dec(L, off=tuple(off), ln=tuple(ln), ok=None) == -1
+    assert b"d_ok" in L.fastrack_last_error()

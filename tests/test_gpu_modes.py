@@ -247,3 +247,45 @@ def test_pipelines_reject_ranges_outside_one_pinned_allocation(F):
                                               d_tags.data_ptr(), ptr, tags.data_ptr(), s, s, mode)
             assert rc == -3 and b"pinned" in L.fastrack_last_error(), (what, mode, rc)
     torch.cuda.synchronize()
+
+
+def test_internal_buffers_survive_reuse_while_side_streams_run(F):
+    """The binding allocates the staging ring (H2D) and the device ciphertext and tags (D2H)
+    itself and drops them on return, while the copy and compute streams still use them.
+    New tensors of the same sizes, allocated and filled on the current stream right after
+    the call and before any synchronisation, must not take their memory."""
+    import torch
+    say("internal buffers vs allocator reuse")
+    chain, chunk, depth = 64 * KiB, 1 * MiB, 2
+    length = 12 * MiB + 3 * chain + 100
+    w = W.random_case(91, length, chain, 32)
+    aad = W.case_aad(w, chain)
+    ct, tags = oracle.chains_encrypt(w.key, w.base_iv, chain, w.payload, aad, 32)
+    W.flip_bit(ct[5 * chain:], 17)
+    want_pt, want_ok = oracle.chains_decrypt(w.key, w.base_iv, chain, ct, tags, aad, 32)
+    h_ct = torch.from_numpy(ct).pin_memory()
+    n = tags.shape[0]
+    need = F.stage_bytes(length, chain, 32, chunk, depth)
+    cs, ks = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    pt, ok = F.pipeline_h2d(w.key, w.base_iv, chain, h_ct, torch.from_numpy(tags), torch.from_numpy(aad),
+                            chunk_bytes=chunk, depth=depth, copy_stream=cs, compute_stream=ks)
+    junk = [torch.full((need,), 0xA5, dtype=torch.uint8, device="cuda") for _ in range(3)]
+    junk += [torch.full((sz,), 0x5A, dtype=torch.uint8, device="cuda") for sz in (2 * MiB, MiB, 16 * n)]
+    ks.synchronize()
+    cs.synchronize()
+    assert np.array_equal(host(pt), want_pt)
+    assert np.array_equal(host(ok), want_ok)
+    del junk
+    # D2H: the device ciphertext and tags are the binding's own
+    want_ct, want_tags = oracle.chains_encrypt(w.key, w.base_iv, chain, w.payload, aad, 32)
+    d_pt, d_aad = dev(w.payload), dev(aad)
+    torch.cuda.synchronize()
+    h_out, h_tags = F.pipeline_d2h(w.key, w.base_iv, chain, d_pt, d_aad, chunk_bytes=chunk, copy_stream=cs,
+                                   compute_stream=ks)
+    junk = [torch.full((length,), 0xC3, dtype=torch.uint8, device="cuda") for _ in range(2)]
+    junk += [torch.full((16 * n,), 0x3C, dtype=torch.uint8, device="cuda") for _ in range(2)]
+    cs.synchronize()
+    ks.synchronize()
+    assert np.array_equal(h_tags.numpy(), want_tags)
+    assert np.array_equal(h_out.numpy()[:length], want_ct)

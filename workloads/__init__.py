@@ -187,7 +187,7 @@ def sample_batch(n_samples: int = 256, chains_per_sample: int = 16, seed: int = 
     (the paper's ResNet-50 workload, section 6.1). Samples are packed back to back, each starting
     16-byte aligned, with zero bytes in the gaps; the payload bytes are uniform (compressed data is
     high-entropy). Each sample is cut into ``chains_per_sample`` chains (16 tags per sample as in the
-    paper's evaluation, section 6.3), and each chain carries its 1-byte serial number within the sample as
+    paper's evaluation, section 6.4), and each chain carries its 1-byte serial number within the sample as
     AAD. ``extra`` holds sample_lens, sample_off, chains_per_sample and the AAD array (uint8[n, 1]).
     """
     rng = rng_for(seed)
