@@ -87,6 +87,33 @@ int fastrack_gcm_decrypt_verify(const uint8_t *key, const uint8_t *base_iv, uint
                                 uint32_t flags, void *stream);
 
 /*
+ * Allocation-free decrypt and verify, for callers that cannot allocate device
+ * memory: code under HIP graph capture, serving loops and harnesses that forbid
+ * hipMalloc. The same computation, arguments, outputs and errors as
+ * fastrack_gcm_decrypt_verify (flags included), with no hipMalloc, hipFree or
+ * other device allocation on any call.
+ * Its device memory is one static array of FASTRACK_NOALLOC_SCRATCH_BYTES per
+ * GPU, held until the process ends: the key tables of the last key this entry
+ * point was called with on that GPU (rebuilt in place by a kernel on `stream`
+ * when the key changes), then the 16-byte GHASH partials (one per work item) and
+ * chain masks (one per chain) of launches that cut chains into segments.
+ * Every call on one GPU shares that GPU's array and leaves its contents behind:
+ * calls that overlap on one GPU (on streams not ordered with each other) race on
+ * it and give wrong results; order them. fastrack_shutdown() clears the key
+ * tables.
+ * EINVAL as fastrack_gcm_decrypt_verify, and also when a launch would need more
+ * than FASTRACK_NOALLOC_MAX_PARTIALS partial slots (items + chains); the
+ * library's work planner stays below about 200,000 for every size, so this
+ * limit is a guard, not a size cap callers meet.
+ */
+#define FASTRACK_NOALLOC_SCRATCH_BYTES (4u << 20)
+#define FASTRACK_NOALLOC_MAX_PARTIALS 212256u
+int fastrack_gcm_decrypt_verify_noalloc(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                                        const uint8_t *d_ct, uint64_t len, const uint8_t *d_tags,
+                                        const uint8_t *d_aad, uint32_t aad_bytes, uint8_t *d_pt, uint8_t *d_ok,
+                                        uint32_t flags, void *stream);
+
+/*
  * Encrypt and tag: the GPU-to-CPU direction (paper section 1.1: the sender
  * encrypts and generates the MAC tag). Same chain layout and checks as above.
  *   d_pt    [len] plaintext on the device

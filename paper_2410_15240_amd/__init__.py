@@ -14,7 +14,7 @@ import torch as _torch  # loads the HIP runtime that the library then shares
 
 from . import build as _build
 
-__all__ = ["FastrackError", "decrypt_verify", "encrypt_tag", "decrypt_eager", "Eager", "keystream", "apply_verify",
+__all__ = ["FastrackError", "decrypt_verify", "decrypt_verify_noalloc", "encrypt_tag", "decrypt_eager", "Eager", "keystream", "apply_verify",
            "pipeline_h2d", "pipeline_d2h", "decrypt_verify_ragged", "encrypt_tag_ragged", "sample_chains", "num_chains", "stage_bytes", "shutdown", "library_path", "F_SEQ_GHASH", "PIPE_FUSED",
            "PIPE_EAGER", "PIPE_OTP", "PIPE_DIRECT"]
 
@@ -51,6 +51,9 @@ def lib():
         L.fastrack_num_chains.restype = u64
         L.fastrack_gcm_decrypt_verify.argtypes = [u8p, u8p, u64, u8p, u64, u8p, u8p, u32, u8p, u8p, u32, vp]
         L.fastrack_gcm_decrypt_verify.restype = _ct.c_int
+        L.fastrack_gcm_decrypt_verify_noalloc.argtypes = [u8p, u8p, u64, u8p, u64, u8p, u8p, u32, u8p, u8p, u32,
+                                                          vp]
+        L.fastrack_gcm_decrypt_verify_noalloc.restype = _ct.c_int
         L.fastrack_gcm_encrypt_tag.argtypes = [u8p, u8p, u64, u8p, u64, u8p, u32, u8p, u8p, u32, vp]
         L.fastrack_gcm_encrypt_tag.restype = _ct.c_int
         L.fastrack_pipeline_stage_bytes.argtypes = [u64, u64, u32, u64, _ct.c_int]
@@ -215,6 +218,25 @@ def decrypt_verify(key, base_iv, chain_bytes, ct, tags, aad=None, out=None, ok=N
                                                  chain_bytes, _dptr(ct), ct.numel(), _dptr(tags), _dptr(aad),
                                                  aad_bytes, _dptr(out), _dptr(ok), flags, _stream(stream)))
         _used_on(new, [stream], dev)
+    return out, ok
+
+
+def decrypt_verify_noalloc(key, base_iv, chain_bytes, ct, tags, aad, out, ok, flags=0, stream=None):
+    """decrypt_verify through the allocation-free entry point: the caller passes every
+    buffer (out, ok) and the library allocates no device memory. Calls on one GPU
+    share the library's fixed device area: order calls made on different streams."""
+    _u8(ct, "ct")
+    dev = ct.device
+    n = num_chains(ct.numel(), chain_bytes)
+    _u8(tags, "tags", numel=16 * n, device=dev)
+    aad_bytes = _aad_bytes(aad, n, device=dev)
+    _u8(out, "out", numel=ct.numel(), device=dev)
+    _u8(ok, "ok", numel=n, device=dev)
+    with _torch.cuda.device(dev):
+        _check(lib().fastrack_gcm_decrypt_verify_noalloc(_host_bytes(key, 32, "key"),
+                                                         _host_bytes(base_iv, 12, "base_iv"), chain_bytes, _dptr(ct),
+                                                         ct.numel(), _dptr(tags), _dptr(aad), aad_bytes, _dptr(out),
+                                                         _dptr(ok), flags, _stream(stream)))
     return out, ok
 
 

@@ -350,7 +350,8 @@ void iv_words(const uint8_t *iv, uint32_t w[3])
 int run_gcm(bool encrypt, GcmMode mode, const KeyCtx *ctx, const uint8_t *base_iv, uint64_t chain_bytes,
             uint64_t chain_base, const uint8_t *in, const uint8_t *ks, uint64_t len, uint8_t *out,
             const uint8_t *aad, uint32_t aad_bytes, const uint8_t *tags_in, uint8_t *tags_out, uint8_t *ok,
-            uint32_t flags, int dev, int num_cu, hipStream_t s)
+            uint32_t flags, int dev, int num_cu, hipStream_t s, uint4 *fixed_scratch = nullptr,
+            uint64_t fixed_entries = 0)
 {
     GcmLaunch p;
     std::memset(&p, 0, sizeof p);
@@ -387,11 +388,18 @@ int run_gcm(bool encrypt, GcmMode mode, const KeyCtx *ctx, const uint8_t *base_i
     const bool ghash = mode == kFused || mode == kVerify || mode == kApplyKs;
     p.split = ghash && p.n_items > p.n_chains ? 1u : 0u;
     if (p.split) {   // chains cut into segments: per-item partials and per-chain masks
-        void *sc = nullptr;
-        int rc = scratch_for(dev, s, (size_t)(p.n_items + p.n_chains) * 16, &sc);
-        if (rc)
-            return rc;
-        p.partials = reinterpret_cast<uint4 *>(sc);
+        if (fixed_scratch) {   // the caller's fixed area (allocation-free entry point)
+            if (p.n_items + p.n_chains > fixed_entries)
+                return fail(FASTRACK_EINVAL, "the launch needs %llu partial slots, the fixed scratch holds %llu",
+                            (unsigned long long)(p.n_items + p.n_chains), (unsigned long long)fixed_entries);
+            p.partials = fixed_scratch;
+        } else {
+            void *sc = nullptr;
+            int rc = scratch_for(dev, s, (size_t)(p.n_items + p.n_chains) * 16, &sc);
+            if (rc)
+                return rc;
+            p.partials = reinterpret_cast<uint4 *>(sc);
+        }
         p.masks = p.partials + p.n_items;
     }
     he = launch_gcm(p, encrypt, mode, num_cu, s);
@@ -440,6 +448,107 @@ FT_EXPORT int fastrack_gcm_decrypt_verify(const uint8_t *key, const uint8_t *bas
         return rc;
     return run_gcm(false, kFused, ctx, base_iv, chain_bytes, 0, d_ct, nullptr, len, d_pt, aad_bytes ? d_aad : nullptr, aad_bytes,
                    d_tags, nullptr, d_ok, flags, dev, ncu, s);
+}
+
+// ---------------------------------------------------------------------------
+// Allocation-free decrypt + verify
+// ---------------------------------------------------------------------------
+//
+// One static device array per GPU (each GPU that loads the library holds its own
+// copy until the process ends): the key tables of the last key this entry point
+// was given on that GPU, then the per-item GHASH partials and per-chain masks of
+// launches that cut chains into segments. Host code never passes the array's name
+// to a kernel (on the host it is only a stand-in for the symbol); it uses the
+// device address that hipGetSymbolAddress returns for the current device.
+
+namespace {
+constexpr size_t kNoAllocKeyBytes = (sizeof(KeyCtx) + 255) & ~(size_t)255;
+constexpr uint64_t kNoAllocEntries = (FASTRACK_NOALLOC_SCRATCH_BYTES - kNoAllocKeyBytes) / 16;
+static_assert(kNoAllocEntries == FASTRACK_NOALLOC_MAX_PARTIALS, "header constant matches the layout");
+}  // namespace
+
+static __device__ __align__(256) uint8_t scratch[FASTRACK_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kNoAllocMaxDevices = 64;
+struct NoAllocDevice {
+    uint8_t *ptr = nullptr;              // device address of `scratch` on this device
+    bool have_key = false;               // the key tables at ptr belong to `key`
+    std::array<uint8_t, 32> key{};
+};
+NoAllocDevice g_noalloc[kNoAllocMaxDevices];
+
+// The device address of this device's `scratch`, looked up once per device with
+// the device current.
+int noalloc_area(int dev, NoAllocDevice **out)
+{
+    if (dev < 0 || dev >= kNoAllocMaxDevices)
+        return fail(FASTRACK_EINVAL, "device %d is beyond the %d devices the allocation-free path serves", dev,
+                    kNoAllocMaxDevices);
+    NoAllocDevice &d = g_noalloc[dev];
+    if (!d.ptr) {
+        void *p = nullptr;
+        hipError_t he = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (he != hipSuccess || !p)
+            return hip_fail(he != hipSuccess ? he : hipErrorInvalidSymbol, "hipGetSymbolAddress(scratch)");
+        d.ptr = static_cast<uint8_t *>(p);
+    }
+    *out = &d;
+    return FASTRACK_OK;
+}
+}  // namespace
+
+FT_EXPORT int fastrack_gcm_decrypt_verify_noalloc(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                                                  const uint8_t *d_ct, uint64_t len, const uint8_t *d_tags,
+                                                  const uint8_t *d_aad, uint32_t aad_bytes, uint8_t *d_pt,
+                                                  uint8_t *d_ok, uint32_t flags, void *stream)
+{
+    g_err.clear();
+    int rc = check_common(key, base_iv, chain_bytes, len, d_ct, d_pt, d_aad, aad_bytes, flags);
+    if (rc || len == 0)
+        return rc;
+    if (!d_tags || !d_ok)
+        return fail(FASTRACK_EINVAL, "d_tags and d_ok must be non-NULL");
+    std::lock_guard<std::mutex> lk(g_mu);
+    int dev, ncu;
+    if ((rc = current_device(&dev, &ncu)))
+        return rc;
+    NoAllocDevice *d;
+    if ((rc = noalloc_area(dev, &d)))
+        return rc;
+    // Size check before anything is enqueued: the same plan run_gcm makes.
+    GcmLaunch probe;
+    std::memset(&probe, 0, sizeof probe);
+    make_plan(len, chain_bytes, 0, (uint64_t)ncu * kGcmWavesPerWg * gcm_wgs_per_cu(kFused), probe);
+    if (probe.n_items > 0xFFFFFFFFull)
+        return fail(FASTRACK_EINVAL, "more than 2^32-1 work items in one launch");
+    const bool seq = (flags & FASTRACK_F_SEQ_GHASH) != 0;
+    if (!seq && probe.n_items > probe.n_chains && probe.n_items + probe.n_chains > kNoAllocEntries)
+        return fail(FASTRACK_EINVAL,
+                    "the launch needs %llu partial slots; the allocation-free scratch holds %llu "
+                    "(fastrack_gcm_decrypt_verify has no such limit)",
+                    (unsigned long long)(probe.n_items + probe.n_chains), (unsigned long long)kNoAllocEntries);
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    KeyCtx *ctx = reinterpret_cast<KeyCtx *>(d->ptr);
+    std::array<uint8_t, 32> k;
+    std::memcpy(k.data(), key, 32);
+    if (!d->have_key || d->key != k) {   // the key tables are rebuilt in place, on this stream
+        uint32_t words[8];
+        for (int i = 0; i < 8; ++i)
+            words[i] = (uint32_t)key[4 * i] | ((uint32_t)key[4 * i + 1] << 8) | ((uint32_t)key[4 * i + 2] << 16) |
+                       ((uint32_t)key[4 * i + 3] << 24);
+        d->have_key = false;
+        hipError_t he = launch_key_setup(words, ctx, s);
+        std::memset(words, 0, sizeof words);
+        if (he != hipSuccess)
+            return hip_fail(he, "key setup launch");
+        d->key = k;
+        d->have_key = true;
+    }
+    std::memset(k.data(), 0, 32);
+    return run_gcm(false, kFused, ctx, base_iv, chain_bytes, 0, d_ct, nullptr, len, d_pt,
+                   aad_bytes ? d_aad : nullptr, aad_bytes, d_tags, nullptr, d_ok, flags, dev, ncu, s,
+                   reinterpret_cast<uint4 *>(d->ptr + kNoAllocKeyBytes), kNoAllocEntries);
 }
 
 FT_EXPORT int fastrack_gcm_encrypt_tag(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
@@ -1219,6 +1328,20 @@ FT_EXPORT uint64_t fastrack_sample_chains(const uint64_t *h_sample_len, uint64_t
 FT_EXPORT void fastrack_shutdown(void)
 {
     std::lock_guard<std::mutex> lk(g_mu);
+    // Key-derived tables of the allocation-free path do not outlive the library's use.
+    int cur = -1;
+    if (hipGetDevice(&cur) == hipSuccess) {
+        for (int dev = 0; dev < kNoAllocMaxDevices; ++dev) {
+            NoAllocDevice &d = g_noalloc[dev];
+            if (!d.ptr || !d.have_key)
+                continue;
+            if (hipSetDevice(dev) == hipSuccess && hipDeviceSynchronize() == hipSuccess)
+                (void)hipMemset(d.ptr, 0, kNoAllocKeyBytes);
+            d.have_key = false;
+            d.key.fill(0);
+        }
+        (void)hipSetDevice(cur);
+    }
     if (g_keys.empty() && g_scratch.empty())
         return;
     (void)hipDeviceSynchronize();
