@@ -6,7 +6,9 @@ A timed step is one decrypt + verify pass of the 64 MiB image batch
 (256x3x224x224 uint8, zero-padded, 32-byte AAD per chain) at each of the chain
 sizes 4 KiB, 16 KiB, 64 KiB, 256 KiB and 1 MiB, with every input already
 resident in HBM. `value` is the payload decrypted per second over the whole
-timed region (GB/s, 1e9 bytes). Outside the timed region the script also
+timed region (GB/s, 1e9 bytes). The W warm-up steps are followed by more until
+0.3 s have passed, so the timed steps run at the settled shader clock, which the
+script measures during them. Outside the timed region the script also
 measures encrypt + tag (256 MiB fp32 gradients, 256 KiB chains), the
 sequential-GHASH baseline against the multi-chain path (1 MiB buffer), the
 pipelined 4 GiB host-to-device decrypt against a plain pinned copy, and the
@@ -25,13 +27,12 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0            # MI355X HBM3E peak
 # Integer VALU peak: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz (one 32-bit op per lane per clock).
 ALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12
-# Algorithmic 32-bit integer operations per 16-byte block of decrypt + verify in
-# the T-table formulation: AES-256 rounds 1-13 at 16
-# table lookups + 16 XORs each, the final round at 16 S-box lookups + 16 byte
-# merges/XORs, the initial AddRoundKey (4), the data XOR (4), the counter (1),
-# and one GF(2^128) multiply by a fixed element through 8-bit tables
-# (16 lookups + 64 XORs).
-ALG_OPS_PER_BLOCK = 13 * 32 + 32 + 4 + 4 + 1 + 16 + 64
+# Under sustained load the shader clock dips for a few milliseconds after work
+# starts (kernel traces show launches ~15% slower 2-8 ms into a burst) and then
+# settles; warm-up runs at least this long so that the timed steps see the
+# settled clock whatever --steps is.
+WARMUP_MIN_S = 0.3
+GAPLESS_STEPS = 20
 
 KiB, MiB, GiB = 1024, 1 << 20, 1 << 30
 
@@ -94,16 +95,28 @@ def main():
             if evs is not None:
                 evs[i][1].record(stream)
 
-    log("warmup", args.warmup)
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    log("warmup", args.warmup, "steps, at least %.1f s" % WARMUP_MIN_S)
+    warm_steps, warm_s = warm_up(torch, step, args.warmup, WARMUP_MIN_S)
+    step_est_ms = warm_s * 1e3 / max(1, warm_steps)
     t_start, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     log("timed steps", args.steps)
-    # The timed region holds only the launches: a timing event between launches
-    # costs the GPU a few microseconds each.
+    # The shader clock during the timed steps: probes sleeping on a second stream
+    # for about the length of the timed region (one wave each, next to the launches).
+    pstream = torch.cuda.Stream()
+    go = torch.cuda.Event()
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
+    # The last GAPLESS_STEPS warm-up steps run straight into the timed ones, with no
+    # idle gap between them: after a gap the shader clock dips for several
+    # milliseconds, which would otherwise fall inside a short timed region. The
+    # event pair below brackets exactly the timed steps.
+    for _ in range(GAPLESS_STEPS):
+        step()
+    go.record(stream)
+    pstream.wait_event(go)
+    probe = F.clock_probe(max(1, int(0.9 * args.steps * step_est_ms * 1e3)), 8, stream=pstream)
+    # The timed region holds only the launches: a timing event between launches
+    # costs the GPU a few microseconds each.
     t_start.record(stream)
     for s in range(args.steps):
         step()
@@ -111,17 +124,22 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     total_ms = t_start.elapsed_time(t_end)
+    clocks = F.clock_ghz(probe)
     for chain, ct, tags, aad, out, ok in cases:
         assert bool(ok.all()), "benchmark decrypt rejected a chain"
         assert torch.equal(out, payload), "benchmark decrypt produced wrong plaintext"
-    # Per chain size: 20 back-to-back launches of that size between two events.
+    # Per chain size: 20 back-to-back launches of that size between two events, three
+    # times; the median of the three.
     per = []
     for i, (chain, ct, tags, aad, out, ok) in enumerate(cases):
         one = lambda: F.decrypt_verify(w.key, w.base_iv, chain, ct, tags, aad, out=out, ok=ok)
-        per.append(time_calls(torch, stream, one, 20))
-    # A plain device copy of the same 64 MiB: under rocprofv3 --pmc its FETCH_SIZE /
-    # WRITE_SIZE calibrate the counters against a known byte count.
-    cases[0][4].copy_(cases[0][1])
+        per.append(sorted(time_calls(torch, stream, one, 20, pre=20) for _ in range(3))[1])
+    # The achievable HBM rate on this machine: a plain 64 MiB device-to-device copy
+    # (read + write bytes over time, best of three runs of 20 copies). Under
+    # rocprofv3 --pmc its FETCH_SIZE / WRITE_SIZE also calibrate the counters.
+    dst, src = cases[0][4], cases[0][1]
+    copy_ms = min(time_calls(torch, stream, lambda: dst.copy_(src), 20) for _ in range(3))
+    copy_gbs = 2 * src.numel() / (copy_ms * 1e-3) / 1e9
     torch.cuda.synchronize()
     ms_per_step = total_ms / args.steps
     value = len(cases) * L / (ms_per_step * 1e-3) / 1e9
@@ -130,16 +148,25 @@ def main():
     for i, (chain, ct, tags, aad, out, ok) in enumerate(cases):
         n = tags.shape[0]
         ms = per[i]
+        ab = 2 * L + n * (16 + 32 + 1)   # payload in + out, tags, AAD, ok flags
+        alg_bytes.append(ab)
         sweep["%dKiB" % (chain // KiB)] = {"gbps": round(L / (ms * 1e-3) / 1e9, 1), "us": round(ms * 1e3, 1),
-                                           "chains": n}
-        alg_bytes.append(2 * L + n * (16 + 32 + 1))   # payload in + out, tags, AAD, ok flags
+                                           "chains": n, "hbm_frac": round(ab / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
     # average launch duration over the timed region (5 launches per step, one per chain size)
     launch_ms = ms_per_step / len(cases)
+    per_size_mean_ms = float(np.mean(per))
     bytes_per_launch = float(np.mean(alg_bytes))
-    blocks = L // 16
-    achieved_tops = blocks * ALG_OPS_PER_BLOCK / (launch_ms * 1e-3) / 1e12
     hbm_gbs = bytes_per_launch / (launch_ms * 1e-3) / 1e9
-    log("decrypt sweep %.1f GB/s, %.3f ms/step" % (value, ms_per_step))
+    log("decrypt sweep %.1f GB/s, %.3f ms/step, %.1f us/launch (per-size mean %.1f us), clock %s GHz, copy %.0f GB/s"
+        % (value, ms_per_step, launch_ms * 1e3, per_size_mean_ms * 1e3, ["%.2f" % c for c in clocks], copy_gbs))
+    sq = sq_profile("decrypt")
+    valu = None
+    if sq:
+        insts = float(np.mean([sq[k] for k in sq]))   # VALU wave-instructions per launch, mean over the sizes
+        tops = insts * 64 / (launch_ms * 1e-3) / 1e12
+        valu = {"achieved": round(tops, 2), "peak": round(ALU_PEAK_TOPS, 2), "unit": "T lane-op/s",
+                "frac": round(tops / ALU_PEAK_TOPS, 3), "valu_insts_per_launch": int(insts),
+                "source": "SQ_INSTS_VALU (rocprofv3 --pmc) of the same launches, %s" % os.path.basename(SQ_FILE)}
 
     result = {
         "metric": "AES-256-GCM decrypt+verify GB/s vs chain size; % HBM peak; pipelined H2D GB/s",
@@ -148,8 +175,10 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "warmup_run": {"steps": warm_steps + GAPLESS_STEPS, "seconds": round(warm_s, 3),
+                       "gapless_steps": GAPLESS_STEPS},
         "ms_per_step": round(ms_per_step, 4),
-        "wall_s": round(wall, 3),
+        "wall_s": round(wall, 3),   # host clock: the gapless warm-up steps and the timed steps
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -159,13 +188,21 @@ def main():
                                "chain sizes 4K/16K/64K/256K/1M, 32-byte AAD per chain",
                    "bytes_per_step": len(cases) * L, "parallelism": "single GPU"},
         "sweep": sweep,
-        "roofline": {"bound": "alu", "achieved": round(achieved_tops, 2), "peak": round(ALU_PEAK_TOPS, 2),
-                     "unit": "Tops/s", "frac": round(achieved_tops / ALU_PEAK_TOPS, 3),
-                     "traffic": measured_traffic(),
+        "launch_us": {"timed_region_mean": round(launch_ms * 1e3, 2), "per_size_mean": round(per_size_mean_ms * 1e3, 2),
+                      "ratio": round(launch_ms / per_size_mean_ms, 3)},
+        "shader_clock_ghz": {"mean": round(float(np.mean(clocks)), 3), "min": round(min(clocks), 3),
+                             "max": round(max(clocks), 3),
+                             "how": "s_memtime cycles over s_memrealtime ticks, 8 probe waves (one per XCD) "
+                                    "sleeping on a second stream during the timed steps"},
+        "roofline": {"bound": "hbm", "achieved": round(hbm_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(hbm_gbs / HBM_PEAK_GBS, 4), "traffic": measured_traffic(),
                      "kernel": "gcm_kernel<decrypt> (+ chain_tag_kernel where chains are cut into segments)",
-                     "alg_ops_per_block": ALG_OPS_PER_BLOCK, "launch_us": round(launch_ms * 1e3, 2)},
-        "hbm": {"achieved": round(hbm_gbs, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(hbm_gbs / HBM_PEAK_GBS, 3), "alg_bytes_per_launch": int(bytes_per_launch)},
+                     "alg_bytes_per_launch": int(bytes_per_launch), "launch_us": round(launch_ms * 1e3, 2),
+                     "device_copy_gbps": round(copy_gbs, 1),
+                     "frac_of_device_copy": round(hbm_gbs / copy_gbs, 4),
+                     "limiter": "LDS table reads and integer VALU issue (the AES T-table lookups and GHASH "
+                                "table lookups), not HBM",
+                     "valu": valu},
     }
 
     if not args.skip_extras:
@@ -206,9 +243,60 @@ def measured_traffic():
         return None
 
 
-def time_calls(torch, stream, fn, reps):
-    fn()
+def warm_up(torch, step, steps, min_s):
+    """Run `steps` untimed steps, then more in blocks of 20 until min_s seconds have
+    passed. Returns (steps run, seconds)."""
     torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    n = 0
+    for _ in range(steps):
+        step()
+        n += 1
+    torch.cuda.synchronize()
+    while time.perf_counter() - t0 < min_s:
+        for _ in range(20):
+            step()
+        n += 20
+        torch.cuda.synchronize()
+    return n, time.perf_counter() - t0
+
+
+SQ_FILE = os.path.join(ROOT, "profiles", "gcm_image-batch-64MiB_valu.txt")
+
+
+def sq_profile(direction):
+    """VALU wave-instructions per launch of each chain size ("decrypt" or "encrypt")
+    from the committed rocprofv3 counter summary, or None when the kernel sources
+    have changed since it was taken."""
+    try:
+        fields, out = {}, {}
+        for line in open(SQ_FILE):
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip()
+        if fields.get("kernels_sha256") != kernels_sha256():
+            return None
+        for k, v in fields.items():
+            if k.startswith(direction + "_valu_insts_"):
+                out[k[len(direction) + len("_valu_insts_"):]] = float(v)
+        return out or None
+    except (OSError, ValueError):
+        return None
+
+
+def time_calls(torch, stream, fn, reps, pre=None):
+    """Mean time of one call (ms) over `reps` back-to-back calls between two events.
+    Untimed calls run first with no idle gap before the timed ones (after idling,
+    the GPU runs its first milliseconds at a lower clock): `pre` of them, or by
+    default as many as fill about 8 ms."""
+    torch.cuda.synchronize()
+    if pre is None:
+        t0 = time.perf_counter()
+        fn()
+        torch.cuda.synchronize()
+        pre = min(200, max(1, int(8e-3 / max(time.perf_counter() - t0, 1e-6))))
+    for _ in range(pre):
+        fn()
     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     a.record(stream)
     for _ in range(reps):
@@ -227,8 +315,11 @@ def extras(F, W, torch, np, dev, stream, args):
     out4 = torch.empty_like(pt4)
     tags4 = torch.empty((F.num_chains(pt4.numel(), c4), 16), dtype=torch.uint8, device=dev)
     ms = time_calls(torch, stream, lambda: F.encrypt_tag(w4.key, w4.base_iv, c4, pt4, out=out4, tags=tags4), 20)
+    n4 = tags4.shape[0]
     res["encrypt_tag"] = {"workload": "fp32-gradients-256MiB, 256 KiB chains", "gbps": round(pt4.numel() / ms / 1e6, 1),
-                          "us": round(ms * 1e3, 1)}
+                          "us": round(ms * 1e3, 1),
+                          "hbm_frac": round((2 * pt4.numel() + 16 * n4) / ms / 1e6 / HBM_PEAK_GBS, 4),
+                          "note": "256 MiB in + 256 MiB out partly served by the 256 MB Infinity Cache"}
     log("encrypt+tag %.1f GB/s" % res["encrypt_tag"]["gbps"])
     del pt4, out4, tags4
 
@@ -237,12 +328,22 @@ def extras(F, W, torch, np, dev, stream, args):
     p2s = torch.from_numpy(w2s.payload).to(dev)
     o2s = torch.empty_like(p2s)
     esweep = {}
+    sq = sq_profile("encrypt") or {}
+    L2 = p2s.numel()
     for chain in w2s.chain_sizes:
         a2s = torch.from_numpy(w2s.aad(chain)).to(dev)
-        t2s = torch.empty((F.num_chains(p2s.numel(), chain), 16), dtype=torch.uint8, device=dev)
-        ms = time_calls(torch, stream, lambda: F.encrypt_tag(w2s.key, w2s.base_iv, chain, p2s, a2s, out=o2s, tags=t2s), 20)
-        esweep["%dKiB" % (chain // KiB)] = {"gbps": round(p2s.numel() / ms / 1e6, 1), "us": round(ms * 1e3, 1)}
-    res["encrypt_sweep"] = {"workload": "image-batch-64MiB, 32-byte AAD per chain", "sweep": esweep}
+        n2 = F.num_chains(L2, chain)
+        t2s = torch.empty((n2, 16), dtype=torch.uint8, device=dev)
+        enc = lambda: F.encrypt_tag(w2s.key, w2s.base_iv, chain, p2s, a2s, out=o2s, tags=t2s)
+        ms = sorted(time_calls(torch, stream, enc, 20) for _ in range(3))[1]
+        name = "%dKiB" % (chain // KiB)
+        e = {"gbps": round(L2 / ms / 1e6, 1), "us": round(ms * 1e3, 1),
+             "hbm_frac": round((2 * L2 + n2 * (32 + 16)) / ms / 1e6 / HBM_PEAK_GBS, 4)}
+        if name in sq:
+            e["valu_frac"] = round(sq[name] * 64 / (ms * 1e-3) / 1e12 / ALU_PEAK_TOPS, 3)
+        esweep[name] = e
+    res["encrypt_sweep"] = {"workload": "image-batch-64MiB, 32-byte AAD per chain", "sweep": esweep,
+                            "valu_frac_source": os.path.basename(SQ_FILE) if sq else None}
     log("encrypt sweep:", esweep)
     del p2s, o2s
 
@@ -260,6 +361,10 @@ def extras(F, W, torch, np, dev, stream, args):
             assert bool(k1.all())
             seq["%s_%dKiB" % (name, chain // KiB)] = {"us": round(ms * 1e3, 1),
                                                       "gbps": round(p1.numel() / ms / 1e6, 2)}
+    for chain in w1.chain_sizes:
+        k = "%dKiB" % (chain // KiB)
+        seq["sequential_over_multi_chain_%s" % k] = round(seq["sequential_ghash_" + k]["us"] / seq["multi_chain_" + k]["us"], 1)
+    seq["paper_multi_chain_gain"] = "5-15x (section 5.2; 16 tags per item up to 16x, section 6.4), context only"
     res["config1_1MiB"] = seq
     log("1 MiB:", seq)
 
@@ -392,21 +497,26 @@ def hip_runtime_path():
 
 def pipeline(F, W, torch, np, dev):
     length, chain, chunk = 4 * GiB, MiB, 8 * MiB
-    rng = W.rng_for(5)
-    key, iv = W.draw_key_iv(rng)
-    # Seeded bytes (a 64 MiB random block tiled), encrypted on the GPU: the bench
-    # times the path; correctness of this path is established by the tests.
-    block = torch.from_numpy(np.frombuffer(rng.bytes(64 * MiB), np.uint8).copy())
+    # The 4 GiB of seeded bytes of the pipelined workload, generated straight into
+    # pinned memory, then encrypted by this library's encrypt + tag (the timed legs
+    # never run the CPU oracle; the parity tests check this path against the
+    # oracle's own encryption of the same bytes).
+    h_pt = torch.empty(length, dtype=torch.uint8, pin_memory=True)
+    w5 = W.config5(length, out=h_pt.numpy())
+    key, iv = w5.key, w5.base_iv
     h_ct = torch.empty(length, dtype=torch.uint8, pin_memory=True)
     n = F.num_chains(length, chain)
     h_tags = torch.empty((n, 16), dtype=torch.uint8)
-    d_pt = block.to(dev).repeat(length // block.numel())
+    d_pt = h_pt.to(dev)
+    del h_pt
     d_ct, d_tags = F.encrypt_tag(key, iv, chain, d_pt)
     h_ct.copy_(d_ct)
     h_tags.copy_(d_tags)
     del d_ct, d_tags
     torch.cuda.synchronize()
-    res = {"workload": "uniform-4GiB (seeded 64 MiB block tiled), 1 MiB chains, 8 MiB chunks"}
+    res = {"workload": "uniform-4GiB: 4 GiB of seeded bytes in pinned memory, 1 MiB chains, 8 MiB chunks",
+           "input": "the workload's bytes encrypted on the GPU by this library's encrypt+tag (the parity tests "
+                    "use the oracle's encryption of the same bytes)"}
     stage = torch.empty(F.stage_bytes(length, chain, 0, chunk, 3), dtype=torch.uint8, device=dev)
     out = torch.empty(length, dtype=torch.uint8, device=dev)
     ok = torch.empty(n, dtype=torch.uint8, device=dev)

@@ -330,6 +330,18 @@ int fastrack_gcm_encrypt_tag_ragged(const uint8_t *key, const uint8_t *base_iv, 
 uint64_t fastrack_sample_chains(const uint64_t *h_sample_len, uint64_t n_samples, uint32_t chains_per_sample,
                                 uint64_t *h_chain_off, uint64_t *h_chain_len);
 
+/*
+ * Measurement helper, not part of the method: enqueues on `stream` one wave per
+ * probe (n_probes in 1..1024; probes go to the XCDs in turn) that sleeps for
+ * window_us microseconds of real time (1..10^7) and writes to d_out[2p] the
+ * shader-clock cycles and to d_out[2p+1] the 100 MHz real-time ticks that
+ * elapsed, so cycles / (ticks / 100 MHz) is the shader clock over the window.
+ * Launched on a second stream beside other work, it measures the clock that
+ * work runs at (each probe holds one wave slot and almost no issue cycles).
+ * EINVAL: NULL d_out, n_probes or window_us out of range.
+ */
+int fastrack_clock_probe(uint64_t window_us, uint32_t n_probes, uint64_t *d_out, void *stream);
+
 /* Message of the last failure on this thread ("" if none). */
 const char *fastrack_last_error(void);
 

@@ -15,7 +15,7 @@ import torch as _torch  # loads the HIP runtime that the library then shares
 from . import build as _build
 
 __all__ = ["FastrackError", "decrypt_verify", "decrypt_verify_noalloc", "encrypt_tag", "decrypt_eager", "Eager", "keystream", "apply_verify",
-           "pipeline_h2d", "pipeline_d2h", "decrypt_verify_ragged", "encrypt_tag_ragged", "sample_chains", "num_chains", "stage_bytes", "shutdown", "library_path", "F_SEQ_GHASH", "PIPE_FUSED",
+           "pipeline_h2d", "pipeline_d2h", "decrypt_verify_ragged", "encrypt_tag_ragged", "sample_chains", "num_chains", "stage_bytes", "shutdown", "clock_probe", "clock_ghz", "library_path", "F_SEQ_GHASH", "PIPE_FUSED",
            "PIPE_EAGER", "PIPE_OTP", "PIPE_DIRECT"]
 
 F_SEQ_GHASH = 1
@@ -81,6 +81,8 @@ def lib():
         L.fastrack_gcm_encrypt_tag_ragged.restype = _ct.c_int
         L.fastrack_sample_chains.argtypes = [vp, u64, u32, vp, vp]
         L.fastrack_sample_chains.restype = u64
+        L.fastrack_clock_probe.argtypes = [u64, u32, vp, vp]
+        L.fastrack_clock_probe.restype = _ct.c_int
         L.fastrack_last_error.restype = _ct.c_char_p
         L.fastrack_shutdown.restype = None
         _lib = L
@@ -519,6 +521,23 @@ def encrypt_tag_ragged(key, base_iv, chain_off, chain_len, pt, aad=None, out=Non
                                                      aad_bytes, _dptr(out), _dptr(tags), _stream(stream)))
         _used_on(new, [stream], dev)
     return out, tags
+
+
+def clock_probe(window_us, n_probes=8, stream=None, device=None):
+    """Measurement helper: enqueue the shader-clock probe (one sleeping wave per probe
+    for window_us of real time). Returns a uint64 tensor (n_probes, 2) of (shader
+    cycles, 100 MHz ticks); read it once the stream is done (see clock_ghz)."""
+    dev = _torch.device("cuda", _torch.cuda.current_device()) if device is None else _torch.device(device)
+    out = _torch.zeros((n_probes, 2), dtype=_torch.int64, device=dev)
+    with _torch.cuda.device(dev):
+        _check(lib().fastrack_clock_probe(int(window_us), int(n_probes), out.data_ptr(), _stream(stream)))
+    return out
+
+
+def clock_ghz(probe):
+    """Shader clock in GHz of each probe of a finished clock_probe result."""
+    c = probe.cpu().double()
+    return (c[:, 0] / (c[:, 1] / 1e8) / 1e9).tolist()
 
 
 def shutdown():

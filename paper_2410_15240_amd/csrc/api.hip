@@ -1325,6 +1325,17 @@ FT_EXPORT uint64_t fastrack_sample_chains(const uint64_t *h_sample_len, uint64_t
     return off;
 }
 
+FT_EXPORT int fastrack_clock_probe(uint64_t window_us, uint32_t n_probes, uint64_t *d_out, void *stream)
+{
+    g_err.clear();
+    if (!d_out || n_probes == 0 || n_probes > 1024)
+        return fail(FASTRACK_EINVAL, "d_out must be non-NULL and n_probes in 1..1024 (got %u)", n_probes);
+    if (window_us == 0 || window_us > 10000000)
+        return fail(FASTRACK_EINVAL, "window_us must be in 1..10^7 (got %llu)", (unsigned long long)window_us);
+    hipError_t he = launch_clock_probe(window_us * 100, n_probes, d_out, reinterpret_cast<hipStream_t>(stream));
+    return he == hipSuccess ? FASTRACK_OK : hip_fail(he, "clock probe launch");
+}
+
 FT_EXPORT void fastrack_shutdown(void)
 {
     std::lock_guard<std::mutex> lk(g_mu);

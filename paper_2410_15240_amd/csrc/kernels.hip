@@ -1193,6 +1193,33 @@ hipError_t launch_gcm(const GcmLaunch &p, bool encrypt, GcmMode mode, int num_cu
     return hipErrorInvalidValue;
 }
 
+// Measurement helper (not part of the method): the shader clock over a window
+// of real time. One wave per workgroup; lane 0 reads the shader-cycle counter
+// (s_memtime) and the fixed 100 MHz counter (s_memrealtime) at both ends of a
+// sleep loop that lasts `ticks` of the 100 MHz counter (or at most 2^26
+// polls), so it ends whatever else runs. Workgroups go to the XCDs in turn.
+__global__ __launch_bounds__(64) void clock_probe_kernel(uint64_t ticks, uint64_t *__restrict__ out)
+{
+    if (threadIdx.x != 0)
+        return;
+    const uint64_t c0 = __builtin_amdgcn_s_memtime();
+    const uint64_t r0 = __builtin_amdgcn_s_memrealtime();
+    uint64_t r1 = r0;
+    for (uint32_t i = 0; i < (1u << 26) && r1 - r0 < ticks; ++i) {
+        __builtin_amdgcn_s_sleep(20);
+        r1 = __builtin_amdgcn_s_memrealtime();
+    }
+    const uint64_t c1 = __builtin_amdgcn_s_memtime();
+    out[2 * blockIdx.x] = c1 - c0;
+    out[2 * blockIdx.x + 1] = r1 - r0;
+}
+
+hipError_t launch_clock_probe(uint64_t ticks, uint32_t n_wg, uint64_t *out, hipStream_t s)
+{
+    hipLaunchKernelGGL(clock_probe_kernel, dim3(n_wg), dim3(64), 0, s, ticks, out);
+    return hipGetLastError();
+}
+
 hipError_t launch_seq_ghash(const GcmLaunch &p, bool encrypt, hipStream_t s)
 {
     const uint32_t wgs = (p.n_chains + 255) / 256;

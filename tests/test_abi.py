@@ -84,6 +84,14 @@ def test_encrypt_rejects_bad_arguments(L, kw):
     assert enc(L, **kw) == -1
 
 
+@pytest.mark.parametrize("args", [(0, 8, 0x1000), (10 ** 7 + 1, 8, 0x1000), (100, 0, 0x1000), (100, 1025, 0x1000),
+                                  (100, 8, None)])
+def test_clock_probe_rejects_bad_arguments(L, args):
+    """The shader-clock probe checks its window, probe count and output pointer before any launch."""
+    window, n, out = args
+    assert L.fastrack_clock_probe(window, n, out, None) == -1
+
+
 def test_zero_length_is_a_no_op(L):
     assert dec(L, length=0) == 0
     assert enc(L, length=0) == 0
