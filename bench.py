@@ -51,6 +51,8 @@ def main():
     ap.add_argument("--skip-extras", action="store_true", help="only the timed decrypt sweep")
     ap.add_argument("--pipeline-only", action="store_true",
                     help="only the 4 GiB pipeline leg; prints its results as one JSON line (for tracing)")
+    ap.add_argument("--formulation-only", action="store_true",
+                    help="only the T-table against bitsliced keystream leg; one JSON line (for profiling)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: the path is per-GPU and shards by whole chains with no exchange "
@@ -72,6 +74,9 @@ def main():
     stream = torch.cuda.current_stream()
     if args.pipeline_only:
         print(json.dumps(pipeline(F, W, torch, np, dev)), flush=True)
+        return
+    if args.formulation_only:
+        print(json.dumps(aes_formulation(F, W, torch, dev, stream)), flush=True)
         return
 
     # ---------------- inputs (config: image batch, chain sweep) ----------------
@@ -216,7 +221,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gcm_decrypt_image-batch-64MiB_tra
 # everything that shapes the kernels' machine code
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2410_15240_amd", *p) for p in
                (("csrc", "kernels.hip"), ("csrc", "aes_dev.h"), ("csrc", "gf128_dev.h"), ("csrc", "keyctx.h"),
-                ("csrc", "launch.h"), ("build.py",))]
+                ("csrc", "launch.h"), ("csrc", "chain_dev.h"), ("build.py",))]
 
 
 def kernels_sha256():
@@ -436,6 +441,7 @@ def extras(F, W, torch, np, dev, stream, args):
     apply_ms = time_calls(torch, stream, lambda: F.apply_verify(w2.key, w2.base_iv, MiB, c5, ks5, t5, out=o5, ok=k5), 50)
     assert bool(k5.all()) and torch.equal(o5, p5)
     fused5_ms = time_calls(torch, stream, lambda: F.decrypt_verify(w2.key, w2.base_iv, MiB, c5, t5, out=o5, ok=k5), 50)
+    res["aes_formulation"] = aes_formulation(F, W, torch, dev, stream)
     res["otp"] = {"workload": "8 MiB chunk, 1 MiB chains", "keystream_us": round(ks_ms * 1e3, 1),
                   "after_arrival_fused_us": round(fused5_ms * 1e3, 1),
                   "after_arrival_apply_us": round(apply_ms * 1e3, 1)}
@@ -482,6 +488,24 @@ def extras(F, W, torch, np, dev, stream, args):
     if not args.skip_pipeline:
         res["pipeline_h2d"] = pipeline(F, W, torch, np, dev)
     return res
+
+
+def aes_formulation(F, W, torch, dev, stream):
+    """The two AES formulations on the same keystream (64 MiB of the image-batch key
+    and IV, 1 MiB and 64 KiB chains): T-tables in LDS against the bitsliced circuit."""
+    w = W.config2()
+    form = {}
+    ks = torch.empty(64 * MiB, dtype=torch.uint8, device=dev)
+    for chain in (MiB, 64 * KiB):
+        ref = F.keystream(w.key, w.base_iv, chain, 64 * MiB)
+        t_ms = time_calls(torch, stream, lambda: F.keystream(w.key, w.base_iv, chain, 64 * MiB, out=ks), 20)
+        b_ms = time_calls(torch, stream, lambda: F.keystream(w.key, w.base_iv, chain, 64 * MiB, out=ks,
+                                                            bitsliced=True), 20)
+        assert torch.equal(ks, ref), "bitsliced keystream differs from the T-table keystream"
+        form["%dKiB" % (chain // KiB)] = {"ttable_us": round(t_ms * 1e3, 1), "bitsliced_us": round(b_ms * 1e3, 1),
+                                          "bitsliced_over_ttable": round(b_ms / t_ms, 3)}
+    log("aes formulation:", form)
+    return {"workload": "64 MiB keystream (no data read)", "by_chain": form}
 
 
 def hip_runtime_path():

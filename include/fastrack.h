@@ -154,6 +154,16 @@ int fastrack_gcm_decrypt_eager(const uint8_t *key, const uint8_t *base_iv, uint6
  */
 int fastrack_gcm_keystream(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes, uint64_t chain_base,
                            uint64_t len, uint8_t *d_ks, void *stream);
+/*
+ * The same keystream as fastrack_gcm_keystream (same arguments, same output,
+ * same errors), computed by a bitsliced AES-256 (FIPS-197 rounds as Boolean
+ * circuits on 32 blocks per 32-bit lane, no table lookups) instead of the
+ * T-table kernel: the alternative AES formulation, kept to compare the two on
+ * this GPU. A wave pass covers 2048 consecutive blocks of one chain, so chains
+ * much shorter than 32 KiB leave most of a pass idle.
+ */
+int fastrack_gcm_keystream_bitsliced(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                                     uint64_t chain_base, uint64_t len, uint8_t *d_ks, void *stream);
 int fastrack_gcm_apply_verify(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes, uint64_t chain_base,
                               const uint8_t *d_ct, uint64_t len, const uint8_t *d_ks, const uint8_t *d_tags,
                               const uint8_t *d_aad, uint32_t aad_bytes, uint8_t *d_pt, uint8_t *d_ok,

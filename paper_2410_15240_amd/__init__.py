@@ -73,6 +73,8 @@ def lib():
         L.fastrack_gcm_decrypt_eager.restype = _ct.c_int
         L.fastrack_gcm_keystream.argtypes = [u8p, u8p, u64, u64, u64, u8p, vp]
         L.fastrack_gcm_keystream.restype = _ct.c_int
+        L.fastrack_gcm_keystream_bitsliced.argtypes = [u8p, u8p, u64, u64, u64, u8p, vp]
+        L.fastrack_gcm_keystream_bitsliced.restype = _ct.c_int
         L.fastrack_gcm_apply_verify.argtypes = [u8p, u8p, u64, u64, u8p, u64, u8p, u8p, u8p, u32, u8p, u8p, vp]
         L.fastrack_gcm_apply_verify.restype = _ct.c_int
         L.fastrack_gcm_decrypt_verify_ragged.argtypes = [u8p, u8p, vp, vp, u64, u8p, u8p, u8p, u32, u8p, u8p, vp]
@@ -319,8 +321,9 @@ def decrypt_eager(key, base_iv, chain_bytes, ct, tags, aad=None, out=None, ok=No
     return Eager(out, ok, ev)
 
 
-def keystream(key, base_iv, chain_bytes, length, chain_base=0, out=None, stream=None, device=None):
-    """The CTR keystream of chains chain_base.. covering `length` bytes (a uint8 CUDA tensor)."""
+def keystream(key, base_iv, chain_bytes, length, chain_base=0, out=None, stream=None, device=None, bitsliced=False):
+    """The CTR keystream of chains chain_base.. covering `length` bytes (a uint8 CUDA tensor).
+    bitsliced=True computes it with the bitsliced AES kernel instead of the T-table one."""
     new = []
     if out is None:
         device = _torch.device("cuda", _torch.cuda.current_device()) if device is None else _torch.device(device)
@@ -328,8 +331,9 @@ def keystream(key, base_iv, chain_bytes, length, chain_base=0, out=None, stream=
         new.append(out)
     _u8(out, "out", min_numel=length)
     with _torch.cuda.device(out.device):
-        _check(lib().fastrack_gcm_keystream(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"),
-                                            chain_bytes, chain_base, length, _dptr(out), _stream(stream)))
+        fn = lib().fastrack_gcm_keystream_bitsliced if bitsliced else lib().fastrack_gcm_keystream
+        _check(fn(_host_bytes(key, 32, "key"), _host_bytes(base_iv, 12, "base_iv"), chain_bytes, chain_base, length,
+                  _dptr(out), _stream(stream)))
         _used_on(new, [stream], out.device)
     return out
 

@@ -11,7 +11,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "_lib")
 LIB = os.path.join(OUT_DIR, "libfastrack.so")
-SOURCES = ["kernels.hip", "api.hip"]
+# Each source with the LLVM scheduling flags it is built with (see below).
+SOURCES = [("kernels.hip", True), ("api.hip", True), ("bitslice.hip", False)]
 ARCH = "gfx950"
 
 
@@ -25,25 +26,39 @@ def hipcc() -> str:
 def build(verbose: bool = False) -> str:
     os.makedirs(OUT_DIR, exist_ok=True)
     tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [hipcc(), "--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-shared", "-fvisibility=hidden",
-           # keep hipcc from forming packed-FP32 instructions (this code has no FP, the flag is policy)
-           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           # LLVM's iterative max-occupancy scheduler keeps 4-8 table lookups in
-           # flight per wave in the AES rounds; the default strategy serialises
-           # them to 1-2 once the kernel's live state grows.
-           "-mllvm", "--amdgpu-sched-strategy=iterative-maxocc",
-           "-I", os.path.join(ROOT, "include"), "-I", CSRC]
-    cmd += [os.path.join(CSRC, s) for s in SOURCES]
-    cmd += ["-o", tmp, "-Wl,-rpath,/opt/rocm/lib"]
+    base = [hipcc(), "--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",
+            # keep hipcc from forming packed-FP32 instructions (this code has no FP, the flag is policy)
+            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+            "-I", os.path.join(ROOT, "include"), "-I", CSRC]
+    # LLVM's iterative max-occupancy scheduler keeps 4-8 table lookups in flight
+    # per wave in the T-table AES rounds; the default strategy serialises them to
+    # 1-2 once the kernel's live state grows. The bitsliced kernel (no lookups, a
+    # 128-word state) is built with the default strategy, which keeps its rounds
+    # free of register spills.
+    maxocc = ["-mllvm", "--amdgpu-sched-strategy=iterative-maxocc"]
+    noise = "is not a recognized feature for this target"
+    objs, procs = [], []
+    for src, sched in SOURCES:
+        obj = os.path.join(OUT_DIR, src.replace(".hip", ".o.tmp%d" % os.getpid()))
+        cmd = base + (maxocc if sched else []) + ["-c", os.path.join(CSRC, src), "-o", obj]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)))
+        objs.append(obj)
+    for src, pr in procs:
+        out = "\n".join(l for l in pr.communicate()[0].splitlines() if noise not in l)
+        if pr.returncode != 0:
+            raise RuntimeError("hipcc failed on %s:\n%s" % (src, out))
+        if verbose and out.strip():
+            print(out)
+    cmd = [hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC"] + objs + ["-o", tmp, "-Wl,-rpath,/opt/rocm/lib"]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)
-    noise = "is not a recognized feature for this target"
-    out = "\n".join(l for l in r.stdout.splitlines() if noise not in l)
+    for o in objs:
+        os.remove(o)
     if r.returncode != 0:
-        raise RuntimeError("hipcc failed:\n" + out)
-    if verbose and out.strip():
-        print(out)
+        raise RuntimeError("hipcc link failed:\n" + r.stdout)
     os.replace(tmp, LIB)
     return LIB
 

@@ -638,6 +638,31 @@ FT_EXPORT int fastrack_gcm_keystream(const uint8_t *key, const uint8_t *base_iv,
                    nullptr, nullptr, nullptr, 0, dev, ncu, s);
 }
 
+FT_EXPORT int fastrack_gcm_keystream_bitsliced(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
+                                               uint64_t chain_base, uint64_t len, uint8_t *d_ks, void *stream)
+{
+    g_err.clear();
+    int rc = check_common(key, base_iv, chain_bytes, len, d_ks, d_ks, nullptr, 0, 0);
+    if (rc || len == 0)
+        return rc;
+    std::lock_guard<std::mutex> lk(g_mu);
+    int dev, ncu;
+    if ((rc = current_device(&dev, &ncu)))
+        return rc;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    const KeyCtx *ctx;
+    if ((rc = key_ctx(key, s, dev, &ctx)))
+        return rc;
+    GcmLaunch p;
+    std::memset(&p, 0, sizeof p);
+    make_plan(len, chain_bytes, chain_base, (uint64_t)ncu * kGcmWavesPerWg, p);
+    p.ctx = ctx;
+    p.out = d_ks;
+    iv_words(base_iv, p.iv);
+    hipError_t he = launch_bs_keystream(p, ncu, s);
+    return he == hipSuccess ? FASTRACK_OK : hip_fail(he, "bitsliced keystream launch");
+}
+
 FT_EXPORT int fastrack_gcm_apply_verify(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
                                         uint64_t chain_base, const uint8_t *d_ct, uint64_t len, const uint8_t *d_ks,
                                         const uint8_t *d_tags, const uint8_t *d_aad, uint32_t aad_bytes,

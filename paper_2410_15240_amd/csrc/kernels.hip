@@ -37,6 +37,7 @@
 #include <stdint.h>
 
 #include "aes_dev.h"
+#include "chain_dev.h"
 #include "gf128_dev.h"
 #include "keyctx.h"
 #include "launch.h"
@@ -185,44 +186,6 @@ hipError_t launch_key_setup(const uint32_t key_words[8], KeyCtx *ctx, hipStream_
 // Shared per-chain pieces
 // ===========================================================================
 
-__device__ __forceinline__ u4 zero4()
-{
-    u4 z = {{0u, 0u, 0u, 0u}};
-    return z;
-}
-
-// Little-endian word form of the 96-bit IV of global chain i:
-// base_IV xor (0^32 || [i]_64), the index big-endian in IV bytes 4..11.
-__device__ __forceinline__ void chain_iv(const GcmLaunch &p, uint64_t gchain, uint32_t iv[3])
-{
-    iv[0] = p.iv[0];
-    iv[1] = p.iv[1] ^ bswap32((uint32_t)(gchain >> 32));
-    iv[2] = p.iv[2] ^ bswap32((uint32_t)gchain);
-}
-
-// Load n (<= 16) bytes as a zero-padded block (constant register indices only).
-__device__ inline u4 load_bytes(const uint8_t *src, uint32_t n)
-{
-    u4 r = zero4();
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int b = 0; b < 4; ++b)
-            if ((uint32_t)(4 * j + b) < n)
-                r.w[j] |= (uint32_t)src[4 * j + b] << (8 * b);
-    return r;
-}
-
-__device__ inline void store_bytes(uint8_t *dst, const u4 &v, uint32_t n)
-{
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int b = 0; b < 4; ++b)
-            if ((uint32_t)(4 * j + b) < n)
-                dst[4 * j + b] = (uint8_t)(v.w[j] >> (8 * b));
-}
-
 // Position of an item: chain, segment s of S, the block range [b, e) of the
 // segment in the chain's q blocks, and the chain's byte offset, length and
 // final partial-block bytes.
@@ -293,7 +256,7 @@ constexpr int kTreeLds = 3;                  // of which levels 0..2 in LDS (the
 constexpr uint32_t kGhBase = 4096;           // uint4 index of the GHASH table (64 KiB)
 constexpr uint32_t kTreeBase = 8192;         // uint4 index of the tree tables (128 KiB)
 constexpr uint32_t kWgTagBase = (128 + 8 * kTreeLds) * 1024 / 16;   // uint4 index: 16 partials, 16 masks
-static_assert(kWavesPerWg == 16, "one workgroup-combine slot per wave");
+static_assert(kWavesPerWg <= 16 && kWavesPerWg % 4 == 0, "one workgroup-combine slot per wave");
 constexpr uint32_t kLdsBytes = (128 + 8 * kTreeLds) * 1024 + 512 + 64;
 // Modes without data AES: the GHASH table, T0 (for the J0 masks) and all six tree tables.
 constexpr uint32_t kT0GhashOnly = 4096;         // uint4 index: 64 KiB
@@ -306,6 +269,11 @@ constexpr uint32_t kProgBaseGhashOnly = kLdsGhashOnly / 4 - 16;
 
 
 #define FT_SEL(k) (0x0C020400u + ((uint32_t)(k) << 8))
+
+// The streamed data blocks are read and written with non-temporal (nt) vector
+// accesses: each byte is touched once, so they should not displace the key
+// tables and partials from the L2 (1.4-2.2% per 64 MiB launch in an A/B run).
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ uint32_t tlk(const char *lds, uint32_t word, uint32_t lanec, uint32_t sel)
 {
@@ -634,8 +602,8 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
             for (int i = tid; i < 256; i += kThreads)
                 t0l[i] = c->t0[i];
         }
-        if (tid < 16)
-            reinterpret_cast<uint32_t *>(lds4)[kProg + tid] = 0u;
+        if (tid < 16)   // slot 4 s + m: the m-th wave of SIMD s; slots no wave uses never hold anyone back
+            reinterpret_cast<uint32_t *>(lds4)[kProg + tid] = (tid & 3) < kWavesPerWg / 4 ? 0u : 0xFFFFFFFFu;
         if (kGhash) {   // all loads of the 32 KiB GHASH table and the tree tables first, then the stores
             const uint4 *g = reinterpret_cast<const uint4 *>(c->g16[(L >> 3) - 1]);
             const uint4 *sq = reinterpret_cast<const uint4 *>(c->sq_tab);
@@ -819,7 +787,7 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
             u4 x = zero4();
             if (q.active) {
                 if (!q.partial) {
-                    const uint4 y = reinterpret_cast<const uint4 *>(base)[q.t];
+                    const v4u y = __builtin_nontemporal_load(reinterpret_cast<const v4u *>(base) + q.t);
                     x.w[0] = y.x; x.w[1] = y.y; x.w[2] = y.z; x.w[3] = y.w;
                 } else {
                     x = load_bytes(base + 16ull * q.t, tail);
@@ -883,7 +851,8 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
             }
             if (kWrite && q.active) {
                 if (!q.partial) {
-                    reinterpret_cast<uint4 *>(dst)[t] = make_uint4(o.w[0], o.w[1], o.w[2], o.w[3]);
+                    const v4u ov = {o.w[0], o.w[1], o.w[2], o.w[3]};
+                    __builtin_nontemporal_store(ov, reinterpret_cast<v4u *>(dst) + t);
                 } else {
                     store_bytes(dst + 16ull * t, o, tail);
                 }

@@ -95,5 +95,7 @@ hipError_t launch_key_setup(const uint32_t key_words[8], KeyCtx *ctx, hipStream_
 hipError_t launch_gcm(const GcmLaunch &p, bool encrypt, GcmMode mode, int num_cu, hipStream_t s);
 hipError_t launch_seq_ghash(const GcmLaunch &p, bool encrypt, hipStream_t s);
 hipError_t launch_clock_probe(uint64_t ticks, uint32_t n_wg, uint64_t *out, hipStream_t s);
+// Bitsliced keystream (bitslice.hip): the keystream of every chain of p, as kKeystream computes it.
+hipError_t launch_bs_keystream(const GcmLaunch &p, int num_cu, hipStream_t s);
 
 }  // namespace fastrack

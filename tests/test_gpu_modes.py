@@ -84,18 +84,33 @@ def test_eager_rejects_decrypting_in_place(F):
 
 
 KS_SHAPES = [(4096 * 5 + 7, 4096, 0), (4096 * 5 + 7, 4096, 3), (3 * 65536 + 16, 65536, 1), (1 * MiB, 1 * MiB, 0),
-             (8 * MiB + 48, 1 * MiB, 2), (5, 16, 7)]
+             (8 * MiB + 48, 1 * MiB, 2), (5, 16, 7),
+             # a chain one block past a 2048-block pass, a ragged last chain, one short chain
+             (3 * 32784 + 4099, 32784, 1), (32768 * 2 + 33, 32768, 0), (100, 96, 2)]
 
 
+@pytest.mark.parametrize("bitsliced", [False, True], ids=["ttable", "bitsliced"])
 @pytest.mark.parametrize("length,chain,base", KS_SHAPES)
-def test_keystream_is_the_ciphertext_of_zeros(F, length, chain, base):
-    say("keystream", length, chain, base)
+def test_keystream_is_the_ciphertext_of_zeros(F, length, chain, base, bitsliced):
+    say("keystream", length, chain, base, "bitsliced" if bitsliced else "ttable")
     w = W.random_case(length % 991 + base, 16, 16, 0)        # key and IV only
     total = base * chain + length
     zeros = np.zeros(total, np.uint8)
     ct_zero, _ = oracle.chains_encrypt(w.key, w.base_iv, chain, zeros)
-    ks = F.keystream(w.key, w.base_iv, chain, length, chain_base=base)
+    ks = F.keystream(w.key, w.base_iv, chain, length, chain_base=base, bitsliced=bitsliced)
     assert np.array_equal(host(ks), ct_zero[base * chain:])
+
+
+def test_bitsliced_keystream_far_chain_index(F):
+    """Chain indices above 2^32 reach the upper IV word: each chain is the oracle's
+    GCM encryption of zeros under its own IV_i."""
+    say("bitsliced keystream, chain base 2^32 + 3")
+    w = W.random_case(77, 16, 16, 0)
+    chain, base = 40960, (1 << 32) + 3
+    ks = host(F.keystream(w.key, w.base_iv, chain, 2 * chain, chain_base=base, bitsliced=True))
+    for j in range(2):
+        want, _ = oracle.gcm_encrypt(w.key, oracle.chain_iv(w.base_iv, base + j), bytes(chain))
+        assert np.array_equal(ks[j * chain:(j + 1) * chain], np.frombuffer(bytes(want), np.uint8))
 
 
 @pytest.mark.parametrize("length,chain,abytes", EAGER_SHAPES)

@@ -53,7 +53,7 @@ def test_library_host_paths_under_asan_ubsan(tmp_path):
                    "-Xarch_host", "-fno-sanitize-recover=all", "-Xarch_host", "-fno-omit-frame-pointer",
                    "-I", os.path.join(ROOT, "include"), "-I", CSRC,
                    os.path.join(SAN, "host_asan.cpp"), os.path.join(CSRC, "api.hip"),
-                   os.path.join(CSRC, "kernels.hip"), "-o", exe], timeout=600)
+                   os.path.join(CSRC, "kernels.hip"), os.path.join(CSRC, "bitslice.hip"), "-o", exe], timeout=600)
     assert rc == 0, out[-4000:]
     rc, out = run([exe], env=ENV, timeout=300)
     assert rc == 0 and "0 failures" in out and "Sanitizer" not in out, out[-4000:]
