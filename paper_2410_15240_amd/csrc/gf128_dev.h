@@ -86,6 +86,29 @@ __device__ inline u4 be_mul_xk_any(const u4 &y, int k)
     return be_mul_xk(be_mul_xk(y, 64), k - 64);
 }
 
+// X . Y for arbitrary X and Y in big-endian-word form, by one wave (setup only):
+// lane l adds Y . x^i for each set degree i in {l, l + 64} of X, and the wave
+// XOR-sums the 64 terms. Every lane returns the product. All lanes must be active.
+__device__ inline u4 wave_mul_be(const u4 &x, const u4 &y, uint32_t lane)
+{
+    u4 acc = {{0u, 0u, 0u, 0u}};
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const uint32_t i = lane + 64u * h;   // degree i: word i / 32, bit 31 - i % 32
+        const uint32_t w = i < 32 ? x.w[0] : (i < 64 ? x.w[1] : (i < 96 ? x.w[2] : x.w[3]));
+        if ((w >> (31 - (i & 31))) & 1u) {
+            const u4 t = be_mul_xk_any(y, (int)i);
+            for (int j = 0; j < 4; ++j)
+                acc.w[j] ^= t.w[j];
+        }
+    }
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1)
+        for (int j = 0; j < 4; ++j)
+            acc.w[j] ^= __shfl_xor(acc.w[j], d, 64);
+    return acc;
+}
+
 // ---- little-endian-word table multiplies -------------------------------
 
 // X . Y with Y's 4-bit positional table. Word j holds bytes 4j..4j+3, and

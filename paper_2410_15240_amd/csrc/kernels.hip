@@ -70,6 +70,12 @@ __device__ inline void build_tab4_row(const u4 &y, int p, Tab4 *out)
     }
 }
 
+// Key setup in two launches. key_setup_kernel (one workgroup) runs the short
+// dependent chain: the S-box and T0, the AES-256 key expansion, H = AES_K(0),
+// the powers H^1..H^65 (level by level, the products of a level spread over the
+// waves) and the squares H^(2^t) (25 squarings in turn), each product one wave
+// multiply. key_tables_kernel (many workgroups) then builds every table from
+// those powers, one table entry per thread.
 __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__restrict__ ctx)
 {
     __shared__ uint32_t s_sbox[256];
@@ -77,9 +83,9 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
     __shared__ uint32_t s_rk[60];
     __shared__ u4 s_hp[kMaxPow + 2];
     __shared__ u4 s_hsq[kSquares];
-    __shared__ u4 s_basis[8][128];
-    __shared__ Tab4 s_tab;
     const int tid = threadIdx.x;
+    const uint32_t lane = tid & 63, wave = (uint32_t)tid >> 6;
+    constexpr uint32_t kWaves = 1024 / 64;
 
     if (tid < 256) {
         uint32_t s = sbox_entry(tid);
@@ -111,66 +117,72 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
     }
     __syncthreads();
 
-    // Powers H^1..H^64 by doubling: with a table for H^(2^r), H^(2^r + j) = H^j . H^(2^r).
+    // Powers by doubling: H^(2^r + j) = H^j . H^(2^r), j = 1..2^r, the products of
+    // a level over the waves; then H^65 = H^64 . H.
     for (int r = 0; r < 6; ++r) {
-        const int half = 1 << r;
-        if (tid < kTab4Pos)
-            build_tab4_row(s_hp[half], tid, &s_tab);
-        __syncthreads();
-        if (tid < half)
-            s_hp[half + tid + 1] = mul_tab4(s_hp[tid + 1], &s_tab);
-        __syncthreads();
-    }
-    // H^65 = H^64 . H
-    if (tid < kTab4Pos)
-        build_tab4_row(s_hp[1], tid, &s_tab);
-    __syncthreads();
-    if (tid == 0)
-        s_hp[kMaxPow + 1] = mul_tab4(s_hp[kMaxPow], &s_tab);
-    __syncthreads();
-    // Squares H^(2^t): t <= 6 are already powers; the rest by repeated squaring.
-    if (tid <= 6)
-        s_hsq[tid] = s_hp[1 << tid];
-    __syncthreads();
-    for (int t = 7; t < kSquares; ++t) {
-        if (tid < kTab4Pos)
-            build_tab4_row(s_hsq[t - 1], tid, &s_tab);
-        __syncthreads();
-        if (tid == 0)
-            s_hsq[t] = mul_tab4(s_hsq[t - 1], &s_tab);
+        const uint32_t half = 1u << r;
+        for (uint32_t j = 1 + wave; j <= half; j += kWaves) {
+            const u4 prod = from_be(wave_mul_be(to_be(s_hp[j]), to_be(s_hp[half]), lane));
+            if (lane == 0)
+                s_hp[half + j] = prod;
+        }
         __syncthreads();
     }
+    if (wave == 0) {
+        const u4 prod = from_be(wave_mul_be(to_be(s_hp[kMaxPow]), to_be(s_hp[1]), lane));
+        if (lane == 0)
+            s_hp[kMaxPow + 1] = prod;
+        // Squares H^(2^t): t <= 6 are powers already; the rest by squaring in turn.
+        u4 sq = to_be(s_hp[1u << 6]);
+        if (lane < 7)
+            s_hsq[lane] = s_hp[1u << lane];
+        for (int t = 7; t < kSquares; ++t) {
+            sq = wave_mul_be(sq, sq, lane);
+            if (lane == 0)
+                s_hsq[t] = from_be(sq);
+        }
+    }
+    __syncthreads();
     for (int i = tid; i <= kMaxPow + 1; i += blockDim.x)
         for (int j = 0; j < 4; ++j)
             ctx->hp[i][j] = s_hp[i].w[j];
     for (int i = tid; i < kSquares; i += blockDim.x)
         for (int j = 0; j < 4; ++j)
             ctx->hsq[i][j] = s_hsq[i].w[j];
+}
 
-    // 4-bit tables: H and every H^(2^t).
-    for (int task = tid; task < (1 + kSquares) * kTab4Pos; task += blockDim.x) {
-        const int tbl = task / kTab4Pos, p = task % kTab4Pos;
-        if (tbl == 0)
-            build_tab4_row(s_hp[1], p, &ctx->h1_tab);
-        else
-            build_tab4_row(s_hsq[tbl - 1], p, &ctx->sq_tab[tbl - 1]);
-    }
+// The tables, one task per thread: a nibble position (16 entries) of the 4-bit
+// tables of H and of every H^(2^t), or one entry of the 8-bit positional tables
+// of H^8, H^16, ..., H^64:
+// g16[i][v][k] = (byte v at byte k) . H^(8 (i + 1)), v's bit 7 = degree 8k.
+constexpr uint32_t kTab4Tasks = (1 + kSquares) * kTab4Pos;
+constexpr uint32_t kTab8Entries = 8 * 16 * 256;
+constexpr uint32_t kTableThreads = 256;
 
-    // 8-bit positional tables of H^8, H^16, ..., H^64:
-    // g16[i][v][k] = (byte v at byte k) . H^(8 (i + 1)), v's bit 7 = degree 8k.
-    for (int b = tid; b < 8 * 128; b += blockDim.x)
-        s_basis[b >> 7][b & 127] = be_mul_xk_any(to_be(s_hp[8 * ((b >> 7) + 1)]), b & 127);
-    __syncthreads();
-    for (int ent = tid; ent < 8 * 16 * 256; ent += blockDim.x) {
-        const int i = ent >> 12, k = (ent >> 8) & 15, v = ent & 255;
-        u4 e = {{0u, 0u, 0u, 0u}};
-        for (int b = 0; b < 8; ++b)
-            if (v & (0x80 >> b))
-                e = xor4(e, s_basis[i][8 * k + b]);
-        const u4 le = from_be(e);
-        for (int j = 0; j < 4; ++j)
-            ctx->g16[i][v][k][j] = le.w[j];
+__global__ __launch_bounds__(kTableThreads) void key_tables_kernel(KeyCtx *__restrict__ ctx)
+{
+    const uint32_t task = blockIdx.x * kTableThreads + threadIdx.x;
+    if (task < kTab4Tasks) {
+        const uint32_t tbl = task / kTab4Pos, p = task % kTab4Pos;
+        const uint32_t *y = tbl == 0 ? ctx->h : ctx->hsq[tbl - 1];
+        build_tab4_row(u4{{y[0], y[1], y[2], y[3]}}, (int)p, tbl == 0 ? &ctx->h1_tab : &ctx->sq_tab[tbl - 1]);
+        return;
     }
+    const uint32_t ent = task - kTab4Tasks;
+    if (ent >= kTab8Entries)
+        return;
+    const uint32_t i = ent >> 12, k = (ent >> 8) & 15, v = ent & 255;
+    const uint32_t *hp = ctx->hp[8 * (i + 1)];
+    u4 b = be_mul_xk_any(to_be(u4{{hp[0], hp[1], hp[2], hp[3]}}), (int)(8 * k));   // degree 8k: v's bit 7
+    u4 e = {{0u, 0u, 0u, 0u}};
+    for (int bit = 7; bit >= 0; --bit) {
+        if ((v >> bit) & 1u)
+            e = xor4(e, b);
+        b = be_mul_xk(b, 1);
+    }
+    const u4 le = from_be(e);
+    for (int j = 0; j < 4; ++j)
+        ctx->g16[i][v][k][j] = le.w[j];
 }
 
 hipError_t launch_key_setup(const uint32_t key_words[8], KeyCtx *ctx, hipStream_t s)
@@ -179,6 +191,12 @@ hipError_t launch_key_setup(const uint32_t key_words[8], KeyCtx *ctx, hipStream_
     for (int i = 0; i < 8; ++i)
         a.key[i] = key_words[i];
     hipLaunchKernelGGL(key_setup_kernel, dim3(1), dim3(1024), 0, s, a, ctx);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess)
+        return e;
+    constexpr uint32_t kTasks = kTab4Tasks + kTab8Entries;
+    hipLaunchKernelGGL(key_tables_kernel, dim3((kTasks + kTableThreads - 1) / kTableThreads), dim3(kTableThreads), 0, s,
+                       ctx);
     return hipGetLastError();
 }
 
@@ -1062,40 +1080,55 @@ __device__ inline u4 j0_mask(const GcmLaunch &p, uint64_t gchain, LK T)
 }
 
 // The paper's baseline authentication: one thread per chain, Horner with H over
-// A, then every ciphertext block in order, then the length block.
+// A, then every ciphertext block in order, then the length block. Each step
+// multiplies by H through an 8-bit table of H in LDS (16 lookups), laid out and
+// read like the streaming kernel's table of H^L (value-major, the lanes' byte
+// positions rotated so that 16 lanes read 16 different bank groups), so the
+// baseline gets the same table machinery as the multi-chain path and differs
+// only in being one sequential chain per tag.
 template <bool ENC>
 __global__ __launch_bounds__(256) void seq_ghash_kernel(GcmLaunch p)
 {
+    __shared__ uint4 s_tab[4096];   // entry (position k, value v) at v * 16 + k: (byte v at byte k) . H
     __shared__ uint32_t s_t0[256];
-    s_t0[threadIdx.x] = p.ctx->t0[threadIdx.x];
+    const KeyCtx *__restrict__ c = p.ctx;
+    const Tab4 *h1 = &c->h1_tab;
+    for (uint32_t e = threadIdx.x; e < 4096; e += 256) {
+        const uint32_t v = e >> 4, k = e & 15;   // byte k: nibble positions 2k (high) and 2k+1 (low)
+        const uint4 hi = *reinterpret_cast<const uint4 *>(h1->e[2 * k][v >> 4]);
+        const uint4 lo = *reinterpret_cast<const uint4 *>(h1->e[2 * k + 1][v & 15]);
+        s_tab[e] = make_uint4(hi.x ^ lo.x, hi.y ^ lo.y, hi.z ^ lo.z, hi.w ^ lo.w);
+    }
+    s_t0[threadIdx.x] = c->t0[threadIdx.x];
     __syncthreads();
     const uint32_t chain = blockIdx.x * blockDim.x + threadIdx.x;
     if (chain >= p.n_chains)
         return;
-    const KeyCtx *__restrict__ c = p.ctx;
+    const char *lds = reinterpret_cast<const char *>(s_tab);
+    const GhLane gk = ghash_lane(threadIdx.x & 63, 0u);
+    auto mul_h = [&](const u4 &x) { return ghash_step(lds, x, zero4(), gk); };   // x . H
     const uint64_t gchain = p.chain_base + chain;
     const bool last = chain == p.n_chains - 1;
     const uint64_t len_i = last ? p.last_len : p.chain_bytes;
-    const Tab4 *hT = &c->h1_tab;
     u4 y = zero4();
     const uint8_t *a = p.aad + gchain * p.aad_bytes;
     for (uint32_t off = 0; off < p.aad_bytes; off += 16) {
         const uint32_t n = p.aad_bytes - off < 16 ? p.aad_bytes - off : 16;
-        y = mul_tab4(xor4(y, load_bytes(a + off, n)), hT);
+        y = mul_h(xor4(y, load_bytes(a + off, n)));
     }
     const uint8_t *ct = (ENC ? p.out : p.in) + (uint64_t)chain * p.chain_bytes;
     const uint64_t whole = len_i / 16;
     for (uint64_t t = 0; t < whole; ++t) {
         const uint4 x = reinterpret_cast<const uint4 *>(ct)[t];
         const u4 xv = {{x.x, x.y, x.z, x.w}};
-        y = mul_tab4(xor4(y, xv), hT);
+        y = mul_h(xor4(y, xv));
     }
     if (len_i & 15)
-        y = mul_tab4(xor4(y, load_bytes(ct + 16 * whole, (uint32_t)(len_i & 15))), hT);
+        y = mul_h(xor4(y, load_bytes(ct + 16 * whole, (uint32_t)(len_i & 15))));
     const uint64_t abits = (uint64_t)p.aad_bytes * 8, cbits = len_i * 8;
     const u4 lens = {{bswap32((uint32_t)(abits >> 32)), bswap32((uint32_t)abits), bswap32((uint32_t)(cbits >> 32)),
                       bswap32((uint32_t)cbits)}};
-    y = mul_tab4(xor4(y, lens), hT);
+    y = mul_h(xor4(y, lens));
     const u4 tag = xor4(y, j0_mask(p, gchain, [&](uint32_t x) { return s_t0[x]; }));
     emit_tag<ENC>(p, gchain, tag, ENC ? zero4() : load16(p.tags_in + 16 * gchain));
 }
