@@ -48,7 +48,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--skip-pipeline", action="store_true")
     ap.add_argument("--skip-cpu", action="store_true")
-    ap.add_argument("--skip-extras", action="store_true", help="only the timed decrypt sweep")
+    ap.add_argument("--skip-extras", action="store_true", help="only the timed decrypt sweep and the encrypt sweep")
     ap.add_argument("--pipeline-only", action="store_true",
                     help="only the 4 GiB pipeline leg; prints its results as one JSON line (for tracing)")
     ap.add_argument("--formulation-only", action="store_true",
@@ -210,6 +210,7 @@ def main():
                      "valu": valu},
     }
 
+    result["encrypt_sweep"] = encrypt_sweep(F, W, torch, dev, stream)
     if not args.skip_extras:
         result.update(extras(F, W, torch, np, dev, stream, args))
     if not args.skip_cpu:
@@ -311,24 +312,8 @@ def time_calls(torch, stream, fn, reps, pre=None):
     return a.elapsed_time(b) / reps
 
 
-def extras(F, W, torch, np, dev, stream, args):
-    res = {}
-    # encrypt + tag: fp32 gradients, 256 KiB chains
-    w4 = W.config4()
-    pt4 = torch.from_numpy(w4.payload).to(dev)
-    c4 = w4.chain_sizes[0]
-    out4 = torch.empty_like(pt4)
-    tags4 = torch.empty((F.num_chains(pt4.numel(), c4), 16), dtype=torch.uint8, device=dev)
-    ms = time_calls(torch, stream, lambda: F.encrypt_tag(w4.key, w4.base_iv, c4, pt4, out=out4, tags=tags4), 20)
-    n4 = tags4.shape[0]
-    res["encrypt_tag"] = {"workload": "fp32-gradients-256MiB, 256 KiB chains", "gbps": round(pt4.numel() / ms / 1e6, 1),
-                          "us": round(ms * 1e3, 1),
-                          "hbm_frac": round((2 * pt4.numel() + 16 * n4) / ms / 1e6 / HBM_PEAK_GBS, 4),
-                          "note": "256 MiB in + 256 MiB out partly served by the 256 MB Infinity Cache"}
-    log("encrypt+tag %.1f GB/s" % res["encrypt_tag"]["gbps"])
-    del pt4, out4, tags4
-
-    # encrypt + tag against chain size: the decrypt sweep's image batch and chain sizes
+def encrypt_sweep(F, W, torch, dev, stream):
+    """Encrypt + tag against chain size: the decrypt sweep's image batch and chain sizes."""
     w2s = W.config2()
     p2s = torch.from_numpy(w2s.payload).to(dev)
     o2s = torch.empty_like(p2s)
@@ -347,10 +332,27 @@ def extras(F, W, torch, np, dev, stream, args):
         if name in sq:
             e["valu_frac"] = round(sq[name] * 64 / (ms * 1e-3) / 1e12 / ALU_PEAK_TOPS, 3)
         esweep[name] = e
-    res["encrypt_sweep"] = {"workload": "image-batch-64MiB, 32-byte AAD per chain", "sweep": esweep,
-                            "valu_frac_source": os.path.basename(SQ_FILE) if sq else None}
     log("encrypt sweep:", esweep)
-    del p2s, o2s
+    return {"workload": "image-batch-64MiB, 32-byte AAD per chain", "sweep": esweep,
+            "valu_frac_source": os.path.basename(SQ_FILE) if sq else None}
+
+
+def extras(F, W, torch, np, dev, stream, args):
+    res = {}
+    # encrypt + tag: fp32 gradients, 256 KiB chains
+    w4 = W.config4()
+    pt4 = torch.from_numpy(w4.payload).to(dev)
+    c4 = w4.chain_sizes[0]
+    out4 = torch.empty_like(pt4)
+    tags4 = torch.empty((F.num_chains(pt4.numel(), c4), 16), dtype=torch.uint8, device=dev)
+    ms = time_calls(torch, stream, lambda: F.encrypt_tag(w4.key, w4.base_iv, c4, pt4, out=out4, tags=tags4), 20)
+    n4 = tags4.shape[0]
+    res["encrypt_tag"] = {"workload": "fp32-gradients-256MiB, 256 KiB chains", "gbps": round(pt4.numel() / ms / 1e6, 1),
+                          "us": round(ms * 1e3, 1),
+                          "hbm_frac": round((2 * pt4.numel() + 16 * n4) / ms / 1e6 / HBM_PEAK_GBS, 4),
+                          "note": "256 MiB in + 256 MiB out partly served by the 256 MB Infinity Cache"}
+    log("encrypt+tag %.1f GB/s" % res["encrypt_tag"]["gbps"])
+    del pt4, out4, tags4
 
     # the paper's sequential GHASH vs multi-chain, 1 MiB buffer
     w1 = W.config1()

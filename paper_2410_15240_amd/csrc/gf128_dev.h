@@ -86,6 +86,37 @@ __device__ inline u4 be_mul_xk_any(const u4 &y, int k)
     return be_mul_xk(be_mul_xk(y, 64), k - 64);
 }
 
+// Bit i of w moved to bit 2i + 1 of a 64-bit word (the other bits zero).
+__device__ __forceinline__ uint64_t spread_odd(uint32_t w)
+{
+    uint64_t x = w;
+    x = (x | (x << 16)) & 0x0000FFFF0000FFFFull;
+    x = (x | (x << 8)) & 0x00FF00FF00FF00FFull;
+    x = (x | (x << 4)) & 0x0F0F0F0F0F0F0F0Full;
+    x = (x | (x << 2)) & 0x3333333333333333ull;
+    x = (x | (x << 1)) & 0x5555555555555555ull;
+    return x << 1;
+}
+
+// Y^2 in big-endian-word form (setup only). Squaring is linear over GF(2): the
+// coefficient of degree d moves to degree 2d. With V = w0:w1:w2:w3 as a 128-bit
+// integer (degree d at bit 127 - d) the square is the 256-bit integer with bit p of
+// V at bit 2p + 1; its upper half holds degrees 0..127 and its lower half F the
+// degrees 128..255, which come back as F . x^128 = F . (1 + x + x^2 + x^7).
+__device__ inline u4 be_square(const u4 &y)
+{
+    const uint64_t h0 = spread_odd(y.w[0]), h1 = spread_odd(y.w[1]);
+    const uint64_t f0 = spread_odd(y.w[2]), f1 = spread_odd(y.w[3]);
+    const u4 f = {{(uint32_t)(f0 >> 32), (uint32_t)f0, (uint32_t)(f1 >> 32), (uint32_t)f1}};
+    const u4 a = be_mul_xk(f, 1), b = be_mul_xk(f, 2), c = be_mul_xk(f, 7);
+    u4 r;
+    r.w[0] = (uint32_t)(h0 >> 32) ^ f.w[0] ^ a.w[0] ^ b.w[0] ^ c.w[0];
+    r.w[1] = (uint32_t)h0 ^ f.w[1] ^ a.w[1] ^ b.w[1] ^ c.w[1];
+    r.w[2] = (uint32_t)(h1 >> 32) ^ f.w[2] ^ a.w[2] ^ b.w[2] ^ c.w[2];
+    r.w[3] = (uint32_t)h1 ^ f.w[3] ^ a.w[3] ^ b.w[3] ^ c.w[3];
+    return r;
+}
+
 // X . Y for arbitrary X and Y in big-endian-word form, by one wave (setup only):
 // lane l adds Y . x^i for each set degree i in {l, l + 64} of X, and the wave
 // XOR-sums the 64 terms. Every lane returns the product. All lanes must be active.

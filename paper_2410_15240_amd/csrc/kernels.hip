@@ -73,8 +73,8 @@ __device__ inline void build_tab4_row(const u4 &y, int p, Tab4 *out)
 // Key setup in two launches. key_setup_kernel (one workgroup) runs the short
 // dependent chain: the S-box and T0, the AES-256 key expansion, H = AES_K(0),
 // the powers H^1..H^65 (level by level, the products of a level spread over the
-// waves) and the squares H^(2^t) (25 squarings in turn), each product one wave
-// multiply. key_tables_kernel (many workgroups) then builds every table from
+// waves, each product one wave multiply) and the squares H^(2^t) (25 squarings
+// in turn, each a bit spread and a reduction). key_tables_kernel (many workgroups) then builds every table from
 // those powers, one table entry per thread.
 __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__restrict__ ctx)
 {
@@ -136,8 +136,8 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
         u4 sq = to_be(s_hp[1u << 6]);
         if (lane < 7)
             s_hsq[lane] = s_hp[1u << lane];
-        for (int t = 7; t < kSquares; ++t) {
-            sq = wave_mul_be(sq, sq, lane);
+        for (int t = 7; t < kSquares; ++t) {   // every lane squares the same value
+            sq = be_square(sq);
             if (lane == 0)
                 s_hsq[t] = from_be(sq);
         }
