@@ -2,6 +2,7 @@
 // table cache, per-stream scratch, work planning and the H2D pipeline.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <array>
 #include <cstdarg>
 #include <cstdio>
@@ -58,11 +59,12 @@ struct ScratchEntry {
     hipStream_t stream;
     void *ptr;
     size_t bytes;
-    // pinned host staging for the tables of ragged launches, and the event after
-    // the copy that last read it
-    void *host = nullptr;
-    size_t host_bytes = 0;
-    hipEvent_t host_read = nullptr;
+    // two pinned host staging buffers for the tables of ragged launches, used in
+    // turn, and for each the event after the copy that last read it
+    void *host[2] = {nullptr, nullptr};
+    size_t host_bytes[2] = {0, 0};
+    hipEvent_t host_read[2] = {nullptr, nullptr};
+    int cur = 0;
 };
 
 struct DevInfo {
@@ -204,7 +206,8 @@ int scratch_for(int dev, hipStream_t s, size_t bytes, void **out)
 }
 
 // Pinned host staging of at least `bytes` for (device, stream), free to overwrite:
-// the copy that last read it has completed.
+// the copy that last read it has completed. Two buffers are used in turn, so the
+// tables of the next call are written while the copy of the last one is pending.
 int staging_for(int dev, hipStream_t s, size_t bytes, uint8_t **out)
 {
     ScratchEntry *e = nullptr;
@@ -215,34 +218,37 @@ int staging_for(int dev, hipStream_t s, size_t bytes, uint8_t **out)
         g_scratch.push_back(ScratchEntry{dev, s, nullptr, 0});
         e = &g_scratch.back();
     }
+    e->cur ^= 1;
+    const int b = e->cur;
     hipError_t he;
-    if (e->host_read && (he = hipEventSynchronize(e->host_read)) != hipSuccess)
+    if (e->host_read[b] && (he = hipEventSynchronize(e->host_read[b])) != hipSuccess)
         return hip_fail(he, "hipEventSynchronize");
-    if (!e->host_read && (he = hipEventCreateWithFlags(&e->host_read, hipEventDisableTiming)) != hipSuccess) {
-        e->host_read = nullptr;
+    if (!e->host_read[b] && (he = hipEventCreateWithFlags(&e->host_read[b], hipEventDisableTiming)) != hipSuccess) {
+        e->host_read[b] = nullptr;
         return hip_fail(he, "hipEventCreate");
     }
-    if (e->host_bytes < bytes) {
-        if (e->host)
-            (void)hipHostFree(e->host);
-        e->host = nullptr;
-        e->host_bytes = 0;
-        if ((he = hipHostMalloc(&e->host, bytes, 0)) != hipSuccess) {
-            e->host = nullptr;
+    if (e->host_bytes[b] < bytes) {
+        if (e->host[b])
+            (void)hipHostFree(e->host[b]);
+        e->host[b] = nullptr;
+        e->host_bytes[b] = 0;
+        if ((he = hipHostMalloc(&e->host[b], bytes, hipHostMallocMapped)) != hipSuccess) {
+            e->host[b] = nullptr;
             return fail(FASTRACK_ENOMEM, "hipHostMalloc(%zu) for staging: %s", bytes, hipGetErrorString(he));
         }
-        e->host_bytes = bytes;
+        e->host_bytes[b] = bytes;
     }
-    *out = static_cast<uint8_t *>(e->host);
+    *out = static_cast<uint8_t *>(e->host[b]);
     return FASTRACK_OK;
 }
 
-// Record on `s` that the staging of (dev, s) has been read by the work queued so far.
+// Record on `s` that the staging buffer of (dev, s) handed out last has been read
+// by the work queued so far.
 int staging_read(int dev, hipStream_t s)
 {
     for (auto &x : g_scratch)
         if (x.dev == dev && x.stream == s) {
-            hipError_t he = hipEventRecord(x.host_read, s);
+            hipError_t he = hipEventRecord(x.host_read[x.cur], s);
             return he == hipSuccess ? FASTRACK_OK : hip_fail(he, "hipEventRecord");
         }
     return fail(FASTRACK_EHIP, "no staging for this stream");
@@ -1180,6 +1186,7 @@ int run_ragged(bool encrypt, const uint8_t *key, const uint8_t *base_iv, const u
     if (n > 0xFFFFFFFFull)
         return fail(FASTRACK_EINVAL, "more than 2^32-1 chains");
     uint64_t end = 0, blocks = 0, qmax = 0;
+    std::vector<uint32_t> q(n);   // blocks of each chain (a partial block counts as one)
     for (uint64_t i = 0; i < n; ++i) {
         if (h_off[i] & 15)
             return fail(FASTRACK_EINVAL, "chain %llu starts at offset %llu, not a multiple of 16", (unsigned long long)i,
@@ -1190,9 +1197,9 @@ int run_ragged(bool encrypt, const uint8_t *key, const uint8_t *base_iv, const u
         if ((h_len[i] + 15) / 16 > kMaxChainBlocks)
             return fail(FASTRACK_EINVAL, "chain %llu is longer than (2^32-2)*16 bytes", (unsigned long long)i);
         end = h_off[i] + h_len[i];
-        const uint64_t q = (h_len[i] + 15) / 16;
-        blocks += q;
-        qmax = q > qmax ? q : qmax;
+        q[i] = (uint32_t)((h_len[i] + 15) / 16);
+        blocks += q[i];
+        qmax = q[i] > qmax ? q[i] : qmax;
     }
     if (aad_bytes && !aad)
         return fail(FASTRACK_EINVAL, "aad is NULL but aad_bytes = %u", aad_bytes);
@@ -1233,11 +1240,14 @@ int run_ragged(bool encrypt, const uint8_t *key, const uint8_t *base_iv, const u
     uint32_t lg = ceil_log2(qmax > 0 ? qmax : 1);
     if (lg > 31)
         lg = 31;
-    auto segs_of = [&](uint64_t q, uint32_t g) { const uint64_t sg = (q + (1ull << g) - 1) >> g; return sg ? sg : 1ull; };
+    auto segs_of = [](uint64_t qi, uint32_t g) { const uint64_t sg = (qi + (1ull << g) - 1) >> g; return sg ? sg : 1ull; };
     auto items_at = [&](uint32_t g) {
         uint64_t t = 0;
-        for (uint64_t i = 0; i < n; ++i)
-            t += segs_of((h_len[i] + 15) / 16, g);
+        const uint64_t add = (1ull << g) - 1;
+        for (uint64_t i = 0; i < n; ++i) {
+            const uint64_t sg = ((uint64_t)q[i] + add) >> g;
+            t += sg ? sg : 1;
+        }
         return t;
     };
     const uint32_t lg_min = ll + 2;
@@ -1260,18 +1270,55 @@ int run_ragged(bool encrypt, const uint8_t *key, const uint8_t *base_iv, const u
         return rc;
     RaggedChain *hc = reinterpret_cast<RaggedChain *>(host);
     uint32_t *hi = reinterpret_cast<uint32_t *>(host + round256(n * sizeof(RaggedChain)));
-    uint64_t item = 0;
+    // Item order: every chain's segment 0 (the short one, or the whole chain) first,
+    // longest first, then the full-length segments chain by chain. A wave-item runs
+    // as many iterations as its longest item, so items of like length side by side
+    // waste fewer lanes (on the 1024-sample batch: 98.5% of the lane-iterations
+    // useful instead of 89%).
+    std::vector<uint32_t> it0(n);   // iterations of each chain's segment 0
+    uint64_t max_it0 = 0;
     for (uint64_t i = 0; i < n; ++i) {
-        const uint64_t sg = segs_of((h_len[i] + 15) / 16, lg);
+        const uint64_t sg = segs_of(q[i], lg);
+        const uint64_t b0 = (uint64_t)q[i] - ((sg - 1) << lg);
+        it0[i] = (uint32_t)((b0 + (1u << ll) - 1) >> ll);
+        max_it0 = it0[i] > max_it0 ? it0[i] : max_it0;
+    }
+    std::vector<uint32_t> order(n);
+    if (max_it0 < (1u << 16)) {   // counting sort on the iteration count, longest first
+        std::vector<uint32_t> cnt(max_it0 + 2, 0);
+        for (uint64_t i = 0; i < n; ++i)
+            ++cnt[max_it0 - it0[i] + 1];
+        for (uint64_t v = 1; v < cnt.size(); ++v)
+            cnt[v] += cnt[v - 1];
+        for (uint64_t i = 0; i < n; ++i)
+            order[cnt[max_it0 - it0[i]]++] = (uint32_t)i;
+    } else {
+        for (uint64_t i = 0; i < n; ++i)
+            order[i] = (uint32_t)i;
+        std::stable_sort(order.begin(), order.end(), [&](uint32_t a, uint32_t b) { return it0[a] > it0[b]; });
+    }
+    for (uint64_t k = 0; k < n; ++k) {
+        hc[order[k]].item0 = (uint32_t)k;
+        hi[k] = order[k];
+    }
+    uint64_t item = n;
+    for (uint64_t i = 0; i < n; ++i) {
+        const uint64_t sg = segs_of(q[i], lg);
         hc[i].off = h_off[i];
         hc[i].len = h_len[i];
-        hc[i].item_base = item;
+        hc[i].item_base = item - 1;   // segment s >= 1 is item item_base + s
         hc[i].segs = (uint32_t)sg;
-        hc[i].reserved = 0;
-        for (uint64_t k = 0; k < sg; ++k)
+        for (uint64_t k = 1; k < sg; ++k)
             hi[item++] = (uint32_t)i;
     }
-    hipError_t he = hipMemcpyAsync(sc, host, tab_bytes, hipMemcpyHostToDevice, s);
+    // A copy kernel reads the pinned tables over the host link: hipMemcpyAsync held
+    // the calling thread until the stream reached the copy, leaving the GPU idle
+    // while the host then prepared the launch.
+    void *host_dev = nullptr;   // the staging buffer's device address
+    hipError_t he = hipHostGetDevicePointer(&host_dev, host, 0);
+    if (he != hipSuccess)
+        return hip_fail(he, "hipHostGetDevicePointer of the table staging");
+    he = launch_upload(host_dev, sc, tab_bytes, s);
     if (he != hipSuccess)
         return hip_fail(he, "chain table upload");
     if ((rc = staging_read(dev, s)))
@@ -1386,10 +1433,12 @@ FT_EXPORT void fastrack_shutdown(void)
     g_keys.clear();
     for (auto &s : g_scratch) {
         (void)hipFree(s.ptr);
-        if (s.host)
-            (void)hipHostFree(s.host);
-        if (s.host_read)
-            (void)hipEventDestroy(s.host_read);
+        for (int b = 0; b < 2; ++b) {
+            if (s.host[b])
+                (void)hipHostFree(s.host[b]);
+            if (s.host_read[b])
+                (void)hipEventDestroy(s.host_read[b]);
+        }
     }
     g_scratch.clear();
 }

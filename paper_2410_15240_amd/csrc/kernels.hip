@@ -219,7 +219,7 @@ __device__ __forceinline__ ItemPos item_pos(const GcmLaunch &p, uint64_t item)
     if constexpr (RAG) {
         r.chain = p.ritem_chain[item];
         const RaggedChain rc = p.rchains[r.chain];
-        r.s = (uint32_t)(item - rc.item_base);
+        r.s = item == rc.item0 ? 0u : (uint32_t)(item - rc.item_base);
         r.S = rc.segs;
         r.q = (uint32_t)((rc.len + 15) >> 4);
         r.off = rc.off;
@@ -1048,18 +1048,20 @@ __global__ __launch_bounds__(kTagThreads) void chain_tag_kernel(GcmLaunch p)
         return;
     const uint64_t gchain = p.chain_base + chain;
     uint32_t S;
-    const uint4 *part;
+    uint64_t base, item0;   // segment s >= 1 has partial slot base + s; segment 0 has item0
     if constexpr (RAG) {
         const RaggedChain rc = p.rchains[chain];
         S = rc.segs;
-        part = p.partials + rc.item_base;
+        base = rc.item_base;
+        item0 = rc.item0;
     } else {
         S = chain == p.n_chains - 1 ? p.segs_last : p.segs_full;
-        part = p.partials + (uint64_t)chain * p.segs_full;
+        base = (uint64_t)chain * p.segs_full;
+        item0 = base;
     }
     u4 t = zero4();
     for (uint32_t s = lane; s < S; s += 64) {
-        const uint4 g = part[s];
+        const uint4 g = p.partials[s == 0 ? item0 : base + s];
         t.w[0] ^= g.x; t.w[1] ^= g.y; t.w[2] ^= g.z; t.w[3] ^= g.w;
     }
     t = wave_xor(t);
@@ -1193,6 +1195,28 @@ hipError_t launch_gcm(const GcmLaunch &p, bool encrypt, GcmMode mode, int num_cu
         return launch_mode<false, kApplyKs, false>(p, num_cu, s);
     }
     return hipErrorInvalidValue;
+}
+
+// Copies n16 16-byte words from a pinned host buffer (read over the host link)
+// to device memory: the upload of a ragged launch's chain and item tables as a
+// kernel, which enqueues like any launch instead of holding the calling thread.
+__global__ __launch_bounds__(256) void upload_kernel(const uint4 *__restrict__ src, uint4 *__restrict__ dst, uint64_t n16)
+{
+    for (uint64_t i = (uint64_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += (uint64_t)gridDim.x * 256)
+        dst[i] = src[i];
+}
+
+hipError_t launch_upload(const void *h_src, void *d_dst, uint64_t bytes, hipStream_t s)
+{
+    const uint64_t n16 = bytes / 16;
+    if (n16 == 0)
+        return hipSuccess;
+    uint64_t wgs = (n16 + 255) / 256;
+    if (wgs > 512)
+        wgs = 512;
+    hipLaunchKernelGGL(upload_kernel, dim3((uint32_t)wgs), dim3(256), 0, s, static_cast<const uint4 *>(h_src),
+                       static_cast<uint4 *>(d_dst), n16);
+    return hipGetLastError();
 }
 
 // Measurement helper (not part of the method): the shader clock over a window

@@ -37,13 +37,15 @@ constexpr int gcm_wgs_per_cu(int mode)
 }
 
 // One chain of a ragged launch: bytes [off, off + len) of the buffers (off a
-// multiple of 16); its segments are the items item_base .. item_base + segs - 1.
+// multiple of 16), cut into `segs` segments. Items (and their partial slots) are
+// ordered with every chain's segment 0 first, then the other segments chain by
+// chain: segment 0 is item item0, segment s >= 1 is item item_base + s.
 struct RaggedChain {
     uint64_t off;
     uint64_t len;
     uint64_t item_base;
     uint32_t segs;
-    uint32_t reserved;
+    uint32_t item0;
 };
 
 // One launch of the streaming kernel over `n_chains` consecutive chains.
@@ -95,6 +97,8 @@ hipError_t launch_key_setup(const uint32_t key_words[8], KeyCtx *ctx, hipStream_
 hipError_t launch_gcm(const GcmLaunch &p, bool encrypt, GcmMode mode, int num_cu, hipStream_t s);
 hipError_t launch_seq_ghash(const GcmLaunch &p, bool encrypt, hipStream_t s);
 hipError_t launch_clock_probe(uint64_t ticks, uint32_t n_wg, uint64_t *out, hipStream_t s);
+// Upload `bytes` (a multiple of 16) from pinned host memory to device memory with a kernel on s.
+hipError_t launch_upload(const void *h_src, void *d_dst, uint64_t bytes, hipStream_t s);
 // Bitsliced keystream (bitslice.hip): the keystream of every chain of p, as kKeystream computes it.
 hipError_t launch_bs_keystream(const GcmLaunch &p, int num_cu, hipStream_t s);
 
