@@ -65,6 +65,14 @@ struct ScratchEntry {
     size_t host_bytes[2] = {0, 0};
     hipEvent_t host_read[2] = {nullptr, nullptr};
     int cur = 0;
+    // Ragged launches: two device table slots (written only by the uploads, read
+    // only by the ragged kernels), the library's upload stream, and for each slot
+    // the event after the kernels that last read it.
+    void *rtab = nullptr;
+    size_t rtab_slot = 0;
+    hipStream_t up = nullptr;
+    hipEvent_t slot_free[2] = {nullptr, nullptr};
+    bool slot_used[2] = {false, false};
 };
 
 struct DevInfo {
@@ -242,13 +250,13 @@ int staging_for(int dev, hipStream_t s, size_t bytes, uint8_t **out)
     return FASTRACK_OK;
 }
 
-// Record on `s` that the staging buffer of (dev, s) handed out last has been read
-// by the work queued so far.
-int staging_read(int dev, hipStream_t s)
+// Record on `rs` (the stream whose work reads it) that the staging buffer of
+// (dev, s) handed out last has been read by the work queued there so far.
+int staging_read(int dev, hipStream_t s, hipStream_t rs)
 {
     for (auto &x : g_scratch)
         if (x.dev == dev && x.stream == s) {
-            hipError_t he = hipEventRecord(x.host_read[x.cur], s);
+            hipError_t he = hipEventRecord(x.host_read[x.cur], rs);
             return he == hipSuccess ? FASTRACK_OK : hip_fail(he, "hipEventRecord");
         }
     return fail(FASTRACK_EHIP, "no staging for this stream");
@@ -1172,6 +1180,50 @@ namespace {
 // AAD i, ok[i]. The chains are planned on the host (lanes per item from the mean
 // chain length, segments of one size for all chains) and the chain and item
 // tables go to the device through the stream's pinned staging.
+// The ragged table slot b of (dev, s) with room for `bytes`, the upload stream and
+// events created on first use. Growing the slots waits for both streams first.
+int ragged_slot(int dev, hipStream_t s, int b, size_t bytes, ScratchEntry **out_e, uint8_t **out)
+{
+    ScratchEntry *e = nullptr;
+    for (auto &x : g_scratch)
+        if (x.dev == dev && x.stream == s)
+            e = &x;
+    if (!e)
+        return fail(FASTRACK_EHIP, "no staging for this stream");
+    hipError_t he;
+    if (!e->up) {
+        // default priority: the library keeps every stream at the default
+        if ((he = hipStreamCreateWithFlags(&e->up, hipStreamNonBlocking)) != hipSuccess) {
+            e->up = nullptr;
+            return hip_fail(he, "hipStreamCreate for the table uploads");
+        }
+        for (int k = 0; k < 2; ++k)
+            if ((he = hipEventCreateWithFlags(&e->slot_free[k], hipEventDisableTiming)) != hipSuccess) {
+                e->slot_free[k] = nullptr;
+                return hip_fail(he, "hipEventCreate");
+            }
+    }
+    if (e->rtab_slot < bytes) {
+        if (e->rtab) {   // earlier kernels and uploads may still use the old slots
+            if ((he = hipStreamSynchronize(s)) != hipSuccess || (he = hipStreamSynchronize(e->up)) != hipSuccess)
+                return hip_fail(he, "hipStreamSynchronize");
+            (void)hipFree(e->rtab);
+            e->rtab = nullptr;
+            e->rtab_slot = 0;
+            e->slot_used[0] = e->slot_used[1] = false;
+        }
+        const size_t slot = (bytes + (1u << 20) - 1) & ~(size_t)((1u << 20) - 1);   // whole MiB, fewer regrowths
+        if ((he = hipMalloc(&e->rtab, 2 * slot)) != hipSuccess) {
+            e->rtab = nullptr;
+            return fail(FASTRACK_ENOMEM, "hipMalloc(%zu) for the ragged tables: %s", 2 * slot, hipGetErrorString(he));
+        }
+        e->rtab_slot = slot;
+    }
+    *out_e = e;
+    *out = static_cast<uint8_t *>(e->rtab) + (size_t)b * e->rtab_slot;
+    return FASTRACK_OK;
+}
+
 int run_ragged(bool encrypt, const uint8_t *key, const uint8_t *base_iv, const uint64_t *h_off, const uint64_t *h_len,
                uint64_t n, const uint8_t *in, uint8_t *out, const uint8_t *aad, uint32_t aad_bytes,
                const uint8_t *tags_in, uint8_t *tags_out, uint8_t *ok, void *stream)
@@ -1259,14 +1311,23 @@ int run_ragged(bool encrypt, const uint8_t *key, const uint8_t *base_iv, const u
         return fail(FASTRACK_EINVAL, "more than 2^32-1 work items");
 
     // Device: chain table | item table | (split) partials | masks. Host: the two tables.
+    // Tables (chain table | item table) go through pinned staging and an upload kernel
+    // into a table slot; partials and masks (split launches) use the stream's scratch.
     const size_t tab_bytes = round256(n * sizeof(RaggedChain)) + round256(n_items * 4);
     const bool split = n_items > n;
-    const size_t dev_bytes = tab_bytes + (split ? (n_items + n) * 16 : 0);
     void *sc = nullptr;
-    if ((rc = scratch_for(dev, s, dev_bytes, &sc)))
+    if (split && (rc = scratch_for(dev, s, (n_items + n) * 16, &sc)))
         return rc;
     uint8_t *host = nullptr;
     if ((rc = staging_for(dev, s, tab_bytes, &host)))
+        return rc;
+    ScratchEntry *se = nullptr;
+    uint8_t *tab = nullptr;
+    int slot = 0;
+    for (auto &x : g_scratch)
+        if (x.dev == dev && x.stream == s)
+            slot = x.cur;
+    if ((rc = ragged_slot(dev, s, slot, tab_bytes, &se, &tab)))
         return rc;
     RaggedChain *hc = reinterpret_cast<RaggedChain *>(host);
     uint32_t *hi = reinterpret_cast<uint32_t *>(host + round256(n * sizeof(RaggedChain)));
@@ -1314,15 +1375,21 @@ int run_ragged(bool encrypt, const uint8_t *key, const uint8_t *base_iv, const u
     // A copy kernel reads the pinned tables over the host link: hipMemcpyAsync held
     // the calling thread until the stream reached the copy, leaving the GPU idle
     // while the host then prepared the launch.
+    // The upload runs on the library's upload stream, so it overlaps the kernels of
+    // the call before: it waits only for the kernels that last read this slot (two
+    // calls back), and the kernels of this call wait for it.
     void *host_dev = nullptr;   // the staging buffer's device address
     hipError_t he = hipHostGetDevicePointer(&host_dev, host, 0);
     if (he != hipSuccess)
         return hip_fail(he, "hipHostGetDevicePointer of the table staging");
-    he = launch_upload(host_dev, sc, tab_bytes, s);
-    if (he != hipSuccess)
+    if (se->slot_used[slot] && (he = hipStreamWaitEvent(se->up, se->slot_free[slot], 0)) != hipSuccess)
+        return hip_fail(he, "hipStreamWaitEvent");
+    if ((he = launch_upload(host_dev, tab, tab_bytes, se->up)) != hipSuccess)
         return hip_fail(he, "chain table upload");
-    if ((rc = staging_read(dev, s)))
+    if ((rc = staging_read(dev, s, se->up)))   // the staging is read once the upload has run
         return rc;
+    if ((he = hipStreamWaitEvent(s, se->host_read[slot], 0)) != hipSuccess)
+        return hip_fail(he, "hipStreamWaitEvent");
 
     GcmLaunch p;
     std::memset(&p, 0, sizeof p);
@@ -1340,16 +1407,19 @@ int run_ragged(bool encrypt, const uint8_t *key, const uint8_t *base_iv, const u
     p.lanes_log2 = ll;
     p.seg_log2 = lg;
     p.qc = (uint32_t)qmax;
-    p.rchains = reinterpret_cast<const RaggedChain *>(sc);
-    p.ritem_chain = reinterpret_cast<const uint32_t *>(static_cast<uint8_t *>(sc) + round256(n * sizeof(RaggedChain)));
+    p.rchains = reinterpret_cast<const RaggedChain *>(tab);
+    p.ritem_chain = reinterpret_cast<const uint32_t *>(tab + round256(n * sizeof(RaggedChain)));
     p.split = split ? 1u : 0u;
     if (split) {
-        p.partials = reinterpret_cast<uint4 *>(static_cast<uint8_t *>(sc) + tab_bytes);
+        p.partials = reinterpret_cast<uint4 *>(sc);
         p.masks = p.partials + n_items;
     }
     he = launch_gcm(p, encrypt, kFused, ncu, s);
     if (he != hipSuccess)
         return hip_fail(he, "GCM launch");
+    if ((he = hipEventRecord(se->slot_free[slot], s)) != hipSuccess)
+        return hip_fail(he, "hipEventRecord");
+    se->slot_used[slot] = true;
     return FASTRACK_OK;
 }
 
@@ -1433,12 +1503,17 @@ FT_EXPORT void fastrack_shutdown(void)
     g_keys.clear();
     for (auto &s : g_scratch) {
         (void)hipFree(s.ptr);
+        (void)hipFree(s.rtab);
         for (int b = 0; b < 2; ++b) {
             if (s.host[b])
                 (void)hipHostFree(s.host[b]);
             if (s.host_read[b])
                 (void)hipEventDestroy(s.host_read[b]);
+            if (s.slot_free[b])
+                (void)hipEventDestroy(s.slot_free[b]);
         }
+        if (s.up)
+            (void)hipStreamDestroy(s.up);
     }
     g_scratch.clear();
 }
