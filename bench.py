@@ -466,14 +466,17 @@ def extras(F, W, torch, np, dev, stream, args):
     c6, t6 = F.encrypt_tag_ragged(w6.key, w6.base_iv, off6, ln6, p6, a6)
     o6 = torch.empty_like(c6)
     k6 = torch.empty(off6.size, dtype=torch.uint8, device=dev)
+    # 100 untimed calls first: the first calls of this leg also touch freshly allocated
+    # table slots and staging (slower for the first ~50 calls on the box)
     rag_ms = time_calls(torch, stream, lambda: F.decrypt_verify_ragged(w6.key, w6.base_iv, off6, ln6, c6, t6, a6,
-                                                                      out=o6, ok=k6), 20)
+                                                                      out=o6, ok=k6), 40, pre=100)
     assert bool(k6.all())
     enc_ms = time_calls(torch, stream, lambda: F.encrypt_tag_ragged(w6.key, w6.base_iv, off6, ln6, p6, a6, out=o6,
-                                                                   tags=t6), 20)
+                                                                   tags=t6), 40, pre=100)
     cu, tu = F.encrypt_tag(w6.key, w6.base_iv, 8 * KiB, p6)
     ku = torch.empty(tu.shape[0], dtype=torch.uint8, device=dev)
-    uni_ms = time_calls(torch, stream, lambda: F.decrypt_verify(w6.key, w6.base_iv, 8 * KiB, cu, tu, out=o6, ok=ku), 20)
+    uni_ms = time_calls(torch, stream, lambda: F.decrypt_verify(w6.key, w6.base_iv, 8 * KiB, cu, tu, out=o6, ok=ku), 40,
+                        pre=100)
     nbytes = int(ln6.sum())
     res["ragged"] = {"workload": "sample-batch: 1024 samples (log-normal sizes, median 110 KiB) x 16 chains, "
                                  "1-byte serial AAD, %.1f MiB" % (total6 / MiB),

@@ -62,6 +62,7 @@ struct ScratchEntry {
     // two pinned host staging buffers for the tables of ragged launches, used in
     // turn, and for each the event after the copy that last read it
     void *host[2] = {nullptr, nullptr};
+    void *host_dev[2] = {nullptr, nullptr};   // their device addresses
     size_t host_bytes[2] = {0, 0};
     hipEvent_t host_read[2] = {nullptr, nullptr};
     int cur = 0;
@@ -243,6 +244,11 @@ int staging_for(int dev, hipStream_t s, size_t bytes, uint8_t **out)
         if ((he = hipHostMalloc(&e->host[b], bytes, hipHostMallocMapped)) != hipSuccess) {
             e->host[b] = nullptr;
             return fail(FASTRACK_ENOMEM, "hipHostMalloc(%zu) for staging: %s", bytes, hipGetErrorString(he));
+        }
+        if ((he = hipHostGetDevicePointer(&e->host_dev[b], e->host[b], 0)) != hipSuccess) {
+            (void)hipHostFree(e->host[b]);
+            e->host[b] = nullptr;
+            return hip_fail(he, "hipHostGetDevicePointer of the table staging");
         }
         e->host_bytes[b] = bytes;
     }
@@ -1238,7 +1244,9 @@ int run_ragged(bool encrypt, const uint8_t *key, const uint8_t *base_iv, const u
     if (n > 0xFFFFFFFFull)
         return fail(FASTRACK_EINVAL, "more than 2^32-1 chains");
     uint64_t end = 0, blocks = 0, qmax = 0;
-    std::vector<uint32_t> q(n);   // blocks of each chain (a partial block counts as one)
+    // per-call work arrays, kept per thread so that calls do not allocate them
+    thread_local std::vector<uint32_t> q, it0, order, cnt;
+    q.resize(n);   // blocks of each chain (a partial block counts as one)
     for (uint64_t i = 0; i < n; ++i) {
         if (h_off[i] & 15)
             return fail(FASTRACK_EINVAL, "chain %llu starts at offset %llu, not a multiple of 16", (unsigned long long)i,
@@ -1289,24 +1297,48 @@ int run_ragged(bool encrypt, const uint8_t *key, const uint8_t *base_iv, const u
         }
     if (ll == 0)
         ll = qmean >= 256 ? 6 : (qmean >= 128 ? 5 : 4);
-    uint32_t lg = ceil_log2(qmax > 0 ? qmax : 1);
-    if (lg > 31)
-        lg = 31;
-    auto segs_of = [](uint64_t qi, uint32_t g) { const uint64_t sg = (qi + (1ull << g) - 1) >> g; return sg ? sg : 1ull; };
+    uint32_t lg0 = ceil_log2(qmax > 0 ? qmax : 1);
+    if (lg0 > 31)
+        lg0 = 31;
+    // Items of a chain of x blocks with segments of 2^g: max(1, ceil(x / 2^g)) (no overflow for x < 2^32).
+    auto segs_of = [](uint32_t x, uint32_t g) {
+        const uint32_t sg = (x >> g) + ((x & ((1u << g) - 1)) != 0);
+        return sg ? sg : 1u;
+    };
     auto items_at = [&](uint32_t g) {
         uint64_t t = 0;
-        const uint64_t add = (1ull << g) - 1;
-        for (uint64_t i = 0; i < n; ++i) {
-            const uint64_t sg = ((uint64_t)q[i] + add) >> g;
-            t += sg ? sg : 1;
-        }
+        for (uint64_t i = 0; i < n; ++i)
+            t += segs_of(q[i], g);
         return t;
     };
-    const uint32_t lg_min = ll + 2;
+    const uint32_t lg_min = ll + 2 < lg0 ? ll + 2 : lg0;
     const uint64_t want_items = (4 * slots) << (6 - ll);   // 4 wave-items of 64 / 2^ll items per wave
-    while (lg > lg_min && items_at(lg) < want_items)
-        --lg;
-    const uint64_t n_items = items_at(lg);
+    // The segment size is the largest 2^lg (lg_min <= lg <= lg0) that still gives
+    // want_items items, else 2^lg_min. The item count falls as lg grows, so the
+    // search starts from an estimate (a chain adds about x / 2^lg + 1/2 items) and
+    // steps to the answer: one or two passes over the chains instead of one per
+    // candidate size.
+    uint32_t lg = lg0;
+    {
+        const uint64_t rest = want_items > n / 2 ? want_items - n / 2 : 1;
+        uint32_t ge = 0;
+        while (ge < 31 && ((uint64_t)blocks >> (ge + 1)) >= rest)
+            ++ge;
+        lg = ge < lg_min ? lg_min : (ge > lg0 ? lg0 : ge);
+    }
+    uint64_t n_items = items_at(lg);
+    if (n_items >= want_items) {
+        while (lg < lg0) {
+            const uint64_t up = items_at(lg + 1);
+            if (up < want_items)
+                break;
+            ++lg;
+            n_items = up;
+        }
+    } else {
+        while (lg > lg_min && n_items < want_items)
+            n_items = items_at(--lg);
+    }
     if (n_items > 0xFFFFFFFFull)
         return fail(FASTRACK_EINVAL, "more than 2^32-1 work items");
 
@@ -1336,40 +1368,52 @@ int run_ragged(bool encrypt, const uint8_t *key, const uint8_t *base_iv, const u
     // as many iterations as its longest item, so items of like length side by side
     // waste fewer lanes (on the 1024-sample batch: 98.5% of the lane-iterations
     // useful instead of 89%).
-    std::vector<uint32_t> it0(n);   // iterations of each chain's segment 0
-    uint64_t max_it0 = 0;
+    it0.resize(n);   // iterations of each chain's segment 0, then its item number
+    uint32_t max_it0 = 0;
+    const uint32_t lmask = (1u << lg) - 1, lstep = (1u << ll) - 1;
     for (uint64_t i = 0; i < n; ++i) {
-        const uint64_t sg = segs_of(q[i], lg);
-        const uint64_t b0 = (uint64_t)q[i] - ((sg - 1) << lg);
-        it0[i] = (uint32_t)((b0 + (1u << ll) - 1) >> ll);
+        const uint32_t x = q[i];
+        const uint32_t b0 = x == 0 ? 0u : ((x - 1) & lmask) + 1;   // blocks of segment 0
+        it0[i] = (uint32_t)(((uint64_t)b0 + lstep) >> ll);
         max_it0 = it0[i] > max_it0 ? it0[i] : max_it0;
     }
-    std::vector<uint32_t> order(n);
     if (max_it0 < (1u << 16)) {   // counting sort on the iteration count, longest first
-        std::vector<uint32_t> cnt(max_it0 + 2, 0);
+        cnt.assign((size_t)max_it0 + 1, 0);
         for (uint64_t i = 0; i < n; ++i)
-            ++cnt[max_it0 - it0[i] + 1];
-        for (uint64_t v = 1; v < cnt.size(); ++v)
-            cnt[v] += cnt[v - 1];
-        for (uint64_t i = 0; i < n; ++i)
-            order[cnt[max_it0 - it0[i]]++] = (uint32_t)i;
+            ++cnt[max_it0 - it0[i]];
+        uint32_t run = 0;
+        for (auto &c : cnt) {
+            const uint32_t k = c;
+            c = run;
+            run += k;
+        }
+        for (uint64_t i = 0; i < n; ++i) {
+            const uint32_t k = cnt[max_it0 - it0[i]]++;
+            it0[i] = k;
+            hi[k] = (uint32_t)i;
+        }
     } else {
+        order.resize(n);
         for (uint64_t i = 0; i < n; ++i)
             order[i] = (uint32_t)i;
         std::stable_sort(order.begin(), order.end(), [&](uint32_t a, uint32_t b) { return it0[a] > it0[b]; });
+        for (uint64_t k = 0; k < n; ++k) {
+            it0[order[k]] = (uint32_t)k;
+            hi[k] = order[k];
+        }
     }
-    for (uint64_t k = 0; k < n; ++k) {
-        hc[order[k]].item0 = (uint32_t)k;
-        hi[k] = order[k];
-    }
+    // The chain table in chain order, one sequential pass (with the full-length
+    // segments' items behind the segment-0 items).
     uint64_t item = n;
     for (uint64_t i = 0; i < n; ++i) {
-        const uint64_t sg = segs_of(q[i], lg);
-        hc[i].off = h_off[i];
-        hc[i].len = h_len[i];
-        hc[i].item_base = item - 1;   // segment s >= 1 is item item_base + s
-        hc[i].segs = (uint32_t)sg;
-        for (uint64_t k = 1; k < sg; ++k)
+        const uint32_t sg = segs_of(q[i], lg);
+        RaggedChain &c = hc[i];
+        c.off = h_off[i];
+        c.len = h_len[i];
+        c.item_base = item - 1;   // segment s >= 1 is item item_base + s
+        c.segs = sg;
+        c.item0 = it0[i];
+        for (uint32_t k = 1; k < sg; ++k)
             hi[item++] = (uint32_t)i;
     }
     // A copy kernel reads the pinned tables over the host link: hipMemcpyAsync held
@@ -1378,10 +1422,8 @@ int run_ragged(bool encrypt, const uint8_t *key, const uint8_t *base_iv, const u
     // The upload runs on the library's upload stream, so it overlaps the kernels of
     // the call before: it waits only for the kernels that last read this slot (two
     // calls back), and the kernels of this call wait for it.
-    void *host_dev = nullptr;   // the staging buffer's device address
-    hipError_t he = hipHostGetDevicePointer(&host_dev, host, 0);
-    if (he != hipSuccess)
-        return hip_fail(he, "hipHostGetDevicePointer of the table staging");
+    hipError_t he;
+    const void *host_dev = se->host_dev[slot];   // the staging buffer's device address
     if (se->slot_used[slot] && (he = hipStreamWaitEvent(se->up, se->slot_free[slot], 0)) != hipSuccess)
         return hip_fail(he, "hipStreamWaitEvent");
     if ((he = launch_upload(host_dev, tab, tab_bytes, se->up)) != hipSuccess)
