@@ -51,7 +51,21 @@ struct KeyEntry {
     KeyCtx *ctx;
     hipEvent_t ready;
     uint64_t last_use;
+    int slot;            // its slot in the device's key pool
     bool done = false;   // `ready` has been observed complete
+};
+
+// Per device, kMaxKeys key contexts in one allocation and an event per slot,
+// made with the first key on that device: a new key then allocates nothing
+// (a device allocation held the calling thread ~0.1 ms, more than the key
+// setup itself).
+constexpr size_t kKeySlotBytes = (sizeof(KeyCtx) + 255) & ~(size_t)255;   // slots 256-byte aligned
+
+struct KeyPool {
+    int dev;
+    uint8_t *base = nullptr;
+    hipEvent_t ready[kMaxKeys] = {};
+    bool used[kMaxKeys] = {};
 };
 
 struct ScratchEntry {
@@ -83,6 +97,7 @@ struct DevInfo {
 
 std::mutex g_mu;
 std::vector<KeyEntry> g_keys;
+std::vector<KeyPool> g_pools;
 std::vector<ScratchEntry> g_scratch;
 std::vector<DevInfo> g_dev;
 uint64_t g_tick = 0;
@@ -103,11 +118,41 @@ int num_cu_of(int dev, int *out)
     return FASTRACK_OK;
 }
 
+KeyPool *pool_of(int dev)
+{
+    for (auto &p : g_pools)
+        if (p.dev == dev)
+            return &p;
+    return nullptr;
+}
+
+int pool_for(int dev, KeyPool **out)
+{
+    if ((*out = pool_of(dev)))
+        return FASTRACK_OK;
+    KeyPool p;
+    p.dev = dev;
+    hipError_t he = hipMalloc(reinterpret_cast<void **>(&p.base), kMaxKeys * kKeySlotBytes);
+    if (he != hipSuccess)
+        return fail(FASTRACK_ENOMEM, "hipMalloc(%zu) for the key tables: %s", kMaxKeys * kKeySlotBytes,
+                    hipGetErrorString(he));
+    for (size_t i = 0; i < kMaxKeys; ++i)
+        if ((he = hipEventCreateWithFlags(&p.ready[i], hipEventDisableTiming)) != hipSuccess) {
+            for (size_t j = 0; j < i; ++j)
+                (void)hipEventDestroy(p.ready[j]);
+            (void)hipFree(p.base);
+            return hip_fail(he, "hipEventCreate");
+        }
+    g_pools.push_back(p);
+    *out = &g_pools.back();
+    return FASTRACK_OK;
+}
+
+// The slot is rewritten whole by the next key's setup; the pool is cleared when freed.
 void free_key_entry(KeyEntry &k)
 {
-    (void)hipMemset(k.ctx, 0, sizeof(KeyCtx));   // key-derived material does not outlive the entry
-    (void)hipFree(k.ctx);
-    (void)hipEventDestroy(k.ready);
+    if (KeyPool *p = pool_of(k.dev))
+        p->used[k.slot] = false;
 }
 
 // Device tables for (current device, key); setup is enqueued on `s` the first time.
@@ -137,6 +182,10 @@ int key_ctx(const uint8_t *key, hipStream_t s, int dev, const KeyCtx **out)
             if (victim == g_keys.size() || g_keys[i].last_use < g_keys[victim].last_use)
                 victim = i;
         }
+    KeyPool *pool;
+    int rc;
+    if ((rc = pool_for(dev, &pool)))
+        return rc;
     if (same_dev >= kMaxKeys) {
         // Work queued on any stream may still read the victim's tables.
         hipError_t he = hipDeviceSynchronize();
@@ -145,31 +194,31 @@ int key_ctx(const uint8_t *key, hipStream_t s, int dev, const KeyCtx **out)
         free_key_entry(g_keys[victim]);
         g_keys.erase(g_keys.begin() + (long)victim);
     }
+    int slot = 0;
+    while (slot < (int)kMaxKeys && pool->used[slot])
+        ++slot;
+    if (slot == (int)kMaxKeys)
+        return fail(FASTRACK_EHIP, "key pool full");   // cannot happen: at most kMaxKeys entries per device
     KeyEntry e;
     e.dev = dev;
     e.key = k;
     e.last_use = ++g_tick;
-    hipError_t he = hipMalloc(reinterpret_cast<void **>(&e.ctx), sizeof(KeyCtx));
-    if (he != hipSuccess)
-        return fail(FASTRACK_ENOMEM, "hipMalloc(%zu) for the key tables: %s", sizeof(KeyCtx), hipGetErrorString(he));
+    e.slot = slot;
+    e.ctx = reinterpret_cast<KeyCtx *>(pool->base + (size_t)slot * kKeySlotBytes);
+    e.ready = pool->ready[slot];
     uint32_t words[8];
     for (int i = 0; i < 8; ++i)
         words[i] = (uint32_t)key[4 * i] | ((uint32_t)key[4 * i + 1] << 8) | ((uint32_t)key[4 * i + 2] << 16) |
                    ((uint32_t)key[4 * i + 3] << 24);
-    he = launch_key_setup(words, e.ctx, s);
+    hipError_t he = launch_key_setup(words, e.ctx, s);
     std::memset(words, 0, sizeof words);
-    if (he != hipSuccess) {
-        (void)hipFree(e.ctx);
+    if (he != hipSuccess)
         return hip_fail(he, "key setup launch");
-    }
-    he = hipEventCreateWithFlags(&e.ready, hipEventDisableTiming);
-    if (he == hipSuccess)
-        he = hipEventRecord(e.ready, s);
-    if (he != hipSuccess) {
+    if ((he = hipEventRecord(e.ready, s)) != hipSuccess) {
         (void)hipStreamSynchronize(s);
-        (void)hipFree(e.ctx);
         return hip_fail(he, "hipEventRecord");
     }
+    pool->used[slot] = true;
     g_keys.push_back(e);
     *out = e.ctx;
     return FASTRACK_OK;
@@ -1537,12 +1586,18 @@ FT_EXPORT void fastrack_shutdown(void)
         }
         (void)hipSetDevice(cur);
     }
-    if (g_keys.empty() && g_scratch.empty())
+    if (g_keys.empty() && g_scratch.empty() && g_pools.empty())
         return;
     (void)hipDeviceSynchronize();
-    for (auto &k : g_keys)
-        free_key_entry(k);
     g_keys.clear();
+    for (auto &p : g_pools) {
+        // key-derived material does not outlive the library's state
+        (void)hipMemset(p.base, 0, kMaxKeys * kKeySlotBytes);
+        (void)hipFree(p.base);
+        for (auto &ev : p.ready)
+            (void)hipEventDestroy(ev);
+    }
+    g_pools.clear();
     for (auto &s : g_scratch) {
         (void)hipFree(s.ptr);
         (void)hipFree(s.rtab);

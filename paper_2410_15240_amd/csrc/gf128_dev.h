@@ -47,14 +47,14 @@ __device__ __forceinline__ u4 from_be(const u4 &a) { return to_be(a); }
 // bits that pass degree 127 form F(x) . x^128, and x^128 = 1 + x + x^2 + x^7,
 // so they come back as F xor F.x xor F.x^2 xor F.x^7. For k <= 64, F has
 // degree < 64 and the fold cannot overflow again.
-__device__ inline u4 be_mul_xk(const u4 &y, int k)
+__host__ __device__ constexpr u4 be_mul_xk(const u4 &y, int k)
 {
     if (k == 0)
         return y;
     // 128-bit value v = w0:w1:w2:w3 (w0 most significant as an integer).
     uint64_t hi = ((uint64_t)y.w[0] << 32) | y.w[1];
     uint64_t lo = ((uint64_t)y.w[2] << 32) | y.w[3];
-    uint64_t nhi, nlo, f;
+    uint64_t nhi = 0, nlo = 0, f = 0;
     if (k < 64) {
         f = lo << (64 - k);               // the k bits that fall off, left-aligned
         nlo = (lo >> k) | (hi << (64 - k));
@@ -70,7 +70,7 @@ __device__ inline u4 be_mul_xk(const u4 &y, int k)
     uint64_t r_lo = (f << 63) ^ (f << 62) ^ (f << 57);
     nhi ^= r_hi;
     nlo ^= r_lo;
-    u4 r;
+    u4 r{};
     r.w[0] = (uint32_t)(nhi >> 32);
     r.w[1] = (uint32_t)nhi;
     r.w[2] = (uint32_t)(nlo >> 32);
@@ -79,7 +79,7 @@ __device__ inline u4 be_mul_xk(const u4 &y, int k)
 }
 
 // Y . x^k for 0 <= k <= 127 (two steps of at most 64).
-__device__ inline u4 be_mul_xk_any(const u4 &y, int k)
+__host__ __device__ constexpr u4 be_mul_xk_any(const u4 &y, int k)
 {
     if (k <= 64)
         return be_mul_xk(y, k);
@@ -87,7 +87,7 @@ __device__ inline u4 be_mul_xk_any(const u4 &y, int k)
 }
 
 // Bit i of w moved to bit 2i + 1 of a 64-bit word (the other bits zero).
-__device__ __forceinline__ uint64_t spread_odd(uint32_t w)
+__host__ __device__ constexpr uint64_t spread_odd(uint32_t w)
 {
     uint64_t x = w;
     x = (x | (x << 16)) & 0x0000FFFF0000FFFFull;
@@ -103,13 +103,13 @@ __device__ __forceinline__ uint64_t spread_odd(uint32_t w)
 // integer (degree d at bit 127 - d) the square is the 256-bit integer with bit p of
 // V at bit 2p + 1; its upper half holds degrees 0..127 and its lower half F the
 // degrees 128..255, which come back as F . x^128 = F . (1 + x + x^2 + x^7).
-__device__ inline u4 be_square(const u4 &y)
+__host__ __device__ constexpr u4 be_square(const u4 &y)
 {
     const uint64_t h0 = spread_odd(y.w[0]), h1 = spread_odd(y.w[1]);
     const uint64_t f0 = spread_odd(y.w[2]), f1 = spread_odd(y.w[3]);
     const u4 f = {{(uint32_t)(f0 >> 32), (uint32_t)f0, (uint32_t)(f1 >> 32), (uint32_t)f1}};
     const u4 a = be_mul_xk(f, 1), b = be_mul_xk(f, 2), c = be_mul_xk(f, 7);
-    u4 r;
+    u4 r{};
     r.w[0] = (uint32_t)(h0 >> 32) ^ f.w[0] ^ a.w[0] ^ b.w[0] ^ c.w[0];
     r.w[1] = (uint32_t)h0 ^ f.w[1] ^ a.w[1] ^ b.w[1] ^ c.w[1];
     r.w[2] = (uint32_t)(h1 >> 32) ^ f.w[2] ^ a.w[2] ^ b.w[2] ^ c.w[2];
@@ -117,28 +117,76 @@ __device__ inline u4 be_square(const u4 &y)
     return r;
 }
 
-// X . Y for arbitrary X and Y in big-endian-word form, by one wave (setup only):
-// lane l adds Y . x^i for each set degree i in {l, l + 64} of X, and the wave
-// XOR-sums the 64 terms. Every lane returns the product. All lanes must be active.
-__device__ inline u4 wave_mul_be(const u4 &x, const u4 &y, uint32_t lane)
+// XOR of x over each aligned group of 2^LL lanes, in every lane of the group: a
+// butterfly of VALU moves. Quad permutes pair lanes 1 and 2 apart; once each quad
+// (eight) holds one sum, the half-row (row) mirror pairs it with the neighbouring
+// quad (eight); the half-row and half-wave swaps return both halves, whose XOR is
+// a lane's own value xor its partner's.
+template <int LL>
+__device__ __forceinline__ uint32_t group_xor_sum(uint32_t x)
 {
-    u4 acc = {{0u, 0u, 0u, 0u}};
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-        const uint32_t i = lane + 64u * h;   // degree i: word i / 32, bit 31 - i % 32
-        const uint32_t w = i < 32 ? x.w[0] : (i < 64 ? x.w[1] : (i < 96 ? x.w[2] : x.w[3]));
-        if ((w >> (31 - (i & 31))) & 1u) {
-            const u4 t = be_mul_xk_any(y, (int)i);
-            for (int j = 0; j < 4; ++j)
-                acc.w[j] ^= t.w[j];
+    if constexpr (LL >= 1)
+        x ^= __builtin_amdgcn_update_dpp(0u, x, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
+    if constexpr (LL >= 2)
+        x ^= __builtin_amdgcn_update_dpp(0u, x, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
+    if constexpr (LL >= 3)
+        x ^= __builtin_amdgcn_update_dpp(0u, x, 0x141, 0xF, 0xF, false);  // row_half_mirror
+    if constexpr (LL >= 4)
+        x ^= __builtin_amdgcn_update_dpp(0u, x, 0x140, 0xF, 0xF, false);  // row_mirror
+    if constexpr (LL >= 5) {
+        const auto sw = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+        x = sw[0] ^ sw[1];
+    }
+    if constexpr (LL >= 6) {
+        const auto sw = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+        x = sw[0] ^ sw[1];
+    }
+    return x;
+}
+
+// The columns of S^k, S(V) = V^2, for k = 1..8, in big-endian-word form:
+// c[k - 1][i] = S^k(x^i). Squaring is GF(2)-linear, so V^(2^k) is the XOR of the
+// columns of V's set degrees. Evaluated by the compiler (key-independent).
+struct FrobTable {
+    u4 c[8][128];
+};
+
+constexpr FrobTable make_frob_table()
+{
+    FrobTable t{};
+    for (int i = 0; i < 128; ++i) {
+        u4 v{};
+        v.w[i >> 5] = 1u << (31 - (i & 31));
+        for (int k = 0; k < 8; ++k) {
+            v = be_square(v);
+            t.c[k][i] = v;
         }
     }
-#pragma unroll
-    for (int d = 32; d >= 1; d >>= 1)
-        for (int j = 0; j < 4; ++j)
-            acc.w[j] ^= __shfl_xor(acc.w[j], d, 64);
-    return acc;
+    return t;
 }
+
+// A GF(2)-linear map M on GF(2^128) held by one wave (setup only): lane l keeps
+// the columns M(x^l) and M(x^(l+64)) in big-endian-word form, and M(V) is a
+// select per lane and a wave-wide XOR. All lanes must be active.
+struct WaveLinear {
+    u4 c0, c1;
+    __device__ void load(const u4 *cols, uint32_t lane)
+    {
+        c0 = cols[lane];
+        c1 = cols[lane + 64];
+    }
+    __device__ u4 apply(const u4 &v, uint32_t lane) const
+    {
+        const uint32_t b0 = (lane < 32 ? v.w[0] : v.w[1]) >> (31 - (lane & 31));
+        const uint32_t b1 = (lane < 32 ? v.w[2] : v.w[3]) >> (31 - (lane & 31));
+        const uint32_t m0 = 0u - (b0 & 1u), m1 = 0u - (b1 & 1u);
+        u4 r;
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            r.w[j] = group_xor_sum<6>((c0.w[j] & m0) ^ (c1.w[j] & m1));
+        return r;
+    }
+};
 
 // ---- little-endian-word table multiplies -------------------------------
 

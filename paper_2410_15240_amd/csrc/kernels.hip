@@ -71,11 +71,41 @@ __device__ inline void build_tab4_row(const u4 &y, int p, Tab4 *out)
 }
 
 // Key setup in two launches. key_setup_kernel (one workgroup) runs the short
-// dependent chain: the S-box and T0, the AES-256 key expansion, H = AES_K(0),
-// the powers H^1..H^65 (level by level, the products of a level spread over the
-// waves, each product one wave multiply) and the squares H^(2^t) (25 squarings
-// in turn, each a bit spread and a reduction). key_tables_kernel (many workgroups) then builds every table from
-// those powers, one table entry per thread.
+// dependent chain: the AES-256 key expansion, H = AES_K(0), the powers
+// H^1..H^65 (level by level, the products of a level spread over the waves) and
+// the squares H^(2^t). key_tables_kernel (many workgroups) then builds every
+// table from those powers, one table entry per thread.
+//
+// Key-independent parts come from tables the compiler evaluates: the S-box and
+// T0, and the columns of the squaring map's powers S^k, k = 1..8.
+static __constant__ const SboxTables kSboxTab = make_sbox_tables();
+static __constant__ const FrobTable kFrobCols = make_frob_table();
+
+// AES_K(0^128) by the four lanes of each quad (setup only): lane c holds state
+// column c, and ShiftRows' bytes of columns c + 1, c + 2, c + 3 come by quad
+// permutes. Returns column (lane & 3) of the output block. All lanes active.
+__device__ inline uint32_t aes_zero_quad(const uint32_t *rk, const uint32_t *t0, uint32_t lane)
+{
+    const uint32_t c = lane & 3;
+    uint32_t s = rk[c];   // the zero block after AddRoundKey
+    uint32_t s1 = 0, s2 = 0, s3 = 0;
+    auto shift = [&]() {
+        s1 = __builtin_amdgcn_update_dpp(0u, s, 0x39, 0xF, 0xF, false);   // quad_perm [1,2,3,0]
+        s2 = __builtin_amdgcn_update_dpp(0u, s, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
+        s3 = __builtin_amdgcn_update_dpp(0u, s, 0x93, 0xF, 0xF, false);   // quad_perm [3,0,1,2]
+    };
+#pragma unroll
+    for (int r = 1; r < 14; ++r) {
+        shift();
+        s = t0[s & 0xFF] ^ rotl32(t0[(s1 >> 8) & 0xFF], 8) ^ rotl32(t0[(s2 >> 16) & 0xFF], 16) ^
+            rotl32(t0[s3 >> 24], 24) ^ rk[4 * r + c];
+    }
+    shift();
+    auto S = [&](uint32_t x) { return (t0[x] >> 8) & 0xFFu; };   // S(x) is byte 1 of T0[x]
+    return (S(s & 0xFF) | (S((s1 >> 8) & 0xFF) << 8) | (S((s2 >> 16) & 0xFF) << 16) | (S(s3 >> 24) << 24)) ^
+           rk[56 + c];
+}
+
 __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__restrict__ ctx)
 {
     __shared__ uint32_t s_sbox[256];
@@ -87,11 +117,15 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
     const uint32_t lane = tid & 63, wave = (uint32_t)tid >> 6;
     constexpr uint32_t kWaves = 1024 / 64;
 
+    // wave 7 + k holds the columns of S^k (k = 1..8) for the squares at the end
+    constexpr uint32_t kFrobWave0 = 8;
+    WaveLinear frob;
+    if (wave >= kFrobWave0)
+        frob.load(kFrobCols.c[wave - kFrobWave0], lane);
     if (tid < 256) {
-        uint32_t s = sbox_entry(tid);
-        s_sbox[tid] = s;
-        ctx->sbox[tid] = (uint8_t)s;
-        uint32_t t = t0_entry(s);
+        const uint32_t sb = kSboxTab.sbox[tid], t = kSboxTab.t0[tid];
+        s_sbox[tid] = sb;
+        ctx->sbox[tid] = (uint8_t)sb;
         s_t0[tid] = t;
         ctx->t0[tid] = t;
     }
@@ -99,6 +133,7 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
     if (tid == 0) {
         uint32_t rk[60];
         expand_key_256(a.key, rk, [&](uint32_t x) { return s_sbox[x]; });
+#pragma unroll
         for (int i = 0; i < 60; ++i) {
             s_rk[i] = rk[i];
             ctx->rk[i] = rk[i];
@@ -106,43 +141,62 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
         }
     }
     __syncthreads();
-    if (tid == 0) {
-        u4 zero = {{0u, 0u, 0u, 0u}};
-        u4 h = aes256_encrypt_tt(zero, s_rk, [&](uint32_t x) { return s_t0[x]; });
-        u4 one = {{0x80u, 0u, 0u, 0u}};   // the block 0x80 || 0^120 is 1
-        s_hp[0] = one;
-        s_hp[1] = h;
+    if (wave == 0) {
+        const uint32_t col = aes_zero_quad(s_rk, s_t0, lane);
+        u4 h;
+#pragma unroll
         for (int j = 0; j < 4; ++j)
-            ctx->h[j] = h.w[j];
+            h.w[j] = __builtin_amdgcn_readlane(col, j);
+        if (lane == 0) {
+            const u4 one = {{0x80u, 0u, 0u, 0u}};   // the block 0x80 || 0^120 is 1
+            s_hp[0] = one;
+            s_hp[1] = h;
+        }
+        if (lane < 4)
+            ctx->h[lane] = col;
     }
     __syncthreads();
 
-    // Powers by doubling: H^(2^r + j) = H^j . H^(2^r), j = 1..2^r, the products of
-    // a level over the waves; then H^65 = H^64 . H.
+    // Powers by doubling: H^(2^r + j) = H^j . H^(2^r), j = 1..2^r. Multiplying by
+    // the level's H^(2^r) is one linear map, whose columns every working wave
+    // builds; its products are then one application each.
     for (int r = 0; r < 6; ++r) {
         const uint32_t half = 1u << r;
-        for (uint32_t j = 1 + wave; j <= half; j += kWaves) {
-            const u4 prod = from_be(wave_mul_be(to_be(s_hp[j]), to_be(s_hp[half]), lane));
-            if (lane == 0)
-                s_hp[half + j] = prod;
+        if (1 + wave <= half) {
+            const u4 y = to_be(s_hp[half]);
+            WaveLinear mul;
+            mul.c0 = be_mul_xk_any(y, (int)lane);
+            mul.c1 = be_mul_xk_any(y, (int)lane + 64);
+            for (uint32_t j = 1 + wave; j <= half; j += kWaves) {
+                const u4 prod = from_be(mul.apply(to_be(s_hp[j]), lane));
+                if (lane == 0)
+                    s_hp[half + j] = prod;
+            }
         }
         __syncthreads();
     }
-    if (wave == 0) {
-        const u4 prod = from_be(wave_mul_be(to_be(s_hp[kMaxPow]), to_be(s_hp[1]), lane));
+    if (wave == 0) {   // H^65 = H^64 . H
+        const u4 y = to_be(s_hp[1]);
+        WaveLinear mul;
+        mul.c0 = be_mul_xk_any(y, (int)lane);
+        mul.c1 = be_mul_xk_any(y, (int)lane + 64);
+        const u4 prod = from_be(mul.apply(to_be(s_hp[kMaxPow]), lane));
         if (lane == 0)
             s_hp[kMaxPow + 1] = prod;
-        // Squares H^(2^t): t <= 6 are powers already; the rest by squaring in turn.
-        u4 sq = to_be(s_hp[1u << 6]);
-        if (lane < 7)
+        if (lane < 7)   // squares H^(2^t), t <= 6, are powers already
             s_hsq[lane] = s_hp[1u << lane];
-        for (int t = 7; t < kSquares; ++t) {   // every lane squares the same value
-            sq = be_square(sq);
-            if (lane == 0)
-                s_hsq[t] = from_be(sq);
-        }
     }
     __syncthreads();
+    // The rest eight at a time: H^(2^(b + k)) = S^k(H^(2^b)), k = 1..8, one wave each.
+    for (int b = 6; b < kSquares - 1; b += 8) {
+        const int t = b + (int)(wave - kFrobWave0 + 1);
+        if (wave >= kFrobWave0 && t < kSquares) {
+            const u4 v = frob.apply(to_be(s_hsq[b]), lane);
+            if (lane == 0)
+                s_hsq[t] = from_be(v);
+        }
+        __syncthreads();
+    }
     for (int i = tid; i <= kMaxPow + 1; i += blockDim.x)
         for (int j = 0; j < 4; ++j)
             ctx->hp[i][j] = s_hp[i].w[j];
@@ -360,33 +414,6 @@ __device__ __forceinline__ int wave_min_i32(int x)
     x = min(x, (int)lane_down<2>((uint32_t)x));
     x = min(x, (int)lane_down<1>((uint32_t)x));
     return (int)__builtin_amdgcn_readlane((uint32_t)x, 0);
-}
-
-// XOR of x over each aligned group of 2^LL lanes, in every lane of the group: a
-// butterfly of VALU moves. Quad permutes pair lanes 1 and 2 apart; once each quad
-// (eight) holds one sum, the half-row (row) mirror pairs it with the neighbouring
-// quad (eight); the half-row and half-wave swaps return both halves, whose XOR is
-// a lane's own value xor its partner's.
-template <int LL>
-__device__ __forceinline__ uint32_t group_xor_sum(uint32_t x)
-{
-    if constexpr (LL >= 1)
-        x ^= __builtin_amdgcn_update_dpp(0u, x, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
-    if constexpr (LL >= 2)
-        x ^= __builtin_amdgcn_update_dpp(0u, x, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
-    if constexpr (LL >= 3)
-        x ^= __builtin_amdgcn_update_dpp(0u, x, 0x141, 0xF, 0xF, false);  // row_half_mirror
-    if constexpr (LL >= 4)
-        x ^= __builtin_amdgcn_update_dpp(0u, x, 0x140, 0xF, 0xF, false);  // row_mirror
-    if constexpr (LL >= 5) {
-        const auto sw = __builtin_amdgcn_permlane16_swap(x, x, false, false);
-        x = sw[0] ^ sw[1];
-    }
-    if constexpr (LL >= 6) {
-        const auto sw = __builtin_amdgcn_permlane32_swap(x, x, false, false);
-        x = sw[0] ^ sw[1];
-    }
-    return x;
 }
 
 // X . Y where the L = 2^LL lanes of each aligned lane group hold one X (the
