@@ -95,6 +95,34 @@ def test_small_shapes(F, length, chain, abytes):
             check_encrypt(F, w.key, w.base_iv, chain, w.payload, aad, abytes, flags, inplace, lab)
 
 
+# Launches that leave most waves idle cut chains into short segments (down to
+# 64 blocks, at most 512 per chain): one-iteration segments of 64 KiB chains,
+# 128-block segments of 1 MiB chains, with AAD, tails and tampering inside
+# middle segments.
+SEGMENTED = [(1 * MiB, 64 * KiB, 32), (2 * MiB, 1 * MiB, 32), (4 * MiB - 16, 1 * MiB, 1000),
+             (3 * MiB + 5, 1 * MiB, 13), (512 * KiB + 48, 32 * KiB, 0)]
+
+
+@pytest.mark.parametrize("length,chain,abytes", SEGMENTED)
+def test_short_segments(F, length, chain, abytes):
+    say("short segments", length, chain, abytes)
+    w = W.random_case(length % 977 + abytes, length, chain, abytes)
+    aad = W.case_aad(w, chain)
+    ct, tags = oracle.chains_encrypt(w.key, w.base_iv, chain, w.payload, aad, abytes)
+    lab = "len=%d chain=%d aad=%d" % (length, chain, abytes)
+    assert check_decrypt(F, w.key, w.base_iv, chain, ct, tags, aad, abytes, label=lab).all()
+    check_encrypt(F, w.key, w.base_iv, chain, w.payload, aad, abytes, label=lab)
+    n = tags.shape[0]
+    c2 = ct.copy()
+    bad = sorted({0, n // 2, n - 1})
+    for i in bad:   # one bit in the middle of the chain, far from its first and last segment
+        lo = i * chain
+        hi = min(length, lo + chain)
+        W.flip_bit(c2[lo:], 8 * ((hi - lo) // 2) + 3)
+    ok = check_decrypt(F, w.key, w.base_iv, chain, c2, tags, aad, abytes, label=lab + " tampered")
+    assert [i for i in range(n) if not ok[i]] == bad
+
+
 def test_tamper_positions(F):
     say("tamper positions")
     chain, length, abytes = 8192, 20 * 8192 + 40, 32
