@@ -36,7 +36,11 @@ ALU_PEAK_TOPS = 256 * 128 * 2.4e9 / 1e12
 # settles; warm-up runs at least this long so that the timed steps see the
 # settled clock whatever --steps is.
 WARMUP_MIN_S = 0.3
-GAPLESS_STEPS = 20
+# The timed steps follow at least this long of gap-free steps: after the warm-up's
+# synchronisations the clock still climbs for 20-30 ms of gap-free load (measured with
+# the probe: 2.18 -> 2.22 -> 2.26 GHz in 10 ms chunks, then steady).
+GAPLESS_S = 0.05
+ROTATE = 4                       # buffer sets the per-size timings cycle through
 
 KiB, MiB, GiB = 1024, 1 << 20, 1 << 30
 
@@ -115,11 +119,12 @@ def main():
     go = torch.cuda.Event()
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    # The last GAPLESS_STEPS warm-up steps run straight into the timed ones, with no
+    # The last warm-up steps (GAPLESS_S of them) run straight into the timed ones, with no
     # idle gap between them: after a gap the shader clock dips for several
     # milliseconds, which would otherwise fall inside a short timed region. The
     # event pair below brackets exactly the timed steps.
-    for _ in range(GAPLESS_STEPS):
+    gapless = max(20, int(GAPLESS_S / max(step_est_ms * 1e-3, 1e-6)) + 1)
+    for _ in range(gapless):
         step()
     go.record(stream)
     pstream.wait_event(go)
@@ -138,11 +143,26 @@ def main():
         assert bool(ok.all()), "benchmark decrypt rejected a chain"
         assert torch.equal(out, payload), "benchmark decrypt produced wrong plaintext"
     # Per chain size: 20 back-to-back launches of that size between two events, three
-    # times; the median of the three.
+    # times; the median of the three. Each run starts with 100 untimed launches of the
+    # size, gap-free (the checks above leave the GPU idle, and the clock dips for
+    # several milliseconds after that: with 20 the first size measured ~15% slow).
+    # The launches of one size cycle through four copies of its buffers (512 MiB in all),
+    # as the sweep's five sizes do (640 MiB): re-reading one 64 MiB buffer would be
+    # served partly by the 256 MB Infinity Cache.
     per = []
     for i, (chain, ct, tags, aad, out, ok) in enumerate(cases):
-        one = lambda: F.decrypt_verify(w.key, w.base_iv, chain, ct, tags, aad, out=out, ok=ok)
-        per.append(sorted(time_calls(torch, stream, one, 20, pre=20) for _ in range(3))[1])
+        sets = [(ct, tags, out, ok)] + [(ct.clone(), tags.clone(), torch.empty_like(out), torch.empty_like(ok))
+                                        for _ in range(ROTATE - 1)]
+        turn = [0]
+
+        def one():
+            c_, t_, o_, k_ = sets[turn[0] % ROTATE]
+            turn[0] += 1
+            F.decrypt_verify(w.key, w.base_iv, chain, c_, t_, aad, out=o_, ok=k_)
+        per.append(sorted(time_calls(torch, stream, one, 20, pre=100) for _ in range(3))[1])
+        for c_, t_, o_, k_ in sets:
+            assert bool(k_.all()) and torch.equal(o_, payload), "benchmark decrypt produced wrong plaintext"
+        del sets
     # The achievable HBM rate on this machine: a plain 64 MiB device-to-device copy
     # (read + write bytes over time, best of three runs of 20 copies). Under
     # rocprofv3 --pmc its FETCH_SIZE / WRITE_SIZE also calibrate the counters.
@@ -184,8 +204,8 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "warmup_run": {"steps": warm_steps + GAPLESS_STEPS, "seconds": round(warm_s, 3),
-                       "gapless_steps": GAPLESS_STEPS},
+        "warmup_run": {"steps": warm_steps + gapless, "seconds": round(warm_s, 3),
+                       "gapless_steps": gapless},
         "ms_per_step": round(ms_per_step, 4),
         "wall_s": round(wall, 3),   # host clock: the gapless warm-up steps and the timed steps
         "higher_is_better": True,
@@ -324,12 +344,19 @@ def encrypt_sweep(F, W, torch, dev, stream):
     esweep = {}
     sq = sq_profile("encrypt") or {}
     L2 = p2s.numel()
+    ins = [p2s] + [p2s.clone() for _ in range(ROTATE - 1)]   # four buffer sets, as in the decrypt sweep
+    outs = [o2s] + [torch.empty_like(o2s) for _ in range(ROTATE - 1)]
     for chain in w2s.chain_sizes:
         a2s = torch.from_numpy(w2s.aad(chain)).to(dev)
         n2 = F.num_chains(L2, chain)
-        t2s = torch.empty((n2, 16), dtype=torch.uint8, device=dev)
-        enc = lambda: F.encrypt_tag(w2s.key, w2s.base_iv, chain, p2s, a2s, out=o2s, tags=t2s)
-        ms = sorted(time_calls(torch, stream, enc, 20) for _ in range(3))[1]
+        tgs = [torch.empty((n2, 16), dtype=torch.uint8, device=dev) for _ in range(ROTATE)]
+        turn = [0]
+
+        def enc():
+            j = turn[0] % ROTATE
+            turn[0] += 1
+            F.encrypt_tag(w2s.key, w2s.base_iv, chain, ins[j], a2s, out=outs[j], tags=tgs[j])
+        ms = sorted(time_calls(torch, stream, enc, 20, pre=100) for _ in range(3))[1]
         name = "%dKiB" % (chain // KiB)
         e = {"gbps": round(L2 / ms / 1e6, 1), "us": round(ms * 1e3, 1),
              "hbm_frac": round((2 * L2 + n2 * (32 + 16)) / ms / 1e6 / HBM_PEAK_GBS, 4)}
@@ -413,26 +440,27 @@ def extras(F, W, torch, np, dev, stream, args):
     o2 = torch.empty_like(c2)
     k2 = torch.empty(t2.shape[0], dtype=torch.uint8, device=dev)
     vstream = torch.cuda.Stream()
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-    fused_l, pt_ms, ok_ms = [], [], []
-    for rep in range(21):
-        torch.cuda.synchronize()
-        ev[0].record(stream)
-        F.decrypt_verify(w2.key, w2.base_iv, chain2, c2, t2, a2, out=o2, ok=k2)
-        ev[1].record(stream)
-        torch.cuda.synchronize()
-        if rep:
-            fused_l.append(ev[0].elapsed_time(ev[1]))
-        ev[0].record(stream)
+    fused = lambda: F.decrypt_verify(w2.key, w2.base_iv, chain2, c2, t2, a2, out=o2, ok=k2)
+    fused_ms = time_calls(torch, stream, fused, 40, pre=100)
+    # Eager calls back to back and warm, each one's decryption waiting (on the device)
+    # for the previous call's verification: no call overlaps the next, and the GPU
+    # never idles between them. Plaintext ready = the decrypt stream's part; verified
+    # = through the verification on the second stream.
+    n_e, pre_e = 40, 60
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n_e)]
+    torch.cuda.synchronize()
+    for i in range(pre_e + n_e):
+        stream.wait_stream(vstream)
+        if i >= pre_e:
+            ev[i - pre_e][0].record(stream)
         e = F.decrypt_eager(w2.key, w2.base_iv, chain2, c2, t2, a2, out=o2, ok=k2, decrypt_stream=stream,
                             verify_stream=vstream)
-        ev[1].record(stream)
-        ev[2].record(vstream)
-        torch.cuda.synchronize()
-        if rep:
-            pt_ms.append(ev[0].elapsed_time(ev[1]))
-            ok_ms.append(ev[0].elapsed_time(ev[2]))
-    fused_ms = float(np.median(fused_l))
+        if i >= pre_e:
+            ev[i - pre_e][1].record(stream)
+            ev[i - pre_e][2].record(vstream)
+    torch.cuda.synchronize()
+    pt_ms = [x[0].elapsed_time(x[1]) for x in ev]
+    ok_ms = [x[0].elapsed_time(x[2]) for x in ev]
     assert not e.rejected() and torch.equal(o2, p2)
     res["eager"] = {"workload": "image-batch-64MiB, 64 KiB chains, 32-byte AAD",
                     "fused_us": round(fused_ms * 1e3, 1), "plaintext_ready_us": round(float(np.median(pt_ms)) * 1e3, 1),
