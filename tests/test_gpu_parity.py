@@ -123,6 +123,24 @@ def test_short_segments(F, length, chain, abytes):
     assert [i for i in range(n) if not ok[i]] == bad
 
 
+def test_long_single_chain(F):
+    """One 256 MiB chain (plus a partial block): 4097 segments of 4096 blocks, so the
+    segment weights H^((S-1-s) 2^12) use the squares H^(2^t) up to t = 24, which only
+    chains of millions of blocks reach."""
+    length, abytes = 256 * MiB + 48, 32
+    say("long single chain", length)
+    w = W.random_case(77, length, length, abytes)
+    aad = W.case_aad(w, length)
+    ct, tags = oracle.chains_encrypt(w.key, w.base_iv, length, w.payload, aad, abytes)
+    lab = "one chain of %d bytes" % length
+    assert check_decrypt(F, w.key, w.base_iv, length, ct, tags, aad, abytes, label=lab).all()
+    check_encrypt(F, w.key, w.base_iv, length, w.payload, aad, abytes, label=lab)
+    c2 = ct.copy()
+    W.flip_bit(c2, 8 * (length // 3) + 5)
+    pt, ok = F.decrypt_verify(w.key, w.base_iv, length, dev(c2), dev(tags), dev(aad))
+    assert not bool(ok.cpu().numpy()[0]), "a flipped bit one third into the chain was accepted"
+
+
 def test_tamper_positions(F):
     say("tamper positions")
     chain, length, abytes = 8192, 20 * 8192 + 40, 32
