@@ -300,13 +300,14 @@ __device__ __forceinline__ ItemPos item_pos(const GcmLaunch &p, uint64_t item)
 // The streaming kernel
 // ===========================================================================
 //
-// LDS layout (152 KiB + 64 B, one 1024-thread workgroup per CU):
+// LDS layout (152 KiB + 1600 B, one 1024-thread workgroup per CU):
 //   [0, 64 KiB)        row x (256 B) = T0[x] for lanes 0..31 | T1[x] for lanes 0..31
 //   [64, 128 KiB)      the 8-bit table of H^L: entry (k, v) at 64 KiB + (v*16 + k)*16
 //   [128, 152 KiB)     4-bit tables of H^(2^t), t = 0..2 (8 KiB each): the first levels of
 //                      the lane-combine tree (the rest weights eight-lane group sums from
 //                      the key's tables in global memory)
 //   [152 KiB, +512 B)  per-wave segment partials and tag masks (workgroup tag combine)
+//   then 1 KiB         the tag masks of the workgroup's items when wave 0 computes them all
 //   then 64 B          per-wave progress counters (see the priority steps in the kernel)
 // T_r[x] = rotl(T0[x], 8r), so T2[x] = rotl16(T0[x]) and T3[x] = rotl16(T1[x]): a
 // round column T0[a] ^ T1[b] ^ T2[c] ^ T3[d] ^ k is T0[a] ^ T1[b] ^ rotl16(T0[c] ^
@@ -328,8 +329,9 @@ constexpr int kTreeLds = 3;                  // of which levels 0..2 in LDS (the
 constexpr uint32_t kGhBase = 4096;           // uint4 index of the GHASH table (64 KiB)
 constexpr uint32_t kTreeBase = 8192;         // uint4 index of the tree tables (128 KiB)
 constexpr uint32_t kWgTagBase = (128 + 8 * kTreeLds) * 1024 / 16;   // uint4 index: 16 partials, 16 masks
+constexpr uint32_t kWgMaskBase = kWgTagBase + 32;                     // uint4 index: a tag mask per item (64)
 static_assert(kWavesPerWg <= 16 && kWavesPerWg % 4 == 0, "one workgroup-combine slot per wave");
-constexpr uint32_t kLdsBytes = (128 + 8 * kTreeLds) * 1024 + 512 + 64;
+constexpr uint32_t kLdsBytes = (128 + 8 * kTreeLds) * 1024 + 512 + 1024 + 64;
 // Modes without data AES: the GHASH table, T0 (for the J0 masks) and all six tree tables.
 constexpr uint32_t kT0GhashOnly = 4096;         // uint4 index: 64 KiB
 constexpr uint32_t kTreeBaseGhashOnly = 4160;   // 65 KiB
@@ -716,37 +718,55 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
     // Workgroup tag combine (fused uniform launches of one item per wave).
     constexpr bool kWgCombine = SPLIT && LL == 6 && MODE == kFused && !RAG;
     __builtin_amdgcn_s_setprio(3);
+    // The tag mask AES_K(J0) xor L . H for the item `bitem` in every lane that needs
+    // one (its item exists and starts its chain, segment 0); zero in the others,
+    // which stay inactive through the AES, so a pass reads the LDS for those lanes
+    // only. A wave-collective (len_terms); all lanes must call it.
+    auto mask_pass = [&](uint64_t bitem) {
+        const ItemPos bp = item_pos<RAG>(p, bitem < p.n_items ? bitem : p.n_items - 1);
+        uint32_t biv[3];
+        chain_iv(p, p.chain_base + bp.chain, biv);
+        const u4 j0 = {{biv[0], biv[1], biv[2], bswap32(1u)}};   // J0 = IV_i || 0^31 || 1
+        const bool need = bitem < p.n_items && bp.s == 0;
+        u4 lenh = zero4();
+        if constexpr (!RAG) {
+            const LenTerms lt = len_terms(p, &tree[0], lane);
+            lenh = bp.chain == p.n_chains - 1 ? lt.last : lt.full;
+        }
+        u4 m = zero4();
+        if (need) {
+            if constexpr (RAG) {   // every chain has its own length: each lane multiplies its own
+                const uint64_t abits = (uint64_t)p.aad_bytes * 8, cbits = bp.len * 8;
+                const u4 lens = {{bswap32((uint32_t)(abits >> 32)), bswap32((uint32_t)abits),
+                                  bswap32((uint32_t)(cbits >> 32)), bswap32((uint32_t)cbits)}};
+                lenh = mul_tab4(lens, &tree[0]);
+            }
+            u4 e;
+            if constexpr (kAes)
+                e = aes_block_lds(lds, rk, j0, lc0, lc1);
+            else
+                e = aes256_encrypt_tt(j0, c->rk, [&](uint32_t x) { return t0l[x]; });
+            m = xor4(e, lenh);
+        }
+        return m;
+    };
+    // A full uniform launch (one wave-item per wave): wave 0 computes the masks of
+    // all the workgroup's items in one pass, a lane per item, and leaves them in LDS
+    // for the other waves, which read them after a barrier before their tags. A pass
+    // costs the LDS nearly as much with a few lanes active as with 64, so one pass
+    // per workgroup instead of one per wave frees LDS time for the main loop (the 4
+    // and 16 KiB chains of the 64 MiB batch have one or four items per wave).
+    const bool wg_masks = MODE == kFused && !RAG && !spread && n_wave_items == nwaves;
+    if (wg_masks && wslot == 0) {
+        const uint64_t bitem = ((uint64_t)blockIdx.x * kWavesPerWg + lane / G) * G + lane % G;
+        const u4 m = mask_pass(lane < kWavesPerWg * G ? bitem : p.n_items);
+        if (lane < kWavesPerWg * G)
+            lds4[kWgMaskBase + lane] = make_uint4(m.w[0], m.w[1], m.w[2], m.w[3]);
+    }
     for (uint64_t wi = wave; wi < n_wave_items; wi += nwaves, ++it) {
         const uint32_t bi = it & (L - 1);
-        if (kGhash && bi == 0) {
-            const uint64_t bitem = (wi + (uint64_t)(lane >> (6 - LL)) * nwaves) * G + (lane & (G - 1));
-            const ItemPos bp = item_pos<RAG>(p, bitem < p.n_items ? bitem : p.n_items - 1);
-            uint32_t biv[3];
-            chain_iv(p, p.chain_base + bp.chain, biv);
-            const u4 j0 = {{biv[0], biv[1], biv[2], bswap32(1u)}};   // J0 = IV_i || 0^31 || 1
-            // Only lanes whose item exists and starts its chain (segment 0) need a mask;
-            // the others stay inactive, so the pass costs LDS lookups for those lanes only.
-            const bool need = bitem < p.n_items && bp.s == 0;
-            u4 lenh = zero4();
-            if constexpr (!RAG) {
-                const LenTerms lt = len_terms(p, &tree[0], lane);
-                lenh = bp.chain == p.n_chains - 1 ? lt.last : lt.full;
-            }
-            if (need) {
-                if constexpr (RAG) {   // every chain has its own length: each lane multiplies its own
-                    const uint64_t abits = (uint64_t)p.aad_bytes * 8, cbits = bp.len * 8;
-                    const u4 lens = {{bswap32((uint32_t)(abits >> 32)), bswap32((uint32_t)abits),
-                                      bswap32((uint32_t)(cbits >> 32)), bswap32((uint32_t)cbits)}};
-                    lenh = mul_tab4(lens, &tree[0]);
-                }
-                u4 e;
-                if constexpr (kAes)
-                    e = aes_block_lds(lds, rk, j0, lc0, lc1);
-                else
-                    e = aes256_encrypt_tt(j0, c->rk, [&](uint32_t x) { return t0l[x]; });
-                jmask = xor4(e, lenh);
-            }
-        }
+        if (kGhash && bi == 0 && !wg_masks)
+            jmask = mask_pass((wi + (uint64_t)(lane >> (6 - LL)) * nwaves) * G + (lane & (G - 1)));
         const uint64_t item = wi * G + gs;
         const bool valid = item < p.n_items;
         const ItemPos ip = item_pos<RAG>(p, valid ? item : p.n_items - 1);
@@ -1013,8 +1033,15 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                 }
                 const uint32_t src_lane = bi * G + gs;
                 u4 e;
-                for (int w = 0; w < 4; ++w)   // one item per wave: the mask's lane bi is uniform
-                    e.w[w] = LL == 6 ? __builtin_amdgcn_readlane(jmask.w[w], bi) : __shfl(jmask.w[w], (int)src_lane, 64);
+                if (wg_masks) {   // wave 0's masks of this workgroup's items
+                    __syncthreads();
+                    const uint4 m = lds4[kWgMaskBase + wslot * G + gs];
+                    e = u4{{m.x, m.y, m.z, m.w}};
+                } else {
+                    for (int w = 0; w < 4; ++w)   // one item per wave: the mask's lane bi is uniform
+                        e.w[w] = LL == 6 ? __builtin_amdgcn_readlane(jmask.w[w], bi)
+                                         : __shfl(jmask.w[w], (int)src_lane, 64);
+                }
                 if (kWgCombine && p.wg_tag) {   // the workgroup tags the chain after its barrier
                     if (valid && jl == 0) {
                         lds4[kWgTagBase + wslot] = make_uint4(acc.w[0], acc.w[1], acc.w[2], acc.w[3]);
@@ -1031,8 +1058,15 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                 // The slot holds its chain's whole GHASH(A || C) . H:
                 // T = GHASH(A || C) . H xor L . H xor AES_K(J0).
                 u4 e;
-                for (int w = 0; w < 4; ++w)
-                    e.w[w] = LL == 6 ? __builtin_amdgcn_readlane(jmask.w[w], bi) : __shfl(jmask.w[w], (int)(bi * G + gs), 64);
+                if (wg_masks) {   // wave 0's masks of this workgroup's items
+                    __syncthreads();
+                    const uint4 m = lds4[kWgMaskBase + wslot * G + gs];
+                    e = u4{{m.x, m.y, m.z, m.w}};
+                } else {
+                    for (int w = 0; w < 4; ++w)
+                        e.w[w] = LL == 6 ? __builtin_amdgcn_readlane(jmask.w[w], bi)
+                                         : __shfl(jmask.w[w], (int)(bi * G + gs), 64);
+                }
                 if (valid && jl == 0)
                     emit_tag<ENC>(p, gchain, xor4(acc, e), got);
             }
