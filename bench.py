@@ -41,6 +41,10 @@ WARMUP_MIN_S = 0.3
 # the probe: 2.18 -> 2.22 -> 2.26 GHz in 10 ms chunks, then steady).
 GAPLESS_S = 0.05
 ROTATE = 4                       # buffer sets the per-size timings cycle through
+# LDS reads per 64 blocks of the streaming kernel's main loop and their measured cost
+# (CU-cycles per wave instruction, conflict-free, 16 waves per CU)
+LDS_T_READS, LDS_T_CYCLES = 197, 2.8
+LDS_GH_READS, LDS_GH_CYCLES = 16, 5.5
 
 KiB, MiB, GiB = 1024, 1 << 20, 1 << 30
 
@@ -189,6 +193,16 @@ def main():
     log("decrypt sweep %.1f GB/s, %.3f ms/step, %.1f us/launch (per-size mean %.1f us), clock %s GHz, copy %.0f GB/s"
         % (value, ms_per_step, launch_ms * 1e3, per_size_mean_ms * 1e3, ["%.2f" % c for c in clocks], copy_gbs))
     sq = sq_profile("decrypt")
+    # The LDS bound of the main loop: per 64 blocks (one wave-iteration) 197 conflict-free
+    # 32-bit T-table reads at 2.8 CU-cycles each and 16 conflict-free 16-byte GHASH reads
+    # at 5.5 (microbenchmarks on the box), over 256 CUs at the clock the probe measured.
+    lds_cycles = LDS_T_READS * LDS_T_CYCLES + LDS_GH_READS * LDS_GH_CYCLES
+    clk = float(np.mean(clocks))
+    bound_us = L / 16 / 64 / 256 * lds_cycles / (clk * 1e3)
+    lds_bound = {"cycles_per_64_blocks": round(lds_cycles, 1), "clock_ghz": round(clk, 3),
+                 "main_loop_bound_us": round(bound_us, 2), "frac": round(bound_us / (launch_ms * 1e3), 3),
+                 "note": "launch time against the LDS time of the main loop alone at the measured clock; the "
+                         "rest of a launch is set-up and tail"}
     valu = None
     if sq:
         insts = float(np.mean([sq[k] for k in sq]))   # VALU wave-instructions per launch, mean over the sizes
@@ -231,6 +245,7 @@ def main():
                      "frac_of_device_copy": round(hbm_gbs / copy_gbs, 4),
                      "limiter": "LDS table reads and integer VALU issue (the AES T-table lookups and GHASH "
                                 "table lookups), not HBM",
+                     "lds_bound": lds_bound,
                      "valu": valu},
     }
 
