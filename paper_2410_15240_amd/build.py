@@ -45,12 +45,18 @@ def build(verbose: bool = False) -> str:
             print(" ".join(cmd), flush=True)
         procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)))
         objs.append(obj)
+    failed = []
     for src, pr in procs:
         out = "\n".join(l for l in pr.communicate()[0].splitlines() if noise not in l)
         if pr.returncode != 0:
-            raise RuntimeError("hipcc failed on %s:\n%s" % (src, out))
-        if verbose and out.strip():
+            failed.append("hipcc failed on %s:\n%s" % (src, out))
+        elif verbose and out.strip():
             print(out)
+    if failed:   # no partial objects left behind in the package
+        for o in objs:
+            if os.path.exists(o):
+                os.remove(o)
+        raise RuntimeError("\n".join(failed))
     cmd = [hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC"] + objs + ["-o", tmp, "-Wl,-rpath,/opt/rocm/lib"]
     if verbose:
         print(" ".join(cmd), flush=True)
