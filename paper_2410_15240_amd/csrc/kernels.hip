@@ -763,9 +763,30 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
         if (lane < kWavesPerWg * G)
             lds4[kWgMaskBase + lane] = make_uint4(m.w[0], m.w[1], m.w[2], m.w[3]);
     }
+    // Launches that leave waves without a wave-item (small ones) and are tagged by the
+    // per-chain kernel: the idle waves compute the chains' masks, one lane per chain,
+    // so the mask pass is off the working waves' path (AES of J0 is one more block
+    // per chain, its position fixed by the chain index alone).
+    const bool idle_masks = kGhash && SPLIT && p.idle_masks != 0;
+    if (idle_masks && wave >= n_wave_items) {
+        const uint64_t c0 = ((uint64_t)wave - n_wave_items) * 64;   // uniform
+        if (c0 < p.n_chains) {
+            const uint64_t c = c0 + lane;
+            uint64_t bitem = p.n_items;   // no chain: nothing needed
+            if (c < p.n_chains) {
+                if constexpr (RAG)
+                    bitem = p.rchains[c].item0;
+                else
+                    bitem = c * p.segs_full;
+            }
+            const u4 m = mask_pass(bitem);
+            if (c < p.n_chains)
+                p.masks[c] = make_uint4(m.w[0], m.w[1], m.w[2], m.w[3]);
+        }
+    }
     for (uint64_t wi = wave; wi < n_wave_items; wi += nwaves, ++it) {
         const uint32_t bi = it & (L - 1);
-        if (kGhash && bi == 0 && !wg_masks)
+        if (kGhash && bi == 0 && !wg_masks && !idle_masks)
             jmask = mask_pass((wi + (uint64_t)(lane >> (6 - LL)) * nwaves) * G + (lane & (G - 1)));
         const uint64_t item = wi * G + gs;
         const bool valid = item < p.n_items;
@@ -1051,7 +1072,7 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                     }
                 } else if (valid && jl == 0) {
                     p.partials[item] = make_uint4(acc.w[0], acc.w[1], acc.w[2], acc.w[3]);
-                    if (ip.s == 0)
+                    if (ip.s == 0 && !idle_masks)
                         p.masks[ip.chain] = make_uint4(e.w[0], e.w[1], e.w[2], e.w[3]);
                 }
             } else {
@@ -1215,6 +1236,7 @@ static hipError_t launch_mode(const GcmLaunch &p, int num_cu, hipStream_t s)
     GcmLaunch q = p;
     q.wg_tag = MODE == kFused && !RAG && split && p.lanes_log2 == 6 && p.n_items == wgs * kWavesPerWg &&
                p.segs_full <= (uint32_t)kWavesPerWg && kWavesPerWg % p.segs_full == 0;
+    q.idle_masks = split && !q.wg_tag && wgs * kWavesPerWg >= waves + (p.n_chains + 63) / 64;
     if (p.lanes_log2 == 4 && !split)
         hipLaunchKernelGGL((gcm_kernel<ENC, 4, false, MODE, RAG>), dim3((uint32_t)wgs), dim3(kThreads), 0, s, q);
     else if (p.lanes_log2 == 4)

@@ -86,6 +86,10 @@ struct GcmLaunch {
     // segments on consecutive waves of one workgroup (a segment count dividing 16):
     // the workgroup sums them in LDS and tags the chain itself (no second kernel).
     uint32_t wg_tag;
+    // Split launches tagged by the per-chain kernel whose grid has at least
+    // ceil(n_chains / 64) waves beyond its wave-items: those waves compute every
+    // chain's mask (one lane per chain) and the working waves skip theirs.
+    uint32_t idle_masks;
     // Ragged launches (chains of their own lengths and offsets): the chain table
     // and each item's chain; chain_bytes, qc, last_len and the segs_* fields
     // are then unused. NULL for uniform chains.
