@@ -42,7 +42,7 @@ int hip_fail(hipError_t e, const char *what)
 constexpr uint64_t kMaxChainBlocks = 0xFFFFFFFEull;   // GCM: at most 2^32 - 2 blocks per message
 constexpr size_t kMaxKeys = 8;
 constexpr int kMinSegLog2 = 8;                          // segments of >= 256 blocks (4 per lane)
-constexpr int kMinSmallSegLog2 = 6;                     // small launches: down to 64 blocks (1 per lane)
+constexpr int kMinSmallSegLog2 = 7;                     // small launches: down to 128 blocks (2 per lane)
 constexpr uint64_t kMaxSmallSegs = 512;                 // ... with at most this many segments per chain
 constexpr int kMaxPipelineDepth = 8;                    // staging-ring slots
 constexpr uint64_t kD2hGroupBytes = 32ull << 20;        // D2H: encrypted bytes per copy-stream wait
@@ -358,10 +358,12 @@ void make_plan(uint64_t len, uint64_t chain_bytes, uint64_t chain_base, uint64_t
         while (lg > (uint32_t)kMinSegLog2 && items_at(lg) < slots)
             --lg;
         // Small launches, where even 256-block segments leave more than half of the
-        // waves idle: shorter segments, down to one iteration of the 64 lanes, while
+        // waves idle: shorter segments, down to two iterations of the 64 lanes, while
         // a chain stays at most 512 segments (the tag sums and segment weights grow
-        // with the count). 1 MiB of 64 KiB chains: 21.8 -> 16.3 us; one 1 MiB chain
-        // 22.3 -> 19.9 us; 4 MiB of 1 MiB chains 23.7 -> 22.8 us.
+        // with the count). 1 MiB of 64 KiB chains: 21.8 us with 256-block segments,
+        // 18.2 with 128, 19.5 with 64 (whose 6-bit segment weights cost more than the
+        // shorter items gain); one 1 MiB chain 22.3 -> 19.6 us; 4 MiB of 1 MiB chains
+        // 23.7 -> 21.4 us.
         while (lg > (uint32_t)kMinSmallSegLog2 && items_at(lg) < slots / 2 &&
                ((qc + (1ull << (lg - 1)) - 1) >> (lg - 1)) <= kMaxSmallSegs)
             --lg;

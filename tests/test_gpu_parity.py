@@ -96,7 +96,7 @@ def test_small_shapes(F, length, chain, abytes):
 
 
 # Launches that leave most waves idle cut chains into short segments (down to
-# 64 blocks, at most 512 per chain): one-iteration segments of 64 KiB chains,
+# 128 blocks, at most 512 per chain): two-iteration segments of 64 KiB chains,
 # 128-block segments of 1 MiB chains, with AAD, tails and tampering inside
 # middle segments.
 SEGMENTED = [(1 * MiB, 64 * KiB, 32), (2 * MiB, 1 * MiB, 32), (4 * MiB - 16, 1 * MiB, 1000),
