@@ -67,6 +67,21 @@ enum fastrack_status {
 uint64_t fastrack_num_chains(uint64_t len, uint64_t chain_bytes);
 
 /*
+ * The work plan of a uniform-chain launch, host only (nothing is enqueued, no
+ * device is touched): how decrypt + verify and encrypt + tag cut the chains of
+ * `len` bytes (section 5.2: each chain is one GCM message) into work items for
+ * a GPU with num_cu compute units. A chain of q blocks is cut into segments of
+ * 2^seg_log2 blocks aligned to its end (segment 0 takes the rest); each item is
+ * one segment, run by 2^lanes_log2 lanes for `iters` iterations.
+ *   out[7]  lanes_log2, seg_log2, segments of a full chain, segments of the last
+ *           chain, work items, iterations per item, 1 if chains are cut into
+ *           several segments (0: every item is a whole chain)
+ * EINVAL: NULL out, num_cu == 0, len == 0, chain_bytes as for decrypt, more than
+ * 2^32 - 1 chains.
+ */
+int fastrack_plan(uint64_t len, uint64_t chain_bytes, uint32_t num_cu, uint64_t *out);
+
+/*
  * Decrypt and verify (paper section 5.2: the receiver decrypts with AES-CTR and
  * regenerates each chain's GMAC tag to compare against the received one).
  *   d_ct    [len] ciphertext on the device

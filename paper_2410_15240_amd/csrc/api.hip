@@ -508,6 +508,29 @@ FT_EXPORT uint64_t fastrack_num_chains(uint64_t len, uint64_t chain_bytes)
 
 FT_EXPORT const char *fastrack_last_error(void) { return g_err.c_str(); }
 
+FT_EXPORT int fastrack_plan(uint64_t len, uint64_t chain_bytes, uint32_t num_cu, uint64_t *out)
+{
+    g_err.clear();
+    if (!out || num_cu == 0)
+        return fail(FASTRACK_EINVAL, "out must be non-NULL and num_cu nonzero");
+    if (chain_bytes == 0 || chain_bytes % 16 != 0 || chain_bytes / 16 > kMaxChainBlocks)
+        return fail(FASTRACK_EINVAL, "chain_bytes must be a nonzero multiple of 16, at most (2^32-2)*16");
+    if (len == 0 || (len + chain_bytes - 1) / chain_bytes > 0xFFFFFFFFull)
+        return fail(FASTRACK_EINVAL, "len must be nonzero, with at most 2^32-1 chains");
+    GcmLaunch p;
+    std::memset(&p, 0, sizeof p);
+    make_plan(len, chain_bytes, 0, (uint64_t)num_cu * kGcmWavesPerWg * gcm_wgs_per_cu(kFused), p);
+    const uint64_t L = 1ull << p.lanes_log2, seg = 1ull << p.seg_log2;
+    out[0] = p.lanes_log2;
+    out[1] = p.seg_log2;
+    out[2] = p.segs_full;
+    out[3] = p.segs_last;
+    out[4] = p.n_items;
+    out[5] = ((seg < p.qc ? seg : p.qc) + L - 1) >> p.lanes_log2;   // the kernel's iterations per item
+    out[6] = p.n_items > p.n_chains ? 1u : 0u;
+    return FASTRACK_OK;
+}
+
 FT_EXPORT int fastrack_gcm_decrypt_verify(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
                                           const uint8_t *d_ct, uint64_t len, const uint8_t *d_tags,
                                           const uint8_t *d_aad, uint32_t aad_bytes, uint8_t *d_pt, uint8_t *d_ok,
