@@ -111,13 +111,12 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
     __shared__ uint32_t s_sbox[256];
     __shared__ uint32_t s_t0[256];
     __shared__ uint32_t s_rk[60];
-    __shared__ u4 s_hp[kMaxPow + 2];
     __shared__ u4 s_hsq[kSquares];
+    __shared__ u4 s_h8k[8];
     const int tid = threadIdx.x;
     const uint32_t lane = tid & 63, wave = (uint32_t)tid >> 6;
-    constexpr uint32_t kWaves = 1024 / 64;
 
-    // wave 7 + k holds the columns of S^k (k = 1..8) for the squares at the end
+    // wave 7 + k holds the columns of S^k (k = 1..8) for the squares
     constexpr uint32_t kFrobWave0 = 8;
     WaveLinear frob;
     if (wave >= kFrobWave0)
@@ -147,59 +146,53 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
 #pragma unroll
         for (int j = 0; j < 4; ++j)
             h.w[j] = __builtin_amdgcn_readlane(col, j);
-        if (lane == 0) {
-            const u4 one = {{0x80u, 0u, 0u, 0u}};   // the block 0x80 || 0^120 is 1
-            s_hp[0] = one;
-            s_hp[1] = h;
-        }
+        if (lane == 0)
+            s_hsq[0] = h;
         if (lane < 4)
             ctx->h[lane] = col;
     }
     __syncthreads();
 
-    // Powers by doubling: H^(2^r + j) = H^j . H^(2^r), j = 1..2^r. Multiplying by
-    // the level's H^(2^r) is one linear map, whose columns every working wave
-    // builds; its products are then one application each.
-    for (int r = 0; r < 6; ++r) {
-        const uint32_t half = 1u << r;
-        if (1 + wave <= half) {
-            const u4 y = to_be(s_hp[half]);
-            WaveLinear mul;
-            mul.c0 = be_mul_xk_any(y, (int)lane);
-            mul.c1 = be_mul_xk_any(y, (int)lane + 64);
-            for (uint32_t j = 1 + wave; j <= half; j += kWaves) {
-                const u4 prod = from_be(mul.apply(to_be(s_hp[j]), lane));
-                if (lane == 0)
-                    s_hp[half + j] = prod;
-            }
-        }
-        __syncthreads();
-    }
-    if (wave == 0) {   // H^65 = H^64 . H
-        const u4 y = to_be(s_hp[1]);
+    // Squares eight at a time: H^(2^(b + k)) = S^k(H^(2^b)), k = 1..8, one wave each,
+    // in four rounds. The tables need H^8, H^16, ..., H^64: four are squares, and
+    // the other four are products of them, formed by waves 0..2 during the rounds
+    // after the first (H^24 = H^16 . H^8, H^40 = H^32 . H^8, H^48 = H^32 . H^16,
+    // then H^56 = H^48 . H^8). A product by Y is one linear map whose columns the
+    // wave builds (Y . x^k for its lanes k and k + 64).
+    auto times = [&](const u4 &x, const u4 &y) {
+        const u4 yb = to_be(y);
         WaveLinear mul;
-        mul.c0 = be_mul_xk_any(y, (int)lane);
-        mul.c1 = be_mul_xk_any(y, (int)lane + 64);
-        const u4 prod = from_be(mul.apply(to_be(s_hp[kMaxPow]), lane));
-        if (lane == 0)
-            s_hp[kMaxPow + 1] = prod;
-        if (lane < 7)   // squares H^(2^t), t <= 6, are powers already
-            s_hsq[lane] = s_hp[1u << lane];
-    }
-    __syncthreads();
-    // The rest eight at a time: H^(2^(b + k)) = S^k(H^(2^b)), k = 1..8, one wave each.
-    for (int b = 6; b < kSquares - 1; b += 8) {
+        mul.c0 = be_mul_xk_any(yb, (int)lane);
+        mul.c1 = be_mul_xk_any(yb, (int)lane + 64);
+        return from_be(mul.apply(to_be(x), lane));
+    };
+    for (int r = 0; r < 4; ++r) {
+        const int b = 8 * r;
         const int t = b + (int)(wave - kFrobWave0 + 1);
         if (wave >= kFrobWave0 && t < kSquares) {
             const u4 v = frob.apply(to_be(s_hsq[b]), lane);
             if (lane == 0)
                 s_hsq[t] = from_be(v);
         }
+        if (r == 1 && wave < 3) {   // H^24, H^40, H^48 (H^(2^t) for t <= 8 are in place)
+            const u4 x = s_hsq[wave == 2 ? 5 : 4 + (wave & 1)], y = s_hsq[wave == 2 ? 4 : 3];
+            const u4 prod = times(x, y);
+            if (lane == 0)
+                s_h8k[wave == 0 ? 2 : (wave == 1 ? 4 : 5)] = prod;
+        }
+        if (r == 2 && wave == 0) {   // H^56 = H^48 . H^8
+            const u4 prod = times(s_h8k[5], s_hsq[3]);
+            if (lane == 0)
+                s_h8k[6] = prod;
+        }
         __syncthreads();
     }
-    for (int i = tid; i <= kMaxPow + 1; i += blockDim.x)
+    if (tid < 8) {   // the squares among H^(8 (i + 1)): H^8, H^16, H^32, H^64
+        const int sq = tid == 0 ? 3 : (tid == 1 ? 4 : (tid == 3 ? 5 : (tid == 7 ? 6 : -1)));
+        const u4 v = sq >= 0 ? s_hsq[sq] : s_h8k[tid];
         for (int j = 0; j < 4; ++j)
-            ctx->hp[i][j] = s_hp[i].w[j];
+            ctx->h8k[tid][j] = v.w[j];
+    }
     for (int i = tid; i < kSquares; i += blockDim.x)
         for (int j = 0; j < 4; ++j)
             ctx->hsq[i][j] = s_hsq[i].w[j];
@@ -226,7 +219,7 @@ __global__ __launch_bounds__(kTableThreads) void key_tables_kernel(KeyCtx *__res
     if (ent >= kTab8Entries)
         return;
     const uint32_t i = ent >> 12, k = (ent >> 8) & 15, v = ent & 255;
-    const uint32_t *hp = ctx->hp[8 * (i + 1)];
+    const uint32_t *hp = ctx->h8k[i];
     u4 b = be_mul_xk_any(to_be(u4{{hp[0], hp[1], hp[2], hp[3]}}), (int)(8 * k));   // degree 8k: v's bit 7
     u4 e = {{0u, 0u, 0u, 0u}};
     for (int bit = 7; bit >= 0; --bit) {

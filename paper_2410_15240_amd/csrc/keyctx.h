@@ -19,7 +19,6 @@ namespace fastrack {
 
 constexpr int kTab4Pos = 32;    // nibble positions of a 128-bit operand
 constexpr int kTab4Ent = 16;    // values of a nibble
-constexpr int kMaxPow = 64;     // powers H^1 .. H^64 (Horner multipliers up to one wave of 64 lanes)
 constexpr int kSquares = 32;    // H^(2^t), t = 0..31 (chains are < 2^32 blocks)
 
 struct Tab4 {                   // 4-bit positional multiplication table of a fixed Y:
@@ -32,7 +31,7 @@ struct KeyCtx {
     uint32_t t0[256];           // T0[x] = {02}S(x) | S(x)<<8 | S(x)<<16 | {03}S(x)<<24
     uint8_t sbox[256];
     uint32_t h[4];              // H = AES_K(0^128)
-    uint32_t hp[kMaxPow + 2][4];      // hp[e] = H^e, e = 0..65 (hp[0] = 1)
+    uint32_t h8k[8][4];         // h8k[i] = H^(8 (i + 1)): H^8, H^16, ..., H^64
     uint32_t hsq[kSquares][4];        // hsq[t] = H^(2^t)
     Tab4 h1_tab;                // table of H
     Tab4 sq_tab[kSquares];      // sq_tab[t]: table of H^(2^t) (t = 0..5 also combine the lanes of an item)
