@@ -40,6 +40,9 @@ WARMUP_MIN_S = 0.3
 # synchronisations the clock still climbs for 20-30 ms of gap-free load (measured with
 # the probe: 2.18 -> 2.22 -> 2.26 GHz in 10 ms chunks, then steady).
 GAPLESS_S = 0.05
+# Every other timed leg (per-size launches, encrypt sweep, the extra workloads) first
+# runs its own calls gap-free for this long, at most PRE_MAX_CALLS of them.
+PRE_S, PRE_MAX_CALLS = 0.05, 2000
 ROTATE = 4                       # buffer sets the per-size timings cycle through
 # LDS reads per 64 blocks of the streaming kernel's main loop and their measured cost
 # (CU-cycles per wave instruction, conflict-free, 16 waves per CU)
@@ -147,9 +150,10 @@ def main():
         assert bool(ok.all()), "benchmark decrypt rejected a chain"
         assert torch.equal(out, payload), "benchmark decrypt produced wrong plaintext"
     # Per chain size: 20 back-to-back launches of that size between two events, three
-    # times; the median of the three. Each run starts with 100 untimed launches of the
-    # size, gap-free (the checks above leave the GPU idle, and the clock dips for
-    # several milliseconds after that: with 20 the first size measured ~15% slow).
+    # times with no idle gap between the runs; the median of the three. The runs follow
+    # 50 ms of untimed launches of the size, gap-free (the checks above leave the GPU
+    # idle, and the clock dips for several milliseconds after that: after 100 launches
+    # (8 ms) the first size still measured a few percent slow).
     # The launches of one size cycle through four copies of its buffers (512 MiB in all),
     # as the sweep's five sizes do (640 MiB): re-reading one 64 MiB buffer would be
     # served partly by the 256 MB Infinity Cache.
@@ -163,15 +167,15 @@ def main():
             c_, t_, o_, k_ = sets[turn[0] % ROTATE]
             turn[0] += 1
             F.decrypt_verify(w.key, w.base_iv, chain, c_, t_, aad, out=o_, ok=k_)
-        per.append(sorted(time_calls(torch, stream, one, 20, pre=100) for _ in range(3))[1])
+        per.append(time_calls(torch, stream, one, 20, runs=3))
         for c_, t_, o_, k_ in sets:
             assert bool(k_.all()) and torch.equal(o_, payload), "benchmark decrypt produced wrong plaintext"
         del sets
     # The achievable HBM rate on this machine: a plain 64 MiB device-to-device copy
-    # (read + write bytes over time, best of three runs of 20 copies). Under
+    # (read + write bytes over time, best of five gap-free runs of 20 copies). Under
     # rocprofv3 --pmc its FETCH_SIZE / WRITE_SIZE also calibrate the counters.
     dst, src = cases[0][4], cases[0][1]
-    copy_ms = min(time_calls(torch, stream, lambda: dst.copy_(src), 20) for _ in range(3))
+    copy_ms = time_runs(torch, stream, lambda: dst.copy_(src), 20, 5)[0]
     copy_gbs = 2 * src.numel() / (copy_ms * 1e-3) / 1e9
     torch.cuda.synchronize()
     ms_per_step = total_ms / args.steps
@@ -329,26 +333,35 @@ def sq_profile(direction):
         return None
 
 
-def time_calls(torch, stream, fn, reps, pre=None):
-    """Mean time of one call (ms) over `reps` back-to-back calls between two events.
-    Untimed calls run first with no idle gap before the timed ones (after idling,
-    the GPU runs its first milliseconds at a lower clock): `pre` of them, or by
-    default as many as fill about 8 ms."""
+def time_runs(torch, stream, fn, reps, runs):
+    """Times of one call (ms, sorted): the mean over `reps` back-to-back calls between
+    two events, for each of `runs` runs that follow one another with no idle gap.
+    Untimed calls filling about PRE_S seconds run first, straight into the timed ones:
+    after idling, the GPU runs its first milliseconds at a lower clock, which then
+    keeps climbing for 20-30 ms."""
     torch.cuda.synchronize()
-    if pre is None:
-        t0 = time.perf_counter()
+    t0 = time.perf_counter()
+    for _ in range(4):
         fn()
-        torch.cuda.synchronize()
-        pre = min(200, max(1, int(8e-3 / max(time.perf_counter() - t0, 1e-6))))
-    for _ in range(pre):
-        fn()
-    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    a.record(stream)
-    for _ in range(reps):
-        fn()
-    b.record(stream)
     torch.cuda.synchronize()
-    return a.elapsed_time(b) / reps
+    one = max((time.perf_counter() - t0) / 4, 1e-6)
+    for _ in range(min(PRE_MAX_CALLS, max(1, int(PRE_S / one)))):
+        fn()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(runs)]
+    for a, b in evs:
+        a.record(stream)
+        for _ in range(reps):
+            fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return sorted(a.elapsed_time(b) / reps for a, b in evs)
+
+
+def time_calls(torch, stream, fn, reps, runs=1):
+    """Median over `runs` gap-free runs of the mean time of one call (ms) over `reps`
+    back-to-back calls (see time_runs)."""
+    ts = time_runs(torch, stream, fn, reps, runs)
+    return ts[len(ts) // 2]
 
 
 def encrypt_sweep(F, W, torch, dev, stream):
@@ -371,7 +384,7 @@ def encrypt_sweep(F, W, torch, dev, stream):
             j = turn[0] % ROTATE
             turn[0] += 1
             F.encrypt_tag(w2s.key, w2s.base_iv, chain, ins[j], a2s, out=outs[j], tags=tgs[j])
-        ms = sorted(time_calls(torch, stream, enc, 20, pre=100) for _ in range(3))[1]
+        ms = time_calls(torch, stream, enc, 20, runs=3)
         name = "%dKiB" % (chain // KiB)
         e = {"gbps": round(L2 / ms / 1e6, 1), "us": round(ms * 1e3, 1),
              "hbm_frac": round((2 * L2 + n2 * (32 + 16)) / ms / 1e6 / HBM_PEAK_GBS, 4)}
@@ -456,7 +469,7 @@ def extras(F, W, torch, np, dev, stream, args):
     k2 = torch.empty(t2.shape[0], dtype=torch.uint8, device=dev)
     vstream = torch.cuda.Stream()
     fused = lambda: F.decrypt_verify(w2.key, w2.base_iv, chain2, c2, t2, a2, out=o2, ok=k2)
-    fused_ms = time_calls(torch, stream, fused, 40, pre=100)
+    fused_ms = time_calls(torch, stream, fused, 40)
     # Eager calls back to back and warm, each one's decryption waiting (on the device)
     # for the previous call's verification: no call overlaps the next, and the GPU
     # never idles between them. Plaintext ready = the decrypt stream's part; verified
@@ -512,14 +525,13 @@ def extras(F, W, torch, np, dev, stream, args):
     # 100 untimed calls first: the first calls of this leg also touch freshly allocated
     # table slots and staging (slower for the first ~50 calls on the box)
     rag_ms = time_calls(torch, stream, lambda: F.decrypt_verify_ragged(w6.key, w6.base_iv, off6, ln6, c6, t6, a6,
-                                                                      out=o6, ok=k6), 40, pre=100)
+                                                                      out=o6, ok=k6), 40)
     assert bool(k6.all())
     enc_ms = time_calls(torch, stream, lambda: F.encrypt_tag_ragged(w6.key, w6.base_iv, off6, ln6, p6, a6, out=o6,
-                                                                   tags=t6), 40, pre=100)
+                                                                   tags=t6), 40)
     cu, tu = F.encrypt_tag(w6.key, w6.base_iv, 8 * KiB, p6)
     ku = torch.empty(tu.shape[0], dtype=torch.uint8, device=dev)
-    uni_ms = time_calls(torch, stream, lambda: F.decrypt_verify(w6.key, w6.base_iv, 8 * KiB, cu, tu, out=o6, ok=ku), 40,
-                        pre=100)
+    uni_ms = time_calls(torch, stream, lambda: F.decrypt_verify(w6.key, w6.base_iv, 8 * KiB, cu, tu, out=o6, ok=ku), 40)
     nbytes = int(ln6.sum())
     res["ragged"] = {"workload": "sample-batch: 1024 samples (log-normal sizes, median 110 KiB) x 16 chains, "
                                  "1-byte serial AAD, %.1f MiB" % (total6 / MiB),
