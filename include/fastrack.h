@@ -121,8 +121,8 @@ int fastrack_gcm_decrypt_verify(const uint8_t *key, const uint8_t *base_iv, uint
  * library's work planner stays below about 200,000 for every size, so this
  * limit is a guard, not a size cap callers meet.
  */
-#define FASTRACK_NOALLOC_SCRATCH_BYTES (4u << 20)
-#define FASTRACK_NOALLOC_MAX_PARTIALS 212320u
+#define FASTRACK_NOALLOC_SCRATCH_BYTES (5u << 20)
+#define FASTRACK_NOALLOC_MAX_PARTIALS 230240u
 int fastrack_gcm_decrypt_verify_noalloc(const uint8_t *key, const uint8_t *base_iv, uint64_t chain_bytes,
                                         const uint8_t *d_ct, uint64_t len, const uint8_t *d_tags,
                                         const uint8_t *d_aad, uint32_t aad_bytes, uint8_t *d_pt, uint8_t *d_ok,

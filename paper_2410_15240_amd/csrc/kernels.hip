@@ -71,10 +71,11 @@ __device__ inline void build_tab4_row(const u4 &y, int p, Tab4 *out)
 }
 
 // Key setup in two launches. key_setup_kernel (one workgroup) runs the short
-// dependent chain: the AES-256 key expansion, H = AES_K(0), the powers
-// H^1..H^65 (level by level, the products of a level spread over the waves) and
-// the squares H^(2^t). key_tables_kernel (many workgroups) then builds every
-// table from those powers, one table entry per thread.
+// dependent chain: the AES-256 key expansion, H = AES_K(0), the squares H^(2^t)
+// and the powers H^8, H^16, ..., H^64. key_tables_kernel (many workgroups) then
+// builds every table from those: one wave per table of an odd multiple
+// H^(j 2^t) (j = 3, 5, 7), which forms its element from squares first, and one
+// table row or entry per thread for the others.
 //
 // Key-independent parts come from tables the compiler evaluates: the S-box and
 // T0, and the columns of the squaring map's powers S^k, k = 1..8.
@@ -198,17 +199,47 @@ __global__ __launch_bounds__(1024) void key_setup_kernel(SetupArgs a, KeyCtx *__
             ctx->hsq[i][j] = s_hsq[i].w[j];
 }
 
-// The tables, one task per thread: a nibble position (16 entries) of the 4-bit
-// tables of H and of every H^(2^t), or one entry of the 8-bit positional tables
-// of H^8, H^16, ..., H^64:
+// The tables. First one wave per table of an odd multiple H^(j 2^t) (j = 3, 5, 7): the
+// wave forms the element as a product of squares (H^(3 . 2^t) = H^(2^t) . H^(2^(t+1)),
+// H^(5 . 2^t) = H^(2^t) . H^(2^(t+2)), H^(7 . 2^t) = H^(3 . 2^t) . H^(2^(t+2))), each a
+// linear map whose columns the wave builds, and its lanes 0..31 write the table's
+// nibble positions. These waves come first, as they have the longest path. Then one
+// task per thread: a nibble position (16 entries) of the 4-bit tables of H and of
+// every H^(2^t), or one entry of the 8-bit positional tables of H^8, H^16, ..., H^64:
 // g16[i][v][k] = (byte v at byte k) . H^(8 (i + 1)), v's bit 7 = degree 8k.
+constexpr uint32_t kOddThreads = kOddMul * kOddT * 64;
 constexpr uint32_t kTab4Tasks = (1 + kSquares) * kTab4Pos;
 constexpr uint32_t kTab8Entries = 8 * 16 * 256;
 constexpr uint32_t kTableThreads = 256;
+static_assert(kOddThreads % 64 == 0, "whole waves");
+
+__device__ inline u4 times_wave(const u4 &x, const u4 &y, uint32_t lane)   // x . y, all 64 lanes
+{
+    const u4 yb = to_be(y);
+    WaveLinear mul;
+    mul.c0 = be_mul_xk_any(yb, (int)lane);
+    mul.c1 = be_mul_xk_any(yb, (int)lane + 64);
+    return from_be(mul.apply(to_be(x), lane));
+}
 
 __global__ __launch_bounds__(kTableThreads) void key_tables_kernel(KeyCtx *__restrict__ ctx)
 {
-    const uint32_t task = blockIdx.x * kTableThreads + threadIdx.x;
+    const uint32_t g = blockIdx.x * kTableThreads + threadIdx.x;
+    if (g < kOddThreads) {   // whole waves: the branch is uniform
+        const uint32_t o = g >> 6, lane = g & 63;
+        const uint32_t i = o / kOddT, t = o % kOddT;   // j = 2 i + 3
+        auto sq = [&](uint32_t e) {   // H^(2^e); e = 32 only for the unused H^(5 . 2^30), H^(7 . 2^30)
+            const uint32_t *y = ctx->hsq[min(e, (uint32_t)kSquares - 1)];
+            return u4{{y[0], y[1], y[2], y[3]}};
+        };
+        u4 y = times_wave(sq(t), sq(t + (i == 1 ? 2u : 1u)), lane);
+        if (i == 2)
+            y = times_wave(y, sq(t + 2), lane);
+        if (lane < kTab4Pos)
+            build_tab4_row(y, (int)lane, &ctx->odd_tab[i][t]);
+        return;
+    }
+    const uint32_t task = g - kOddThreads;
     if (task < kTab4Tasks) {
         const uint32_t tbl = task / kTab4Pos, p = task % kTab4Pos;
         const uint32_t *y = tbl == 0 ? ctx->h : ctx->hsq[tbl - 1];
@@ -241,7 +272,7 @@ hipError_t launch_key_setup(const uint32_t key_words[8], KeyCtx *ctx, hipStream_
     hipError_t e = hipGetLastError();
     if (e != hipSuccess)
         return e;
-    constexpr uint32_t kTasks = kTab4Tasks + kTab8Entries;
+    constexpr uint32_t kTasks = kOddThreads + kTab4Tasks + kTab8Entries;
     hipLaunchKernelGGL(key_tables_kernel, dim3((kTasks + kTableThreads - 1) / kTableThreads), dim3(kTableThreads), 0, s,
                        ctx);
     return hipGetLastError();
@@ -409,6 +440,31 @@ __device__ __forceinline__ int wave_min_i32(int x)
     x = min(x, (int)lane_down<2>((uint32_t)x));
     x = min(x, (int)lane_down<1>((uint32_t)x));
     return (int)__builtin_amdgcn_readlane((uint32_t)x, 0);
+}
+
+// Nonzero base-8 digits of m (bit 3i of the OR of m's shifts marks digit i).
+__device__ __forceinline__ uint32_t octal_digits(uint32_t m)
+{
+    return (uint32_t)__popc((m | (m >> 1) | (m >> 2)) & 0x49249249u);
+}
+
+// The table of H^(d 2^(g + 3i)) for the lowest nonzero base-8 digit d of m, at digit
+// position i: with d = d' 2^e (d' odd), H^(d' 2^(g + 3i + e)), a square for d' = 1
+// and an odd multiple for d' = 3, 5, 7. m = 0 gives a table that is not used. The
+// exponent is below a chain's block count, so the indices stay in range (clamped
+// all the same).
+__device__ __forceinline__ const Tab4 *digit_tab(const KeyCtx *__restrict__ c, uint32_t m, uint32_t g)
+{
+    if (m == 0)
+        return &c->sq_tab[0];
+    const uint32_t i = (uint32_t)__builtin_ctz(m) / 3;
+    uint32_t d = (m >> (3 * i)) & 7u;
+    const uint32_t e = (uint32_t)__builtin_ctz(d);
+    d >>= e;
+    const uint32_t t = g + 3 * i + e;
+    if (d == 1)
+        return &c->sq_tab[min(t, (uint32_t)kSquares - 1)];
+    return &c->odd_tab[(d - 3) >> 1][min(t, (uint32_t)kOddT - 1)];
 }
 
 // X . Y where the L = 2^LL lanes of each aligned lane group hold one X (the
@@ -1031,18 +1087,18 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                     acc.w[w] = LL == 6 ? __builtin_amdgcn_readlane(acc.w[w], 0) : __shfl(acc.w[w], (int)(lane - jl), 64);
             if (SPLIT) {
                 // A chain cut into S segments: segment s carries the weight
-                // H^((S-1-s) . 2^seg_log2) inside its chain, one multiply by a
-                // square H^(2^(seg_log2+b)) per set bit b of S-1-s, shared by the
-                // item's lanes. The partials and segment 0's mask go to memory; the
-                // chain kernel sums them.
+                // H^((S-1-s) . 2^seg_log2) inside its chain, one multiply per nonzero
+                // base-8 digit of S-1-s, shared by the item's lanes (a dependent
+                // table multiply each, so at most 2 for up to 64 segments, 3 for 512).
+                // The partials and segment 0's mask go to memory; the chain kernel
+                // sums them.
                 uint32_t m = valid ? ip.S - 1 - ip.s : 0u;
-                const uint32_t rounds = wave_max_u32(__popc(m));
+                const uint32_t rounds = wave_max_u32(octal_digits(m));
                 for (uint32_t r = 0; r < rounds; ++r) {
-                    const uint32_t b = m ? (uint32_t)__builtin_ctz(m) : 0u;
-                    const u4 prod = group_mul_tab4<LL>(acc, &c->sq_tab[p.seg_log2 + b], jl);
+                    const u4 prod = group_mul_tab4<LL>(acc, digit_tab(c, m, p.seg_log2), jl);
                     if (m) {
                         acc = prod;
-                        m &= m - 1;
+                        m &= ~(7u << (3 * ((uint32_t)__builtin_ctz(m) / 3)));
                     }
                 }
                 const uint32_t src_lane = bi * G + gs;

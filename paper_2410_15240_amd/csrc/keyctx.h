@@ -20,6 +20,8 @@ namespace fastrack {
 constexpr int kTab4Pos = 32;    // nibble positions of a 128-bit operand
 constexpr int kTab4Ent = 16;    // values of a nibble
 constexpr int kSquares = 32;    // H^(2^t), t = 0..31 (chains are < 2^32 blocks)
+constexpr int kOddMul = 3;      // odd multipliers j = 3, 5, 7 of the segment weights
+constexpr int kOddT = 31;       // H^(j 2^t), t = 0..30 (3 . 2^30 < 2^32)
 
 struct Tab4 {                   // 4-bit positional multiplication table of a fixed Y:
     uint32_t e[kTab4Pos][kTab4Ent][4];   // e[p][v] = (nibble v at degrees 4p..4p+3) . Y
@@ -40,6 +42,10 @@ struct KeyCtx {
     // Horner multiplier H^L of L = 16, 32, 64 lanes per chain; g16[0..6] also weight the
     // partial sums of an item's eight-lane groups at the end of the lane combine.
     uint32_t g16[8][256][16][4];
+    // A segment weight H^(m 2^g) is applied one nonzero base-8 digit d of m at a time:
+    // H^(d 2^(g + 3i)) is a square for d = 1, 2, 4 and H^(j 2^t) with j = 3, 5, 7 otherwise
+    // (6 = 3 . 2). odd_tab[i][t]: table of H^((2 i + 3) 2^t).
+    Tab4 odd_tab[kOddMul][kOddT];
 };
 
 }  // namespace fastrack
