@@ -144,6 +144,29 @@ __device__ __forceinline__ uint32_t group_xor_sum(uint32_t x)
     return x;
 }
 
+// Segment weights H^(m 2^g), one nonzero base-8 digit of m at a time: digit d at
+// position i is the factor H^(d 2^(g + 3i)) = H^(j 2^t), with j the odd part of d
+// (1, 3, 5 or 7) and t = g + 3i + log2(d / j). The key context holds a table for
+// every such factor (squares for j = 1, odd multiples otherwise).
+__host__ __device__ constexpr uint32_t octal_digits(uint32_t m)   // nonzero base-8 digits of m
+{
+    return (uint32_t)__builtin_popcount((m | (m >> 1) | (m >> 2)) & 0x49249249u);
+}
+
+struct WeightStep {
+    uint32_t j, t;   // the factor H^(j 2^t)
+};
+
+// The factor of m's lowest nonzero digit (m > 0), which is then cleared from m.
+__host__ __device__ constexpr WeightStep weight_step(uint32_t &m, uint32_t g)
+{
+    const uint32_t i = (uint32_t)__builtin_ctz(m) / 3;
+    const uint32_t d = (m >> (3 * i)) & 7u;
+    const uint32_t e = (uint32_t)__builtin_ctz(d);
+    m &= ~(7u << (3 * i));
+    return WeightStep{d >> e, g + 3 * i + e};
+}
+
 // The columns of S^k, S(V) = V^2, for k = 1..8, in big-endian-word form:
 // c[k - 1][i] = S^k(x^i). Squaring is GF(2)-linear, so V^(2^k) is the XOR of the
 // columns of V's set degrees. Evaluated by the compiler (key-independent).

@@ -442,29 +442,13 @@ __device__ __forceinline__ int wave_min_i32(int x)
     return (int)__builtin_amdgcn_readlane((uint32_t)x, 0);
 }
 
-// Nonzero base-8 digits of m (bit 3i of the OR of m's shifts marks digit i).
-__device__ __forceinline__ uint32_t octal_digits(uint32_t m)
+// The table of a segment-weight factor H^(j 2^t) (see weight_step). The exponent
+// is below a chain's block count, so t stays in range (clamped all the same).
+__device__ __forceinline__ const Tab4 *weight_tab(const KeyCtx *__restrict__ c, const WeightStep &w)
 {
-    return (uint32_t)__popc((m | (m >> 1) | (m >> 2)) & 0x49249249u);
-}
-
-// The table of H^(d 2^(g + 3i)) for the lowest nonzero base-8 digit d of m, at digit
-// position i: with d = d' 2^e (d' odd), H^(d' 2^(g + 3i + e)), a square for d' = 1
-// and an odd multiple for d' = 3, 5, 7. m = 0 gives a table that is not used. The
-// exponent is below a chain's block count, so the indices stay in range (clamped
-// all the same).
-__device__ __forceinline__ const Tab4 *digit_tab(const KeyCtx *__restrict__ c, uint32_t m, uint32_t g)
-{
-    if (m == 0)
-        return &c->sq_tab[0];
-    const uint32_t i = (uint32_t)__builtin_ctz(m) / 3;
-    uint32_t d = (m >> (3 * i)) & 7u;
-    const uint32_t e = (uint32_t)__builtin_ctz(d);
-    d >>= e;
-    const uint32_t t = g + 3 * i + e;
-    if (d == 1)
-        return &c->sq_tab[min(t, (uint32_t)kSquares - 1)];
-    return &c->odd_tab[(d - 3) >> 1][min(t, (uint32_t)kOddT - 1)];
+    if (w.j == 1)
+        return &c->sq_tab[min(w.t, (uint32_t)kSquares - 1)];
+    return &c->odd_tab[(w.j - 3) >> 1][min(w.t, (uint32_t)kOddT - 1)];
 }
 
 // X . Y where the L = 2^LL lanes of each aligned lane group hold one X (the
@@ -1095,10 +1079,12 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                 uint32_t m = valid ? ip.S - 1 - ip.s : 0u;
                 const uint32_t rounds = wave_max_u32(octal_digits(m));
                 for (uint32_t r = 0; r < rounds; ++r) {
-                    const u4 prod = group_mul_tab4<LL>(acc, digit_tab(c, m, p.seg_log2), jl);
+                    uint32_t rest = m;
+                    const WeightStep w = m ? weight_step(rest, p.seg_log2) : WeightStep{1u, 0u};
+                    const u4 prod = group_mul_tab4<LL>(acc, weight_tab(c, w), jl);
                     if (m) {
                         acc = prod;
-                        m &= ~(7u << (3 * ((uint32_t)__builtin_ctz(m) / 3)));
+                        m = rest;
                     }
                 }
                 const uint32_t src_lane = bi * G + gs;

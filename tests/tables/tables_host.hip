@@ -1,8 +1,9 @@
 // Host build of the library's compile-time tables and set-up arithmetic for the
 // CPU tests: the S-box and T0 table that the key set-up copies, the columns of
-// the squaring map S^k (k = 1..8) that it applies to H, and the GF(2^128)
-// helpers they are made from (multiply by x^k, square), all evaluated on the
-// host from the same constexpr functions the device code uses. Only the host
+// the squaring map S^k (k = 1..8) that it applies to H, the GF(2^128) helpers
+// they are made from (multiply by x^k, square), and the split of a segment weight
+// into table factors, all evaluated on the host from the same constexpr
+// functions the device code uses. Only the host
 // pass is built (no device code runs).
 #include <stdint.h>
 #include <string.h>
@@ -59,6 +60,21 @@ void tab_mul_xk(const uint8_t *y, int k, uint8_t *out)
 void tab_square(const uint8_t *y, uint8_t *out)
 {
     store_be(be_square(load_be(y)), out);
+}
+
+// The factors H^(j[k] 2^t[k]) that weight a segment by H^(m 2^g), in the order the
+// kernel applies them; returns their count (octal_digits(m) is returned in *digits).
+int tab_weight_steps(uint32_t m, uint32_t g, uint32_t *j, uint32_t *t, uint32_t *digits)
+{
+    *digits = octal_digits(m);
+    int n = 0;
+    while (m) {
+        const WeightStep w = weight_step(m, g);
+        j[n] = w.j;
+        t[n] = w.t;
+        ++n;
+    }
+    return n;
 }
 
 }  // extern "C"

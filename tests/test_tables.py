@@ -6,7 +6,10 @@ host and checked against the CPU oracle and plain definitions:
     multiply (the GCM field of section 3.2, SP 800-38D 6.3);
   * the columns of the squaring map S^k(x^i) = (x^i)^(2^k), k = 1..8, that the key
     set-up applies to H to reach the squares H^(2^t), against repeated oracle
-    multiplies, and their linearity on random elements.
+    multiplies, and their linearity on random elements;
+  * the split of a segment weight H^(m 2^g) into table factors H^(j 2^t) (one per
+    nonzero base-8 digit of m): the exponents sum to m 2^g, every factor has a
+    table, and the product of the factors is H^(m 2^g) in the oracle's field.
 The header functions are constexpr and shared by the device code; only the host
 pass is compiled here."""
 import ctypes
@@ -36,6 +39,8 @@ def T(tmp_path_factory):
     for f in (L.tab_sbox, L.tab_frob, L.tab_mul_xk, L.tab_square):
         f.restype = None
     L.tab_mul_xk.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p]
+    L.tab_weight_steps.argtypes = [ctypes.c_uint32, ctypes.c_uint32] + [ctypes.c_void_p] * 3
+    L.tab_weight_steps.restype = ctypes.c_int
     return L
 
 
@@ -107,3 +112,53 @@ def test_squaring_map_columns(T):
             want = oracle.gf128_mul_bitserial(want, want)
             got = np.bitwise_xor.reduce(cols[k][bits.astype(bool)], axis=0)
             assert np.array_equal(got, want), k + 1
+
+
+def weight_steps(T, m, g):
+    j = np.zeros(12, np.uint32)
+    t = np.zeros(12, np.uint32)
+    d = np.zeros(1, np.uint32)
+    n = T.tab_weight_steps(m, g, p(j), p(t), p(d))
+    return [(int(a), int(b)) for a, b in zip(j[:n], t[:n])], int(d[0])
+
+
+def test_segment_weight_factors(T):
+    # every exponent a segment weight can have: m 2^g below 2^32 (a chain has fewer blocks)
+    rng = np.random.default_rng(14)
+    cases = [(m, g) for g in (0, 4, 7, 8, 10, 13) for m in range(1, 600)]
+    cases += [(int(m), g) for g in range(0, 31) for m in rng.integers(1, 1 << (32 - g), 64) if m << g < 1 << 32]
+    cases += [((1 << 32) - 1, 0), (0o7777777777, 0), (0o3333333333, 1), (6, 29), (3, 30), (1, 31), (4, 29)]
+    for m, g in cases:
+        steps, digits = weight_steps(T, m, g)
+        assert digits == sum(1 for k in range(11) if (m >> (3 * k)) & 7), (m, g)
+        assert len(steps) == digits, (m, g)
+        assert sum(j << t for j, t in steps) == m << g, (m, g)          # the factors make up the weight
+        for j, t in steps:
+            assert j in (1, 3, 5, 7), (m, g, j)
+            assert t < (32 if j == 1 else 31), (m, g, j, t)           # squares t <= 31, odd multiples t <= 30
+    # the product of the factors, each H^(j 2^t) formed as the table kernel forms it, is H^(m 2^g)
+    h = rng.integers(0, 256, 16, dtype=np.uint8)
+    sq = [h]
+    for _ in range(33):
+        sq.append(oracle.gf128_mul_bitserial(sq[-1], sq[-1]))   # sq[t] = H^(2^t)
+
+    def power(e):   # H^e by square-and-multiply over the squares
+        r = None
+        for t in range(40):
+            if (e >> t) & 1:
+                r = sq[t] if r is None else oracle.gf128_mul_bitserial(r, sq[t])
+        return r
+
+    def factor(j, t):   # H^(3 2^t) = H^(2^t) H^(2^(t+1)), H^(5 2^t) = H^(2^t) H^(2^(t+2)), H^(7 2^t) = H^(3 2^t) H^(2^(t+2))
+        if j == 1:
+            return sq[t]
+        y = oracle.gf128_mul_bitserial(sq[t], sq[t + (2 if j == 5 else 1)])
+        return oracle.gf128_mul_bitserial(y, sq[t + 2]) if j == 7 else y
+
+    for m, g in [(1, 7), (6, 7), (7, 10), (63, 8), (511, 7), (0o5307, 4), (12345, 3)]:
+        steps, _ = weight_steps(T, m, g)
+        prod = None
+        for j, t in steps:
+            f = factor(j, t)
+            prod = f if prod is None else oracle.gf128_mul_bitserial(prod, f)
+        assert np.array_equal(prod, power(m << g)), (m, g)
