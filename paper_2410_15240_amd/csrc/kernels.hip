@@ -556,6 +556,15 @@ __device__ inline void emit_tag(const GcmLaunch &p, uint64_t gchain, const u4 &t
     }
 }
 
+// Compile-time switches for the streaming kernel's iteration step: whether the
+// iteration may hold AAD blocks.
+struct AadSteps {
+    static constexpr bool value = true;
+};
+struct NoAadSteps {
+    static constexpr bool value = false;
+};
+
 // AES-256 of one block x (before the first AddRoundKey) with the streaming
 // kernel's LDS T-tables: every lane encrypts its own block. rk holds the round
 // keys of rounds 1..13 rotated by 16 bits (rk[4..55]), the others as they are.
@@ -744,7 +753,13 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
     // its iteration count in LDS and, each iteration, takes issue priority 3 while it
     // is the slowest wave of its SIMD, 2 or 1 while it leads the slowest by one or two
     // iterations, and 0 beyond that, so the four keep pace with each other.
-    volatile uint32_t *prog = reinterpret_cast<volatile uint32_t *>(lds4) + kProg;
+    // The counters are accessed through LDS-typed pointers (address space 3), with
+    // compiler barriers around the accesses in place of `volatile`: a volatile access
+    // through a generic pointer becomes a flat access followed by a wait for every
+    // outstanding global load and store of the wave, once per iteration.
+    typedef __attribute__((address_space(3))) uint32_t lds_u32;
+    typedef __attribute__((address_space(3))) v4u lds_v4u;
+    lds_u32 *prog = (lds_u32 *)(reinterpret_cast<uint32_t *>(lds4) + kProg);
     const uint32_t wslot = (uint32_t)tid >> 6;
     const uint32_t pidx = (wslot & 3) * 4 + (wslot >> 2);
     uint32_t iters_done = 0;
@@ -933,7 +948,9 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
         };
         const uint32_t k3 = rk[3] >> 24;   // key byte that meets the counter's low byte
         // Iteration k on the loaded data block d (and keystream block kv for kApplyKs).
-        auto process = [&](uint32_t k, const Slot &q, const u4 &d, const u4 &kv) {
+        // AAD: whether iteration k may hold AAD blocks (k <= kmax); a step built
+        // without them issues a fixed set of memory accesses.
+        auto process = [&](auto aad, uint32_t k, const Slot &q, const u4 &d, const u4 &kv) {
             const uint32_t t = q.t;
             u4 o;
             if constexpr (kAes) {
@@ -989,31 +1006,109 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
                         }
                     }
                 }
-                if ((int)k <= kmax && q.v < 0 && q.v >= -na)    // an AAD block in a padding slot
-                    g = aad_block(aad_c, (uint32_t)(q.v + na), p.aad_bytes);
+                if constexpr (decltype(aad)::value)
+                    if ((int)k <= kmax && q.v < 0 && q.v >= -na)    // an AAD block in a padding slot
+                        g = aad_block(aad_c, (uint32_t)(q.v + na), p.aad_bytes);
                 acc = (k == 0 && kmin == 0) ? g : ghash_step(lds, acc, g, gk);
             }
         };
-        for (uint32_t k = 0; k < Ku; ++k) {
-            {
-                const uint32_t mine = iters_done + k;
-                if (lane == 0)
-                    prog[pidx] = mine;
-                const uint4 g = reinterpret_cast<const uint4 *>(lds4)[(kProg + (pidx & ~3u)) / 4];
-                const uint32_t mn = __builtin_amdgcn_readfirstlane(min(min(g.x, g.y), min(g.z, g.w)));
-                const uint32_t lead = mine - (mn < mine ? mn : mine);
-                if (lead == 0u)
-                    __builtin_amdgcn_s_setprio(3);
-                else if (lead == 1u)
-                    __builtin_amdgcn_s_setprio(2);
-                else if (lead == 2u)
-                    __builtin_amdgcn_s_setprio(1);
-                else
-                    __builtin_amdgcn_s_setprio(0);
+        auto pace = [&](uint32_t k) {
+            const uint32_t mine = iters_done + k;
+            if (lane == 0)
+                prog[pidx] = mine;
+            asm volatile("" ::: "memory");   // the store is made, the others' counters re-read
+            const v4u g = *(const lds_v4u *)(reinterpret_cast<uint32_t *>(lds4) + kProg + (pidx & ~3u));
+            const uint32_t mn = __builtin_amdgcn_readfirstlane(min(min(g.x, g.y), min(g.z, g.w)));
+            const uint32_t lead = mine - (mn < mine ? mn : mine);
+            if (lead == 0u)
+                __builtin_amdgcn_s_setprio(3);
+            else if (lead == 1u)
+                __builtin_amdgcn_s_setprio(2);
+            else if (lead == 2u)
+                __builtin_amdgcn_s_setprio(1);
+            else
+                __builtin_amdgcn_s_setprio(0);
+        };
+        if constexpr (!kAes && kRead && !SPLIT) {
+            // No AES between a load and its use to hide the memory latency: the loads
+            // run four iterations ahead of the GHASH steps, passed along a queue of
+            // registers. Every queued load is issued unconditionally, so the wait
+            // before each use covers only the oldest one: a lane without a whole
+            // block in that slot (padding, past the item, or the chain's final partial
+            // block) reads 16 bytes of the key context instead and takes zero. The
+            // partial block, if this lane has one, is read once before the loop.
+            // The raw 16 bytes of slot k (the key context's first 16 when the slot has no
+            // whole block); whether to use them is decided where they are used, so the
+            // load itself is not made conditional.
+            auto ldq = [&](const uint8_t *base, uint32_t k) {
+                const Slot q = slot_of(k);
+                const bool whole = k < Ku && q.active && !q.partial;
+                const v4u *a = whole ? reinterpret_cast<const v4u *>(base) + q.t : reinterpret_cast<const v4u *>(c);
+                return __builtin_nontemporal_load(a);
+            };
+            auto take = [&](const Slot &q, const v4u &y, const u4 &part) {
+                return q.partial ? part : (q.active ? u4{{y.x, y.y, y.z, y.w}} : zero4());
+            };
+            u4 pd = zero4(), pk = zero4();   // this lane's partial block (data, keystream)
+            if (tail != 0 && valid && ip.e == ip.q) {
+                const int v = (int)(ip.q - 1 - ip.b) + pad;   // its slot: iteration v / L, lane v % L
+                if ((uint32_t)(v & (int)(L - 1)) == jl) {
+                    pd = load_bytes(src + 16ull * (ip.q - 1), tail);
+                    if constexpr (MODE == kApplyKs)
+                        pk = load_bytes(ksrc + 16ull * (ip.q - 1), tail);
+                }
             }
-            const Slot q = slot_of(k);
-            process(k, q, kRead ? load_block(src, q) : zero4(),
-                    MODE == kApplyKs ? load_block(ksrc, q) : zero4());
+            // Iterations that may hold AAD blocks (segment 0's first ones) run first,
+            // with their loads in line.
+            const uint32_t k0 = kmax < 0 ? 0u : min((uint32_t)kmax + 1u, Ku);
+            for (uint32_t k = 0; k < k0; ++k) {
+                pace(k);
+                const Slot q = slot_of(k);
+                process(AadSteps{}, k, q, load_block(src, q), MODE == kApplyKs ? load_block(ksrc, q) : zero4());
+            }
+            // Everything loaded so far has arrived: the queue below then waits only
+            // for its own oldest load.
+            __builtin_amdgcn_s_waitcnt(0);
+            // Queue depth: four for verification; two when a keystream block and an
+            // output store come with each block. (Items of chains cut into segments
+            // carry more state: with the queue those kernels exceed 128 VGPRs and
+            // spill, so they keep the loop below.)
+            constexpr uint32_t kAhead = MODE == kApplyKs ? 2u : 4u;
+            v4u dq[kAhead], eq[kAhead];
+#pragma unroll
+            for (uint32_t j = 0; j < kAhead; ++j) {
+                dq[j] = ldq(src, k0 + j);
+                if constexpr (MODE == kApplyKs)
+                    eq[j] = ldq(ksrc, k0 + j);
+            }
+            // Iteration k uses the slot loaded kAhead iterations earlier and refills it
+            // for iteration k + kAhead; unrolled by kAhead, so each slot stays in its
+            // registers (moving a register whose load is in flight would wait for it).
+            // The scheduling barrier keeps the steps from interleaving, which would
+            // hold several iterations' registers at once.
+            for (uint32_t k = k0; k < Ku; k += kAhead) {
+#pragma unroll
+                for (uint32_t j = 0; j < kAhead; ++j) {
+                    __builtin_amdgcn_sched_barrier(0);
+                    const uint32_t kk = k + j;
+                    if (kk < Ku) {
+                        pace(kk);
+                        const Slot q = slot_of(kk);
+                        const u4 dv = take(q, dq[j], pd), kv = MODE == kApplyKs ? take(q, eq[j], pk) : zero4();
+                        dq[j] = ldq(src, kk + kAhead);
+                        if constexpr (MODE == kApplyKs)
+                            eq[j] = ldq(ksrc, kk + kAhead);
+                        process(NoAadSteps{}, kk, q, dv, kv);
+                    }
+                }
+            }
+        } else {
+            for (uint32_t k = 0; k < Ku; ++k) {
+                pace(k);
+                const Slot q = slot_of(k);
+                process(AadSteps{}, k, q, kRead ? load_block(src, q) : zero4(),
+                        MODE == kApplyKs ? load_block(ksrc, q) : zero4());
+            }
         }
         iters_done += Ku;
         if constexpr (kGhash) {
