@@ -1029,7 +1029,7 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
             else
                 __builtin_amdgcn_s_setprio(0);
         };
-        if constexpr (!kAes && kRead && !SPLIT) {
+        if constexpr (!kAes && kRead && !(SPLIT && (MODE == kApplyKs || LL < 6))) {
             // No AES between a load and its use to hide the memory latency: the loads
             // run four iterations ahead of the GHASH steps, passed along a queue of
             // registers. Every queued load is issued unconditionally, so the wait
@@ -1069,11 +1069,12 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
             // Everything loaded so far has arrived: the queue below then waits only
             // for its own oldest load.
             __builtin_amdgcn_s_waitcnt(0);
-            // Queue depth: four for verification; two when a keystream block and an
-            // output store come with each block. (Items of chains cut into segments
-            // carry more state: with the queue those kernels exceed 128 VGPRs and
-            // spill, so they keep the loop below.)
-            constexpr uint32_t kAhead = MODE == kApplyKs ? 2u : 4u;
+            // Queue depth: four for verifying whole chains; two when a keystream block
+            // and an output store come with each block, and for 64-lane segments of
+            // split chains, whose items carry more state. (Keystream-apply on split
+            // chains and split items of 16 or 32 lanes would exceed 128 VGPRs with a
+            // queue and spill: they keep the loop below.)
+            constexpr uint32_t kAhead = (MODE == kApplyKs || SPLIT) ? 2u : 4u;
             v4u dq[kAhead], eq[kAhead];
 #pragma unroll
             for (uint32_t j = 0; j < kAhead; ++j) {
