@@ -1029,7 +1029,7 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
             else
                 __builtin_amdgcn_s_setprio(0);
         };
-        if constexpr (!kAes && kRead && !(SPLIT && (MODE == kApplyKs || LL < 6))) {
+        if constexpr (!kAes && kRead && !(SPLIT && LL < 6)) {
             // No AES between a load and its use to hide the memory latency: the loads
             // run four iterations ahead of the GHASH steps, passed along a queue of
             // registers. Every queued load is issued unconditionally, so the wait
@@ -1074,7 +1074,7 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
             // split chains, whose items carry more state. (Keystream-apply on split
             // chains and split items of 16 or 32 lanes would exceed 128 VGPRs with a
             // queue and spill: they keep the loop below.)
-            constexpr uint32_t kAhead = (MODE == kApplyKs || SPLIT) ? 2u : 4u;
+            constexpr uint32_t kAhead = SPLIT ? (MODE == kApplyKs ? 1u : 2u) : (MODE == kApplyKs ? 2u : 4u);
             v4u dq[kAhead], eq[kAhead];
 #pragma unroll
             for (uint32_t j = 0; j < kAhead; ++j) {
