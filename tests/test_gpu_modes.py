@@ -137,6 +137,33 @@ def test_apply_verify_matches_oracle(F, length, chain, abytes):
         assert got[0] == 7 and got[n - 1] == 7                # chains outside the run untouched
 
 
+# Launches of whole chains (no segments) with 16-, 32- and 64-lane items: the verify and
+# keystream-apply kernels then queue their loads four (apply: two) iterations ahead. The
+# last chain ends in a partial block; 32-byte AAD puts AAD blocks in the first iterations.
+WHOLE_SHAPES = [(16384 * 4096 - 9, 4096), (8192 * 8192 - 3, 8192), (4096 * 16384 - 15, 16384)]
+
+
+@pytest.mark.parametrize("length,chain", WHOLE_SHAPES)
+def test_verify_and_apply_whole_chains(F, length, chain):
+    import torch
+    say("whole-chain verify/apply", length, chain)
+    w, aad, ct, tags, want_pt, want_ok = tampered_case(chain + 3, length, chain, 32)
+    n = tags.shape[0]
+    W.flip_bit(ct, 8 * (length - 2))                          # the last chain's partial block
+    W.flip_bit(ct, 8 * (chain * (n // 2) + 16 * 7) + 3)       # a block in a middle chain
+    want_pt, want_ok = oracle.chains_decrypt(w.key, w.base_iv, chain, ct, tags, aad, 32)
+    assert (want_ok == 0).sum() >= 4
+    d_ct, d_tags, d_aad = dev(ct), dev(tags), dev(aad)
+    e = F.decrypt_eager(w.key, w.base_iv, chain, d_ct, d_tags, d_aad)
+    torch.cuda.synchronize()
+    assert np.array_equal(e.plaintext.cpu().numpy(), want_pt)
+    assert e.rejected() == np.nonzero(want_ok == 0)[0].tolist()
+    ks = F.keystream(w.key, w.base_iv, chain, length)
+    pt, ok = F.apply_verify(w.key, w.base_iv, chain, d_ct, ks, d_tags, d_aad)
+    assert np.array_equal(host(pt), want_pt)
+    assert np.array_equal(host(ok), want_ok)
+
+
 @pytest.mark.parametrize("mode,depth", [(1, 2), (1, 3), (1, 8), (2, 2), (2, 3), (0, 0), (0, 2), (0, 8), (3, 0)])
 def test_pipeline_modes_small(F, mode, depth):
     import torch
