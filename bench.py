@@ -541,16 +541,22 @@ def extras(F, W, torch, np, dev, stream, args):
     log("ragged:", res["ragged"])
     del p6, a6, c6, t6, o6, k6, cu, tu, ku
 
-    # per-key setup (first call with a new key)
-    key2 = bytes(range(32))
+    # per-key setup: the first call with a new key (key set-up, tables, 1 MiB decrypt of 16
+    # chains), the median over five keys never used before, each call after an idle GPU
     t = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     ct1, tg1 = F.encrypt_tag(w1.key, w1.base_iv, 65536, p1)
-    torch.cuda.synchronize()
-    t[0].record(stream)
-    F.decrypt_verify(key2, w1.base_iv, 65536, ct1, tg1)
-    t[1].record(stream)
-    torch.cuda.synchronize()
-    res["cold_key_call_us"] = round(t[0].elapsed_time(t[1]) * 1e3, 1)
+    o1c = torch.empty_like(ct1)
+    k1c = torch.empty(tg1.shape[0], dtype=torch.uint8, device=dev)
+    cold = []
+    for i in range(5):
+        key2 = bytes((7 * i + j) & 255 for j in range(32))
+        torch.cuda.synchronize()
+        t[0].record(stream)
+        F.decrypt_verify(key2, w1.base_iv, 65536, ct1, tg1, out=o1c, ok=k1c)
+        t[1].record(stream)
+        torch.cuda.synchronize()
+        cold.append(t[0].elapsed_time(t[1]) * 1e3)
+    res["cold_key_call_us"] = round(sorted(cold)[len(cold) // 2], 1)
 
     if not args.skip_pipeline:
         res["pipeline_h2d"] = pipeline(F, W, torch, np, dev)
