@@ -1031,15 +1031,14 @@ __global__ __launch_bounds__(kThreads, gcm_wgs_per_cu(MODE) * kWavesPerWg / 4) v
         };
         if constexpr (!kAes && kRead && !(SPLIT && LL < 6)) {
             // No AES between a load and its use to hide the memory latency: the loads
-            // run four iterations ahead of the GHASH steps, passed along a queue of
+            // run up to four iterations ahead of the GHASH steps, in a queue of
             // registers. Every queued load is issued unconditionally, so the wait
-            // before each use covers only the oldest one: a lane without a whole
-            // block in that slot (padding, past the item, or the chain's final partial
-            // block) reads 16 bytes of the key context instead and takes zero. The
-            // partial block, if this lane has one, is read once before the loop.
-            // The raw 16 bytes of slot k (the key context's first 16 when the slot has no
-            // whole block); whether to use them is decided where they are used, so the
-            // load itself is not made conditional.
+            // before each use covers only the oldest one: ldq returns the raw 16 bytes
+            // of slot k, or of the key context when the slot holds no whole block
+            // (padding, past the item, or the chain's final partial block), and take()
+            // decides at the use whether they count, so the load itself is never made
+            // conditional. The partial block, if this lane has one, is read before
+            // the loop.
             auto ldq = [&](const uint8_t *base, uint32_t k) {
                 const Slot q = slot_of(k);
                 const bool whole = k < Ku && q.active && !q.partial;
